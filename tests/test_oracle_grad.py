@@ -1,0 +1,167 @@
+"""Pins of the oracle's pose gradient (Eq. 2 and Eq. 3 of the paper) against
+central finite differences of its own loss in double precision, with the
+sample set frozen, plus the ground-truth and structural invariants.  CPU only.
+
+A finite-difference case is valid only if no discrete decision (hash cell,
+ReLU sign, Huber branch, clamp, early-stop index) changes between the three
+evaluations; the oracle reports a signature of all decisions, and cases whose
+signature moves are skipped (and counted)."""
+import dataclasses
+import math
+
+import numpy as np
+import pytest
+from scipy.spatial.transform import Rotation
+
+from paper_2210_10108_amd import synth
+
+H = 1e-8
+
+
+def setup_case(spec_kw=None, K=2, P=8, seed=0, pix_seed=0):
+    w = synth.WORKLOADS["tiny32"]
+    spec = synth.field_spec(w, synth.make_field(w, seed), **(spec_kw or {}))
+    gt = synth.ground_truth_pose(w, seed)
+    intr = synth.intrinsics(w)
+    rng = np.random.default_rng([pix_seed, 11])
+    # pixels near the image centre so that most rays cross the box
+    u = rng.integers(8, 24, size=(K, P))
+    v = rng.integers(8, 24, size=(K, P))
+    pix = (v * w.width + u).astype(np.int32)
+    poses = synth.perturb_poses(gt, K, 8.0, 0.05, seed)
+    return w, spec, gt, intr, pix, poses
+
+
+def observe(of, gt, pix, intr):
+    """Observation = the oracle's own rendering at the ground-truth pose."""
+    obs = np.zeros((intr["height"], intr["width"], 3), np.float32)
+    flat = np.unique(pix.ravel())
+    rgb = of.render(gt[None], flat[None], intr)[0]
+    obs.reshape(-1, 3)[flat] = rgb
+    return obs
+
+
+def ray_dirs64(poses64, pix, intr):
+    K, P = pix.shape
+    out = np.zeros((K * P, 3))
+    for k in range(K):
+        R = poses64[k, :, :3]
+        for s in range(P):
+            p = pix[k, s]
+            u, v = p % intr["width"], p // intr["width"]
+            dc = np.array([(u + 0.5 - intr["cx"]) / intr["fx"], (v + 0.5 - intr["cy"]) / intr["fy"], 1])
+            d = R @ dc
+            out[k * P + s] = d / np.linalg.norm(d)
+    return out
+
+
+def perturbed(poses64, k, comp, h):
+    p = poses64.copy()
+    if comp < 3:
+        e = np.zeros(3)
+        e[comp] = h
+        p[k, :, :3] = Rotation.from_rotvec(e).as_matrix() @ p[k, :, :3]
+    else:
+        p[k, comp - 3, 3] += h
+    return p
+
+
+def fd_check(of, poses, pix, obs, intr, sh_dirs=None, h=H, min_checked=8):
+    m = of.march(poses, pix, intr)
+    p64 = poses.astype(np.float64)
+    base = of.shade(p64, pix, obs, intr, m, sh_dirs=sh_dirs, threads=1)
+    K = pix.shape[0]
+    checked = skipped = 0
+    for k in range(K):
+        for comp in range(6):
+            up = of.shade(perturbed(p64, k, comp, h), pix, obs, intr, m, sh_dirs=sh_dirs, threads=1)
+            dn = of.shade(perturbed(p64, k, comp, -h), pix, obs, intr, m, sh_dirs=sh_dirs, threads=1)
+            if not (up["signature"] == dn["signature"] == base["signature"]):
+                skipped += 1
+                continue
+            fd = (up["loss"][k] - dn["loss"][k]) / (2 * h)
+            an = base["dpose"][k, comp]
+            scale = np.abs(base["dpose"][k]).max()
+            assert abs(fd - an) <= 1e-6 * scale + 1e-13, (k, comp, fd, an)
+            checked += 1
+    assert checked >= min_checked, (checked, skipped)
+    return base
+
+
+@pytest.mark.parametrize("bg", [(0.0, 0.0, 0.0), (0.2, 0.4, 0.6)])
+def test_gradient_fd_full_direction_path(oracle_lib, bg):
+    w, spec, gt, intr, pix, poses = setup_case(dict(background=bg, sh_dir_grad=1))
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    base = fd_check(of, poses, pix, obs, intr)
+    assert np.all(base["loss"] > 0)
+
+
+def test_gradient_fd_literal_eq3_frozen_view_direction(oracle_lib):
+    # sh_dir_grad=0 is the torque of Eq. 3 alone: the view-direction input of
+    # the colour network is held fixed, so finite differences must hold it too
+    w, spec, gt, intr, pix, poses = setup_case(dict(sh_dir_grad=0), seed=1, pix_seed=1)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    dirs = ray_dirs64(poses.astype(np.float64), pix, intr)
+    fd_check(of, poses, pix, obs, intr, sh_dirs=dirs)
+    # and the two gradients differ exactly by the direction path
+    spec1 = dataclasses.replace(spec, sh_dir_grad=1)
+    g0 = of.render_loss_grad(poses, pix, obs, intr)["dpose"]
+    g1 = oracle_lib.OracleField(spec1).render_loss_grad(poses, pix, obs, intr)["dpose"]
+    assert np.allclose(g0[:, 3:], g1[:, 3:], atol=1e-15)
+    assert not np.allclose(g0[:, :3], g1[:, :3])
+
+
+def test_gradient_fd_lattice_occupancy_early_stop(oracle_lib):
+    # dense field (bias +3) so that transmittance drops below t_stop inside the box
+    R = 16
+    occ = synth.occupancy_pattern("sphere", R)
+    kw = dict(march_mode=1, step=math.sqrt(3) / 96, max_samples=200, t_stop=1e-2, occ_res=R,
+              occ_bits=occ, density_bias=3.0, background=(1.0, 1.0, 1.0), sh_dir_grad=1)
+    w, spec, gt, intr, pix, poses = setup_case(kw, seed=2, pix_seed=2)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    m = of.march(poses, pix, intr)
+    out = of.shade(poses.astype(np.float64), pix, obs, intr, m)
+    counts = np.diff(m[0])
+    assert np.any(out["stop"] < counts)          # early stop fires on some rays
+    fd_check(of, poses, pix, obs, intr)
+
+
+def test_zero_loss_and_gradient_at_ground_truth(oracle_lib):
+    w, spec, gt, intr, pix, _ = setup_case(dict(sh_dir_grad=1), K=3, P=64)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    out = of.render_loss_grad(np.repeat(gt[None], 3, 0), pix, obs, intr)
+    assert np.all(out["loss"] < 1e-14)
+    assert np.abs(out["dpose"]).max() < 1e-9
+    # away from the ground truth the loss is clearly positive
+    poses = synth.perturb_poses(gt, 3, 10, 0.05, 4)
+    assert np.all(of.render_loss_grad(poses, pix, obs, intr)["loss"] > 1e-6)
+
+
+@pytest.mark.parametrize("sh_dir_grad", [0, 1])
+def test_torque_perpendicular_to_single_ray(oracle_lib, sh_dir_grad):
+    w, spec, gt, intr, pix, poses = setup_case(dict(sh_dir_grad=sh_dir_grad), K=2, P=1)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    out = of.render_loss_grad(poses, pix, obs, intr)
+    d = ray_dirs64(poses.astype(np.float64), pix, intr)
+    for k in range(2):
+        tau = out["dpose"][k, :3]
+        assert abs(tau @ d[k]) <= 1e-12 * max(np.linalg.norm(tau), 1e-30)
+
+
+def test_hypotheses_are_independent_and_thread_count_invariant(oracle_lib):
+    w, spec, gt, intr, pix, poses = setup_case(K=3, P=32)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    a = of.render_loss_grad(poses, pix, obs, intr, threads=1)
+    poses2 = poses.copy()
+    poses2[1] = synth.perturb_poses(gt, 1, 20, 0.1, 9)[0]
+    b = of.render_loss_grad(poses2, pix, obs, intr, threads=4)
+    for k in (0, 2):
+        assert a["loss"][k] == b["loss"][k]
+        assert np.array_equal(a["dpose"][k], b["dpose"][k])
+    assert a["loss"][1] != b["loss"][1]
