@@ -1,0 +1,212 @@
+"""Throughput of the pose-inversion hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch: render -> Huber loss
+-> pose gradient for K hypotheses (pnerf_render_loss_grad), the momentum update
+(pnerf_step_momentum) and, at the workload's resampling interval, Monte Carlo
+resampling (pnerf_resample_hypotheses).  Inputs (field, observation, pixel
+batches, poses) are resident in HBM before timing starts.
+
+Prints one JSON line.  value = ray-samples/s (samples composited and
+back-propagated to the pose gradient, summed over the timed steps, divided by
+the timed wall time).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2210_10108_amd import synth  # noqa: E402
+
+PEAK_FP32_MFMA = 157.3e12     # dense fp32 MFMA, FLOP/s
+PEAK_HBM = 8.0e12             # bytes/s
+# algorithmic multiply-accumulates per sample (input-gradient only, frozen field):
+# density fwd 32*64 + 64*16, colour fwd 15*64 + 64*64 + 64*3 (+ SH rows 16*64 per ray),
+# and the same layers transposed backward (colour 3*64 + 64*64 + 64*15, density 16*64 + 64*32)
+MAC_FWD = 3072 + 5312
+MAC_BWD = 5248 + 3072
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="ngp800_uniform", choices=synth.ORDER)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    return ap.parse_args()
+
+
+def render_observation(field, w, gt, dev):
+    """Observed image = the field rendered at the ground-truth pose (HIP path)."""
+    import torch
+    n = w.width * w.height
+    out = torch.empty(n, 3, dtype=torch.float32, device=dev)
+    chunk = 1 << 16
+    pose = torch.from_numpy(gt[None]).to(dev)
+    intr = synth.intrinsics(w)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        ids = torch.arange(s, e, dtype=torch.int32, device=dev)[None]
+        out[s:e] = field.render(pose, ids, intr)[0]
+    return out.reshape(w.height, w.width, 3)
+
+
+def cpu_baseline(w, spec, gt, poses, pix, budget_s):
+    """The oracle, untuned, on a bounded sample of the same workload: whole
+    hypotheses (all their pixels) until about `budget_s` seconds of work."""
+    from oracle import oracle as O
+    of = O.OracleField(spec)
+    threads = O.n_threads_default()
+    intr = synth.intrinsics(w)
+    # oracle's own observation at the sampled pixels (untimed)
+    done_s, samples, hyps = 0.0, 0, 0
+    k = 0
+    while done_s < budget_s and k < w.K:
+        obs = np.zeros((w.height, w.width, 3), np.float32)
+        flat = np.unique(pix[k])
+        obs.reshape(-1, 3)[flat] = of.render(gt[None], flat[None].astype(np.int32), intr,
+                                             threads=threads)[0]
+        t0 = time.perf_counter()
+        out = of.render_loss_grad(poses[k:k + 1], pix[k:k + 1], obs, intr, threads=threads)
+        done_s += time.perf_counter() - t0
+        samples += int(out["march"][0][-1])
+        hyps += 1
+        k += 1
+    return {"value": samples / done_s, "unit": "ray-samples/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{hyps} of {w.K} hypotheses x {w.P} pixels of the first batch "
+                      f"({samples} samples, {done_s:.1f} s, fp64 oracle, {threads} threads)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path shards "
+              "over hypotheses but no multi-GPU run is built", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2210_10108_amd import pnerf
+
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS[args.workload]
+    fa = synth.make_field(w, args.seed)
+    spec = synth.field_spec(w, fa)        # occupancy (if any) built on the device
+    field = pnerf.Field(spec)
+    gt = synth.ground_truth_pose(w, args.seed)
+    obs = render_observation(field, w, gt, dev)
+    poses0 = synth.perturb_poses(gt, w.K, w.max_rot_deg, w.max_trans, args.seed)
+    n_batches = 8
+    pix_host = [synth.pixel_batch(args.seed, i, w.K, w.P, w.width, w.height)
+                for i in range(n_batches)]
+    pix = [torch.from_numpy(p).to(dev) for p in pix_host]
+    intr = synth.intrinsics(w)
+    K = w.K
+    loss = torch.empty(K, dtype=torch.float32, device=dev)
+    dpose = torch.empty(K, 6, dtype=torch.float32, device=dev)
+    sr = math.radians(w.resample_sigma_rot_deg)
+
+    def run(n_steps, start, poses, mom, count=False, counts=None):
+        for i in range(start, start + n_steps):
+            field.render_loss_grad(poses, pix[i % n_batches], obs, intr, loss, dpose)
+            if count:
+                counts.append(field.last_sample_count())
+            pnerf.step_momentum(poses, mom, dpose, w.lr, w.beta)
+            if w.resample_every and (i + 1) % w.resample_every == 0:
+                pnerf.resample_hypotheses(poses, mom, loss, w.keep_frac, sr,
+                                          w.resample_sigma_trans, args.seed,
+                                          (i + 1) // w.resample_every)
+
+    def fresh():
+        return (torch.from_numpy(poses0.copy()).to(dev),
+                torch.zeros(K, 6, dtype=torch.float32, device=dev))
+
+    W, S = args.warmup, args.steps
+    # sample counts of the timed steps (deterministic replay, synchronising per step)
+    poses, mom = fresh()
+    counts = []
+    run(W + S, 0, poses, mom, count=True, counts=counts)
+    timed_samples = int(sum(counts[W:]))
+
+    # timed run
+    poses, mom = fresh()
+    run(W, 0, poses, mom)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run(S, W, poses, mom)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    # per-kernel HIP-event timing over an identical pass
+    poses, mom = fresh()
+    run(W, 0, poses, mom)
+    field.set_profiling(True)
+    run(S, W, poses, mom)
+    torch.cuda.synchronize()
+    prof = {name: {"launches": n, "avg_ms": ms / max(n, 1)} for name, n, ms in field.profile()}
+    field.set_profiling(False)
+
+    samples_per_step = timed_samples / S
+    dom = max(prof.items(), key=lambda kv: kv[1]["avg_ms"] * kv[1]["launches"])
+    dom_name, dom_v = dom
+    if dom_name == "shade_fwd":
+        ach = samples_per_step * 2 * MAC_FWD / (dom_v["avg_ms"] * 1e-3)
+    elif dom_name == "shade_bwd":
+        ach = samples_per_step * 2 * MAC_BWD / (dom_v["avg_ms"] * 1e-3)
+    else:
+        ach = float("nan")
+    roof = {"kernel": dom_name, "bound": "mfma", "achieved": ach / 1e12, "peak": PEAK_FP32_MFMA / 1e12,
+            "unit": "TFLOP/s", "frac": ach / PEAK_FP32_MFMA, "traffic": None,
+            "avg_ms": dom_v["avg_ms"],
+            "flops_per_sample": 2 * (MAC_FWD if dom_name == "shade_fwd" else MAC_BWD)}
+    gather_bytes = 8 * w.n_levels * w.n_features * (2 if w.param_dtype == "f16" else 4)
+    enc = {}
+    for kname in ("shade_fwd", "shade_bwd"):
+        if kname in prof:
+            gbs = samples_per_step * gather_bytes / (prof[kname]["avg_ms"] * 1e-3)
+            enc[kname] = {"gather_GBps": gbs / 1e9, "frac_hbm": gbs / PEAK_HBM}
+
+    res = {
+        "metric": "ray-samples/sec fwd+bwd to pose grads",
+        "value": timed_samples / elapsed,
+        "unit": "ray-samples/s",
+        "n_gpus": 1,
+        "steps": S,
+        "warmup": W,
+        "ms_per_step": elapsed / S * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded random frozen field; observation rendered at a seeded ground-truth pose)",
+        "config": {"workload": w.name, "K": K, "P": w.P, "levels": w.n_levels,
+                   "table": f"2^{w.log2_table}", "image": f"{w.width}x{w.height}",
+                   "sampling": "uniform" if w.march_mode == 0 else "lattice+occupancy",
+                   "parallelism": "single-gpu"},
+        "hypothesis_iters_per_sec": K * S / elapsed,
+        "samples_per_step": samples_per_step,
+        "mean_samples_per_ray": samples_per_step / w.n_rays,
+        "roofline": roof,
+        "encoding_gather": enc,
+        "kernels_avg_ms": {k: v["avg_ms"] for k, v in prof.items()},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, spec if spec.occ_res == 0 else None, gt,
+                                           poses0, pix_host[W % n_batches], args.cpu_seconds) \
+            if spec.occ_res == 0 else None
+    field.close()
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

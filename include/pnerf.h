@@ -1,0 +1,211 @@
+/*
+ * pnerf.h -- C ABI of the MI355X (gfx950) hot path of parallel NeRF inversion
+ * for pose estimation (Lin et al., "Parallel Inversion of Neural Radiance
+ * Fields for Robust Pose Estimation", arXiv 2210.10108).
+ *
+ * Problem (Sec. III, iNeRF's formulation): the field Theta is trained and
+ * frozen, intrinsics are known, and the camera pose T is updated iteratively to
+ * minimise a photometric loss between the field's rendering and the observed
+ * image.  This library evaluates, for K pose hypotheses at once (Sec. IV-B),
+ * the loss and its gradient split into a rotation part (the torque of Eq. 3)
+ * and a translation part (the force of Eq. 2), applies the momentum update on
+ * SO(3) x T(3) (Sec. IV-A), and resamples hypotheses (Sec. IV-B).
+ *
+ * Conventions shared by every entry point
+ *  - Poses are camera-to-world float32 [K][3][4] = [R | o], row major: o is the
+ *    camera centre and the origin of every ray (Sec. IV-A).  Camera axes:
+ *    x right, y down, z forward; pixel (u, v) has its centre at (u+0.5, v+0.5).
+ *  - Pose gradients and momenta are float32 [K][6] = (w_x, w_y, w_z, t_x, t_y,
+ *    t_z): w is the gradient w.r.t. a rotation Exp(w) R applied about the
+ *    camera centre in world axes, t the gradient w.r.t. o.
+ *  - Array arguments marked (device) are device pointers owned by the caller;
+ *    they must stay valid until the work queued on `stream` has finished.
+ *    Arguments marked (host) are read before the call returns.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *    enqueues work on it and returns without synchronising, except
+ *    pnerf_create_field and the pnerf_field_* queries, which synchronise it.
+ *  - Arguments are validated on the host before anything is enqueued; a
+ *    failed validation returns PNERF_ERR_INVALID_ARG (or NOT_SUPPORTED) and
+ *    enqueues nothing.  HIP errors map to PNERF_ERR_DEVICE.  The message of
+ *    the last failure on the calling thread is pnerf_last_error().
+ *  - A field is not safe for concurrent calls from several threads; calls on
+ *    one field must be ordered (one stream, or externally synchronised).
+ */
+#ifndef PNERF_H
+#define PNERF_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PNERF_OK = 0,
+  PNERF_ERR_INVALID_ARG = 1,
+  PNERF_ERR_OUT_OF_MEMORY = 2,
+  PNERF_ERR_DEVICE = 3,
+  PNERF_ERR_CAPACITY = 4,
+  PNERF_ERR_NOT_SUPPORTED = 5
+} pnerf_status;
+
+typedef struct pnerf_field pnerf_field; /* opaque; owns device copies + workspace */
+
+/* Pinhole intrinsics of the observed image (Sec. III: intrinsics are known). */
+typedef struct {
+  int32_t width, height;
+  float fx, fy, cx, cy;
+} pnerf_intrinsics;
+
+/* A frozen Instant-NGP-style field (Sec. III, "Instant NGP") and how its rays
+ * are sampled.  All pointers are host pointers, deep-copied by create_field.
+ *
+ * Encoding: L levels of a multiresolution grid; level l has resolution
+ * level_res[l] (vertices 0..N_l per axis) and a table of T = 2^log2_table_size
+ * entries of F = 2 features.  A level whose (N_l+1)^3 vertices fit in T is
+ * indexed 1:1 (i + j(N_l+1) + k(N_l+1)^2) when dense_coarse_levels = 1,
+ * otherwise by the spatial hash (i ^ j*2654435761 ^ k*805459861) mod T.  A
+ * point p maps to x = clamp((p - aabb_min) / extent, 0, 1) and on level l to
+ * the cell whose lower vertex is min(floor(x N_l), N_l - 1); its feature is the
+ * trilinear blend of the 8 vertex entries.  Features concatenate level-major.
+ *
+ * Networks (no biases; weights stored [in][out], out = in @ W):
+ *   density: a = relu(feat @ W_d1) (64), h = a @ W_d2 (16), sigma = exp(h_0 + density_bias)
+ *   colour:  x_c = [h_1..h_15, SH_16(d), 0] (32), b1 = relu(x_c @ W_c1) (64),
+ *            b2 = relu(b1 @ W_c2) (64), rgb = sigmoid(b2 @ W_c3) (3)
+ * SH_16 are the real orthonormal spherical harmonics of degree 0..3 of the unit
+ * ray direction, ordered by l then m = -l..l, without the Condon-Shortley phase.
+ *
+ * Sampling (Sec. IV-A ray model p_i = o + t_i d): the ray is clipped to the box
+ * (t >= 0).  march_mode 0: n_uniform midpoints of equal segments of
+ * [t_near, t_far], spacing delta = (t_far - t_near) / n_uniform.  march_mode 1:
+ * lattice t_j = t_near + (j + 1/2) step below t_far, spacing step, at most
+ * max_samples kept.  With occ_res > 0 a sample is kept only if its cell of the
+ * occ_res^3 occupancy grid (index x + R(y + Rz), LSB-first uint32 words) is
+ * set; occ_bits = NULL builds the grid on the device (bit set iff sigma at the
+ * cell centre > occ_threshold).  Compositing is front to back with background
+ * colour `background`; when t_stop > 0 a ray stops after the first sample whose
+ * outgoing transmittance is below t_stop.
+ *
+ * Loss (Sec. IV-C): loss_type 0 = Huber with threshold loss_param on each
+ * channel residual, averaged over the P pixels and 3 channels of a hypothesis.
+ * sh_dir_grad 0 gives the torque of Eq. 3 alone; 1 also carries the gradient
+ * through the view-direction input of the colour network. */
+typedef struct {
+  int32_t n_levels;             /* L: 4, 8, 12 or 16 */
+  int32_t n_features;           /* F: must be 2 */
+  int32_t log2_table_size;      /* 4..24 */
+  const int32_t* level_res;     /* [L] N_l >= 1 */
+  int32_t dense_coarse_levels;  /* 0 or 1 */
+  int32_t param_dtype;          /* 0: float32, 1: float16 table and weights */
+  const void* table;            /* [L][T][2] */
+  const void* w_density1;       /* [2L][64] */
+  const void* w_density2;       /* [64][16] */
+  const void* w_color1;         /* [32][64] */
+  const void* w_color2;         /* [64][64] */
+  const void* w_color3;         /* [64][3] */
+  float density_bias;
+  float aabb_min[3], aabb_max[3];
+  int32_t march_mode;           /* 0 uniform, 1 lattice */
+  int32_t n_uniform;            /* mode 0: samples per ray, 1..4096 */
+  float step;                   /* mode 1: lattice spacing > 0 */
+  int32_t max_samples;          /* mode 1: cap on kept samples per ray, 1..8192 */
+  float t_stop;                 /* 0 = off */
+  int32_t occ_res;              /* 0 = no occupancy grid, else 1..1024 */
+  const uint32_t* occ_bits;     /* ceil(R^3/32) words, or NULL (build on device) */
+  float occ_threshold;
+  float background[3];
+  int32_t loss_type;            /* 0 = Huber */
+  float loss_param;             /* Huber threshold > 0 */
+  int32_t sh_dir_grad;          /* 0 or 1 */
+  int64_t max_workspace_bytes;  /* sample-buffer budget; 0 = 16 GiB.  Larger
+                                   batches are processed in hypothesis chunks. */
+} pnerf_field_params;
+
+/* Create a field: validates `params`, copies every array to the device (builds
+ * the occupancy grid when asked), and synchronises `stream`.  On success *out
+ * owns all device memory until pnerf_destroy_field. */
+pnerf_status pnerf_create_field(const pnerf_field_params* params, void* stream,
+                                pnerf_field** out);
+/* Release a field (waits for its outstanding work).  NULL is a no-op. */
+void pnerf_destroy_field(pnerf_field* field);
+
+/* The hot path (Sec. IV-A, Eq. 2 and Eq. 3; Sec. IV-C): for every hypothesis
+ * k < K and pixel slot s < P, render pixel pixel_ids[k][s] from poses[k],
+ * take the loss against observed[v][u][0..2], and back-propagate through the
+ * composite, both networks, the trilinear encoding and the sample positions
+ * (the t_i, the sample set and the stop index are held fixed) to
+ *   loss[k]     = (1 / 3P) sum_s sum_c H(C_c - I_c)
+ *   dpose[k]    = (tau, g) with g = sum_rays sum_i dL/dp_i        (Eq. 2)
+ *                 and tau = sum_rays d x sum_i t_i dL/dp_i         (Eq. 3)
+ *                 (+ sum_rays d x dL/dd through SH when sh_dir_grad = 1)
+ * poses (device) [K][3][4]; pixel_ids (device) int32 [K][P], each in [0, W*H);
+ * observed (device) float32 [H][W][3]; loss (device) [K]; dpose (device) [K][6].
+ * Limits: K >= 1, P >= 1, K*P < 2^31, pixel ids in range (not checked on the
+ * device: out-of-range ids are undefined behaviour). */
+pnerf_status pnerf_render_loss_grad(pnerf_field* field, int32_t K, const float* poses,
+                                    int32_t P, const int32_t* pixel_ids,
+                                    const float* observed, const pnerf_intrinsics* intr,
+                                    float* loss, float* dpose, void* stream);
+
+/* Momentum step on SO(3) x T(3) (Sec. IV-A; vector moments): for each k,
+ * m <- beta m + dpose, R <- Exp(-lr m_w) R, o <- o - lr m_t, in place.
+ * poses (device) [K][3][4], momentum (device) [K][6], dpose (device) [K][6]. */
+pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum,
+                                 const float* dpose, float lr, float beta, void* stream);
+
+/* Monte Carlo resampling (Sec. IV-B): rank hypotheses by loss (ascending, ties
+ * by index, NaN last), keep n_keep = max(1, floor(K keep_frac)), and redraw
+ * each other slot -- the i-th one in ascending slot order takes the kept
+ * hypothesis of rank i mod n_keep as parent -- as R = Exp(w) R_parent,
+ * o = o_parent + v with w ~ N(0, sigma_rot^2 I), v ~ N(0, sigma_trans^2 I);
+ * redrawn momenta restart at 0.  The normals of slot s come from the SplitMix64
+ * stream started at seed ^ mix(round << 32 | s) (mix = SplitMix64's output
+ * function), uniforms ((u >> 11) + 1/2) 2^-53, Box-Muller on pairs, in the
+ * order w_x, w_y, w_z, v_x, v_y, v_z.  In place; 1 <= K <= 65535. */
+pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
+                                       const float* loss, float keep_frac,
+                                       float sigma_rot, float sigma_trans, uint64_t seed,
+                                       uint32_t round_idx, void* stream);
+
+/* Forward rendering only (the composite colour of each pixel's ray).
+ * rgb (device) float32 [K][P][3]. */
+pnerf_status pnerf_render(pnerf_field* field, int32_t K, const float* poses, int32_t P,
+                          const int32_t* pixel_ids, const pnerf_intrinsics* intr,
+                          float* rgb, void* stream);
+
+/* The sample set of pnerf_render_loss_grad (rays ordered k*P + s, samples by
+ * increasing t).  ray_offset (device) int64 [K*P+1] receives exclusive offsets
+ * (total in ray_offset[K*P]).  If the total fits in `capacity`, t (device)
+ * float32 and lattice_j (device) int32 [capacity] receive each sample's
+ * distance and lattice / segment index; otherwise only ray_offset is written
+ * and the call still returns PNERF_OK (compare the total with capacity).
+ * Requires the batch to fit one workspace chunk (else PNERF_ERR_CAPACITY). */
+pnerf_status pnerf_march(pnerf_field* field, int32_t K, const float* poses, int32_t P,
+                         const int32_t* pixel_ids, const pnerf_intrinsics* intr,
+                         int64_t* ray_offset, float* t, int32_t* lattice_j, int64_t capacity,
+                         void* stream);
+
+/* Copy the field's occupancy grid to `bits_host` (ceil(R^3/32) words);
+ * synchronises `stream`.  PNERF_ERR_INVALID_ARG if the field has no grid. */
+pnerf_status pnerf_field_occupancy(pnerf_field* field, uint32_t* bits_host, void* stream);
+
+/* Total number of samples processed by the last render_loss_grad / render /
+ * march call on this field (sum over hypothesis chunks); synchronises `stream`. */
+pnerf_status pnerf_field_last_sample_count(pnerf_field* field, int64_t* count, void* stream);
+
+/* Per-kernel timing with HIP events recorded on the call's stream around every
+ * kernel the field launches.  enable = 1 starts (and clears) collection, 0 stops.
+ * pnerf_field_profile_read synchronises the device and returns, for kernel
+ * number `index` (0-based, in launch order of first appearance), its name,
+ * number of launches and total milliseconds; PNERF_ERR_INVALID_ARG past the end. */
+pnerf_status pnerf_field_set_profiling(pnerf_field* field, int32_t enable);
+pnerf_status pnerf_field_profile_read(pnerf_field* field, int32_t index, const char** name,
+                                      int64_t* launches, double* total_ms);
+
+/* Message of the last non-OK status returned on this thread ("" if none). */
+const char* pnerf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -87,7 +87,13 @@ def _p(a: np.ndarray | None):
 
 
 def n_threads_default() -> int:
-    return max(1, len(os.sched_getaffinity(0)))
+    """Host threads for the oracle: the process's CPU affinity, capped by
+    OMP_NUM_THREADS when that is set."""
+    n = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n)
 
 
 def intr_struct(intr: dict) -> _Intr:

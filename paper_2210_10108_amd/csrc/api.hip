@@ -1,0 +1,658 @@
+// C ABI (include/pnerf.h): field creation with MFMA weight-tile layout,
+// workspace management, hypothesis chunking, kernel sequencing, profiling and
+// error reporting.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/pnerf.h"
+#include "pnerf_internal.h"
+
+using namespace pnerf;
+
+namespace {
+
+thread_local std::string g_err;
+
+pnerf_status fail(pnerf_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(e_ == hipErrorOutOfMemory ? PNERF_ERR_OUT_OF_MEMORY : PNERF_ERR_DEVICE, \
+                  "%s: %s", #expr, hipGetErrorString(e_));                              \
+  } while (0)
+
+float half_to_float(uint16_t h) {
+  uint32_t s = (h >> 15) & 1u, e = (h >> 10) & 0x1Fu, m = h & 0x3FFu;
+  float v;
+  if (e == 0)
+    v = std::ldexp((float)m, -24);
+  else if (e == 31)
+    v = m ? NAN : INFINITY;
+  else
+    v = std::ldexp((float)(m | 0x400u), (int)e - 25);
+  return s ? -v : v;
+}
+
+struct KernelStat {
+  std::string name;
+  int64_t launches = 0;
+  double total_ms = 0.0;
+};
+
+struct PendingEvent {
+  int idx;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct pnerf_field {
+  DevField dev{};
+  int device = 0;
+  // owned device memory
+  void* d_table = nullptr;
+  float* d_wfwd = nullptr;
+  float* d_wbwd = nullptr;
+  float* d_wd1 = nullptr;
+  float* d_wd2 = nullptr;
+  uint32_t* d_occ = nullptr;
+  int64_t occ_words = 0;
+  // workspace
+  void* d_ws = nullptr;
+  size_t ws_bytes = 0;
+  int ws_rays = 0;
+  int64_t ws_cap = 0;
+  int32_t* d_totals = nullptr;  // per-chunk sample totals
+  int max_chunks = 0;
+  int last_chunks = 0;
+  int64_t budget = 0;
+  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0;
+  // profiling
+  bool profiling = false;
+  std::vector<KernelStat> stats;
+  std::vector<PendingEvent> pending;
+};
+
+namespace {
+
+// ------------------------------------------------------------ weight tiles
+// A-operand tiles of v_mfma_f32_16x16x4_f32: unit u holds 64 floats, lane l
+// supplies A[row = l % 16][k = l / 16] of one (row tile, K step).  Rows are the
+// layer's outputs; the K order follows the C layout of the previous layer
+// (K step 4*m' + i, position g <-> input 16 m' + 4 g + i) so that accumulators
+// feed the next MFMA without data movement.
+struct Weights {
+  int din;
+  std::vector<float> d1, d2, c1, c2, c3;  // [in][out]
+  float D1(int i, int o) const { return d1[(size_t)i * 64 + o]; }
+  float D2(int i, int o) const { return d2[(size_t)i * 16 + o]; }
+  float C1(int i, int o) const { return c1[(size_t)i * 64 + o]; }
+  float C2(int i, int o) const { return c2[(size_t)i * 64 + o]; }
+  float C3(int i, int o) const { return c3[(size_t)i * 3 + o]; }
+};
+
+void build_fwd_tiles(const Weights& W, int lpg, std::vector<float>& t) {
+  t.assign(fwd_tile_floats(lpg), 0.0f);
+  auto put = [&](int unit, int lane, float v) { t[(size_t)unit * 64 + lane] = v; };
+  const int KD = 2 * lpg;
+  for (int lane = 0; lane < 64; ++lane) {
+    int g = lane / 16, c = lane % 16;
+    for (int m = 0; m < 4; ++m)
+      for (int ks = 0; ks < KD; ++ks) {
+        int level = 4 * (ks / 2) + g, feat = 2 * level + ks % 2;
+        put(fwd_off_d1(lpg) + m * KD + ks, lane, W.D1(feat, 16 * m + c));
+      }
+    for (int ks = 0; ks < 16; ++ks) {
+      int mp = ks / 4, i = ks % 4;
+      put(fwd_off_d2(lpg) + ks, lane, W.D2(16 * mp + 4 * g + i, c));
+      put(fwd_off_c3(lpg) + ks, lane, c < 3 ? W.C3(16 * mp + 4 * g + i, c) : 0.0f);
+      for (int m = 0; m < 4; ++m) put(fwd_off_c2(lpg) + m * 16 + ks, lane, W.C2(16 * mp + 4 * g + i, 16 * m + c));
+    }
+    for (int m = 0; m < 4; ++m)
+      for (int i = 0; i < 4; ++i) {
+        int hidx = 4 * g + i;  // h index; x_c index hidx - 1 (h_0 is not an input)
+        put(fwd_off_c1(lpg) + m * 8 + i, lane, hidx >= 1 ? W.C1(hidx - 1, 16 * m + c) : 0.0f);
+        put(fwd_off_c1(lpg) + m * 8 + 4 + i, lane, W.C1(15 + 4 * g + i, 16 * m + c));
+      }
+  }
+}
+
+void build_bwd_tiles(const Weights& W, int lpg, std::vector<float>& t) {
+  t.assign(bwd_tile_floats(lpg), 0.0f);
+  auto put = [&](int unit, int lane, float v) { t[(size_t)unit * 64 + lane] = v; };
+  const int MD = (lpg + 1) / 2;
+  for (int lane = 0; lane < 64; ++lane) {
+    int g = lane / 16, c = lane % 16;
+    for (int m = 0; m < 4; ++m) put(bwd_off_c3(lpg) + m, lane, g < 3 ? W.C3(16 * m + c, g) : 0.0f);
+    for (int ks = 0; ks < 16; ++ks) {
+      int mp = ks / 4, i = ks % 4, kin = 16 * mp + 4 * g + i;
+      for (int m = 0; m < 4; ++m) put(bwd_off_c2(lpg) + m * 16 + ks, lane, W.C2(16 * m + c, kin));
+      put(bwd_off_c1(lpg) + ks, lane, c >= 1 ? W.C1(c - 1, kin) : 0.0f);
+      put(bwd_off_c1(lpg) + 16 + ks, lane, W.C1(15 + c, kin));
+      for (int m = 0; m < MD; ++m) {
+        int gp = c / 4, ip = c % 4, j = 2 * m + ip / 2;
+        float v = 0.0f;
+        if (j < lpg) v = W.D1(2 * (4 * j + gp) + ip % 2, kin);
+        put(bwd_off_d1(lpg) + m * 16 + ks, lane, v);
+      }
+    }
+    for (int m = 0; m < 4; ++m)
+      for (int i = 0; i < 4; ++i) put(bwd_off_d2(lpg) + m * 4 + i, lane, W.D2(16 * m + c, 4 * g + i));
+  }
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace layout for n_rays rays and cap samples.
+size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* p = base ? base + off : nullptr;
+    off += align_up(bytes);
+    return p;
+  };
+  size_t R = (size_t)n_rays;
+  int n_blocks = (n_rays + 255) / 256;
+  int64_t tiles = (cap + kTile - 1) / kTile;
+  DevWork tmp{};
+  DevWork& x = w ? *w : tmp;
+  x.rdx = (float*)take(R * 4);
+  x.rdy = (float*)take(R * 4);
+  x.rdz = (float*)take(R * 4);
+  x.rtn = (float*)take(R * 4);
+  x.rtf = (float*)take(R * 4);
+  x.rdelta = (float*)take(R * 4);
+  x.count = (int32_t*)take(R * 4);
+  x.off = (int32_t*)take((R + 1) * 4);
+  x.blocksum = (int32_t*)take((size_t)n_blocks * 4);
+  x.ray_loss = (float*)take(R * 4);
+  x.t = (float*)take((size_t)tiles * kTile * 4);
+  x.sray = (int32_t*)take((size_t)tiles * kTile * 4);
+  x.sig = (float*)take((size_t)tiles * kTile * 4);
+  x.cr = (float*)take((size_t)tiles * kTile * 4);
+  x.cg = (float*)take((size_t)tiles * kTile * 4);
+  x.cb = (float*)take((size_t)tiles * kTile * 4);
+  x.masks = (uint32_t*)take((size_t)tiles * kMaskWords * 64 * 4);
+  x.cap = tiles * kTile;
+  (void)F;
+  return off;
+}
+
+const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords;  // t, ray, sigma, rgb + masks
+const int64_t kBytesPerRay = 4 * 10;
+
+pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chunks,
+                              hipStream_t s) {
+  if (n_chunks > F->max_chunks) {
+    if (F->d_totals) {
+      HIP_TRY(hipStreamSynchronize(s));
+      HIP_TRY(hipFree(F->d_totals));
+      F->d_totals = nullptr;
+    }
+    int nc = std::max(n_chunks, 16);
+    HIP_TRY(hipMalloc(&F->d_totals, sizeof(int32_t) * nc));
+    F->max_chunks = nc;
+  }
+  if (n_rays <= F->ws_rays && cap <= F->ws_cap) return PNERF_OK;
+  int nr = std::max(n_rays, F->ws_rays);
+  int64_t nc = std::max(cap, F->ws_cap);
+  size_t bytes = carve(F, nr, nc, nullptr, nullptr);
+  if (F->d_ws) {
+    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(hipFree(F->d_ws));
+    F->d_ws = nullptr;
+    F->ws_bytes = 0;
+    F->ws_rays = 0;
+    F->ws_cap = 0;
+  }
+  hipError_t e = hipMalloc(&F->d_ws, bytes);
+  if (e != hipSuccess)
+    return fail(PNERF_ERR_OUT_OF_MEMORY, "workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
+  F->ws_bytes = bytes;
+  F->ws_rays = nr;
+  F->ws_cap = nc;
+  return PNERF_OK;
+}
+
+// --------------------------------------------------------------- profiling
+template <class Fn>
+hipError_t timed(pnerf_field* F, const char* name, hipStream_t s, Fn fn) {
+  if (!F->profiling) return fn();
+  int idx = -1;
+  for (size_t i = 0; i < F->stats.size(); ++i)
+    if (F->stats[i].name == name) idx = (int)i;
+  if (idx < 0) {
+    F->stats.push_back(KernelStat{name, 0, 0.0});
+    idx = (int)F->stats.size() - 1;
+  }
+  PendingEvent pe{idx, nullptr, nullptr};
+  hipError_t e = hipEventCreate(&pe.a);
+  if (e != hipSuccess) return e;
+  e = hipEventCreate(&pe.b);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(pe.a, s);
+  if (e != hipSuccess) return e;
+  e = fn();
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(pe.b, s);
+  F->pending.push_back(pe);
+  F->stats[idx].launches += 1;
+  return e;
+}
+
+pnerf_status resolve_profile(pnerf_field* F) {
+  for (auto& pe : F->pending) {
+    HIP_TRY(hipEventSynchronize(pe.b));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, pe.a, pe.b));
+    F->stats[pe.idx].total_ms += ms;
+    (void)hipEventDestroy(pe.a);
+    (void)hipEventDestroy(pe.b);
+  }
+  F->pending.clear();
+  return PNERF_OK;
+}
+
+// --------------------------------------------------------------- batches
+pnerf_status check_batch(pnerf_field* F, int32_t K, const float* poses, int32_t P,
+                         const int32_t* pix, const pnerf_intrinsics* intr) {
+  if (!F) return fail(PNERF_ERR_INVALID_ARG, "field is NULL");
+  if (K < 1 || P < 1) return fail(PNERF_ERR_INVALID_ARG, "K=%d and P=%d must be >= 1", K, P);
+  if ((int64_t)K * P >= ((int64_t)1 << 31))
+    return fail(PNERF_ERR_INVALID_ARG, "K*P=%lld exceeds 2^31-1", (long long)K * P);
+  if (!poses || !pix || !intr) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (intr->width < 1 || intr->height < 1 || !(intr->fx > 0.0f) || !(intr->fy > 0.0f) ||
+      !std::isfinite(intr->cx) || !std::isfinite(intr->cy))
+    return fail(PNERF_ERR_INVALID_ARG, "invalid intrinsics");
+  if ((int64_t)intr->width * intr->height >= ((int64_t)1 << 31))
+    return fail(PNERF_ERR_INVALID_ARG, "image too large");
+  return PNERF_OK;
+}
+
+DevBatch make_batch(int32_t K, const float* poses, int32_t P, const int32_t* pix,
+                    const float* obs, const pnerf_intrinsics* intr) {
+  DevBatch b{};
+  b.K = K;
+  b.P = P;
+  b.n_rays = K * P;
+  b.poses = poses;
+  b.pix = pix;
+  b.obs = obs;
+  b.W = intr->width;
+  b.H = intr->height;
+  b.fx = intr->fx;
+  b.fy = intr->fy;
+  b.cx = intr->cx;
+  b.cy = intr->cy;
+  return b;
+}
+
+// Hypotheses per chunk so that one chunk's worst-case samples fit the budget
+// (and int32 sample indexing).
+int chunk_hyps(pnerf_field* F, int32_t K, int32_t P) {
+  int64_t per_hyp = (int64_t)P * F->dev.max_per_ray;
+  int64_t by_budget = F->budget / std::max<int64_t>(1, per_hyp * kBytesPerSample + (int64_t)P * kBytesPerRay);
+  int64_t by_index = (((int64_t)1 << 31) - 4096) / std::max<int64_t>(1, per_hyp);
+  int64_t kc = std::min<int64_t>({(int64_t)K, by_budget, by_index});
+  return (int)std::max<int64_t>(kc, 0);
+}
+
+enum Mode { kLossGrad, kRender, kMarch };
+
+pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32_t P,
+                 const int32_t* pix, const float* obs, const pnerf_intrinsics* intr, float* loss,
+                 float* dpose, float* rgb, int64_t* ray_offset, float* t_out, int32_t* j_out,
+                 int64_t capacity, hipStream_t s) {
+  HIP_TRY(hipSetDevice(F->device));
+  int kc = chunk_hyps(F, K, P);
+  if (kc < 1)
+    return fail(PNERF_ERR_CAPACITY, "one hypothesis (%d rays x %d samples) exceeds the workspace budget",
+                P, F->dev.max_per_ray);
+  int n_chunks = (K + kc - 1) / kc;
+  if (mode == kMarch && n_chunks > 1)
+    return fail(PNERF_ERR_CAPACITY, "march inspection needs the batch in one chunk");
+  int64_t cap = (int64_t)kc * P * F->dev.max_per_ray + kTile;
+  pnerf_status st = ensure_workspace(F, kc * P, cap, n_chunks, s);
+  if (st != PNERF_OK) return st;
+  for (int c = 0; c < n_chunks; ++c) {
+    int k0 = c * kc, kn = std::min(kc, K - k0);
+    DevBatch b = make_batch(kn, poses + (size_t)12 * k0, P, pix + (size_t)P * k0, obs, intr);
+    DevWork w{};
+    carve(F, F->ws_rays, F->ws_cap, &w, (char*)F->d_ws);
+    w.total = F->d_totals + c;
+    // inspection: lattice indices go to the (otherwise unused) blue-channel buffer
+    int32_t* j_tmp = mode == kMarch ? reinterpret_cast<int32_t*>(w.cb) : nullptr;
+    HIP_TRY(timed(F, "march", s, [&] { return launch_march(F->dev, b, w, j_tmp, s); }));
+    if (mode == kMarch) {
+      HIP_TRY(launch_offsets_i64(w.off, ray_offset, b.n_rays + 1, 0, s));
+      if (capacity > 0) HIP_TRY(launch_copy_samples(w.t, j_tmp, t_out, j_out, w.total, capacity, s));
+      continue;
+    }
+    HIP_TRY(timed(F, "shade_fwd", s, [&] { return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, s); }));
+    if (mode == kRender) {
+      HIP_TRY(timed(F, "composite_fwd", s, [&] {
+        return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
+      }));
+      continue;
+    }
+    HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
+    HIP_TRY(timed(F, "shade_bwd", s, [&] { return launch_shade_bwd(F->dev, b, w, F->bwd_blocks, s); }));
+    HIP_TRY(timed(F, "reduce", s, [&] {
+      return launch_reduce(b, w, loss + k0, dpose + (size_t)6 * k0, s);
+    }));
+  }
+  F->last_chunks = n_chunks;
+  return PNERF_OK;
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+extern "C" {
+
+const char* pnerf_last_error(void) { return g_err.c_str(); }
+
+pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf_field** out) {
+  if (!p || !out) return fail(PNERF_ERR_INVALID_ARG, "NULL params or out");
+  *out = nullptr;
+  hipStream_t s = (hipStream_t)stream;
+  const int L = p->n_levels;
+  if (L != 4 && L != 8 && L != 12 && L != 16)
+    return fail(PNERF_ERR_NOT_SUPPORTED, "n_levels=%d (supported: 4, 8, 12, 16)", L);
+  if (p->n_features != 2) return fail(PNERF_ERR_NOT_SUPPORTED, "n_features=%d (supported: 2)", p->n_features);
+  if (p->log2_table_size < 4 || p->log2_table_size > 24)
+    return fail(PNERF_ERR_INVALID_ARG, "log2_table_size=%d outside 4..24", p->log2_table_size);
+  if (p->param_dtype != 0) return fail(PNERF_ERR_NOT_SUPPORTED, "param_dtype=%d (fp16 storage not built)", p->param_dtype);
+  if (!p->level_res || !p->table || !p->w_density1 || !p->w_density2 || !p->w_color1 ||
+      !p->w_color2 || !p->w_color3)
+    return fail(PNERF_ERR_INVALID_ARG, "NULL field array");
+  for (int l = 0; l < L; ++l)
+    if (p->level_res[l] < 1 || p->level_res[l] > (1 << 20))
+      return fail(PNERF_ERR_INVALID_ARG, "level_res[%d]=%d outside 1..2^20", l, p->level_res[l]);
+  for (int a = 0; a < 3; ++a)
+    if (!(p->aabb_max[a] > p->aabb_min[a]) || !std::isfinite(p->aabb_min[a]) || !std::isfinite(p->aabb_max[a]))
+      return fail(PNERF_ERR_INVALID_ARG, "empty or non-finite AABB on axis %d", a);
+  if (p->march_mode == 0) {
+    if (p->n_uniform < 1 || p->n_uniform > 4096)
+      return fail(PNERF_ERR_INVALID_ARG, "n_uniform=%d outside 1..4096", p->n_uniform);
+  } else if (p->march_mode == 1) {
+    if (!(p->step > 0.0f) || !std::isfinite(p->step))
+      return fail(PNERF_ERR_INVALID_ARG, "step must be > 0");
+    if (p->max_samples < 1 || p->max_samples > 8192)
+      return fail(PNERF_ERR_INVALID_ARG, "max_samples=%d outside 1..8192", p->max_samples);
+    double diag2 = 0.0;
+    for (int a = 0; a < 3; ++a) {
+      double e = (double)p->aabb_max[a] - (double)p->aabb_min[a];
+      diag2 += e * e;
+    }
+    if (std::sqrt(diag2) / (double)p->step > (double)kMaxLatticeCandidates)
+      return fail(PNERF_ERR_INVALID_ARG, "step too small: more than %d lattice points per ray",
+                  kMaxLatticeCandidates);
+  } else {
+    return fail(PNERF_ERR_INVALID_ARG, "march_mode=%d", p->march_mode);
+  }
+  if (p->occ_res < 0 || p->occ_res > 1024) return fail(PNERF_ERR_INVALID_ARG, "occ_res=%d", p->occ_res);
+  if (p->loss_type != 0) return fail(PNERF_ERR_NOT_SUPPORTED, "loss_type=%d (supported: 0 Huber)", p->loss_type);
+  if (!(p->loss_param > 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "loss_param must be > 0");
+  if (p->sh_dir_grad != 0 && p->sh_dir_grad != 1) return fail(PNERF_ERR_INVALID_ARG, "sh_dir_grad");
+  if (!(p->t_stop >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "t_stop must be >= 0");
+
+  pnerf_field* F = new pnerf_field();
+  auto cleanup_fail = [&](pnerf_status st) {
+    pnerf_destroy_field(F);
+    return st;
+  };
+  (void)hipGetDevice(&F->device);
+  DevField& d = F->dev;
+  d.L = L;
+  d.lpg = L / 4;
+  d.T = 1u << p->log2_table_size;
+  for (int l = 0; l < kMaxLevels; ++l) {
+    int N = l < L ? p->level_res[l] : 1;
+    uint64_t n1 = (uint64_t)N + 1;
+    d.res[l] = N;
+    d.n1[l] = (uint32_t)n1;
+    d.dense[l] = (p->dense_coarse_levels && n1 * n1 * n1 <= d.T) ? 1u : 0u;
+  }
+  d.f16 = 0;
+  d.density_bias = p->density_bias;
+  for (int a = 0; a < 3; ++a) {
+    d.mn[a] = p->aabb_min[a];
+    d.mx[a] = p->aabb_max[a];
+    float ext = p->aabb_max[a] - p->aabb_min[a];
+    d.inv_ext[a] = 1.0f / ext;
+  }
+  d.march_mode = p->march_mode;
+  d.n_uniform = p->n_uniform;
+  d.step = p->step;
+  d.max_samples = p->max_samples;
+  d.t_stop = p->t_stop;
+  d.occ_res = p->occ_res;
+  for (int q = 0; q < 3; ++q) d.bg[q] = p->background[q];
+  d.loss_type = p->loss_type;
+  d.loss_param = p->loss_param;
+  d.sh_dir_grad = p->sh_dir_grad;
+  if (p->march_mode == 0) {
+    d.max_per_ray = p->n_uniform;
+  } else {
+    double diag = 0.0;
+    for (int a = 0; a < 3; ++a) {
+      double e = (double)p->aabb_max[a] - (double)p->aabb_min[a];
+      diag += e * e;
+    }
+    int64_t lat = (int64_t)std::ceil(std::sqrt(diag) / (double)p->step) + 2;
+    d.max_per_ray = (int)std::min<int64_t>(lat, p->max_samples);
+  }
+  F->budget = p->max_workspace_bytes > 0 ? p->max_workspace_bytes : ((int64_t)16 << 30);
+
+  // weights -> float, then MFMA tiles
+  Weights W;
+  W.din = 2 * L;
+  auto load = [&](const void* src, size_t n, std::vector<float>& dst) {
+    dst.resize(n);
+    if (p->param_dtype == 0)
+      std::memcpy(dst.data(), src, n * sizeof(float));
+    else
+      for (size_t i = 0; i < n; ++i) dst[i] = half_to_float(((const uint16_t*)src)[i]);
+  };
+  load(p->w_density1, (size_t)W.din * 64, W.d1);
+  load(p->w_density2, 64 * 16, W.d2);
+  load(p->w_color1, 32 * 64, W.c1);
+  load(p->w_color2, 64 * 64, W.c2);
+  load(p->w_color3, 64 * 3, W.c3);
+  std::vector<float> tf, tb;
+  build_fwd_tiles(W, d.lpg, tf);
+  build_bwd_tiles(W, d.lpg, tb);
+
+  size_t table_elems = (size_t)L * d.T * 2;
+  size_t table_bytes = table_elems * (p->param_dtype == 0 ? 4 : 2);
+#define CF_TRY(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return cleanup_fail(fail(e_ == hipErrorOutOfMemory ? PNERF_ERR_OUT_OF_MEMORY      \
+                                                         : PNERF_ERR_DEVICE,            \
+                               "%s: %s", #expr, hipGetErrorString(e_)));              \
+  } while (0)
+  CF_TRY(hipMalloc(&F->d_table, table_bytes));
+  CF_TRY(hipMemcpyAsync(F->d_table, p->table, table_bytes, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wfwd, tf.size() * 4));
+  CF_TRY(hipMemcpyAsync(F->d_wfwd, tf.data(), tf.size() * 4, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wbwd, tb.size() * 4));
+  CF_TRY(hipMemcpyAsync(F->d_wbwd, tb.data(), tb.size() * 4, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wd1, W.d1.size() * 4));
+  CF_TRY(hipMemcpyAsync(F->d_wd1, W.d1.data(), W.d1.size() * 4, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wd2, W.d2.size() * 4));
+  CF_TRY(hipMemcpyAsync(F->d_wd2, W.d2.data(), W.d2.size() * 4, hipMemcpyHostToDevice, s));
+  d.table32 = (const float*)F->d_table;
+  d.table16 = nullptr;
+  d.wfwd = F->d_wfwd;
+  d.wbwd = F->d_wbwd;
+  d.wd1 = F->d_wd1;
+  d.wd2 = F->d_wd2;
+  d.occ = nullptr;
+  if (p->occ_res > 0) {
+    int64_t R = p->occ_res;
+    F->occ_words = (R * R * R + 31) / 32;
+    CF_TRY(hipMalloc(&F->d_occ, F->occ_words * 4));
+    d.occ = F->d_occ;
+    if (p->occ_bits)
+      CF_TRY(hipMemcpyAsync(F->d_occ, p->occ_bits, F->occ_words * 4, hipMemcpyHostToDevice, s));
+    else
+      CF_TRY(launch_occupancy(d, F->d_occ, (int)R, p->occ_threshold, s));
+  }
+  hipDeviceProp_t prop;
+  CF_TRY(hipGetDeviceProperties(&prop, F->device));
+  F->n_cu = prop.multiProcessorCount;
+  F->fwd_blocks = F->n_cu * shade_fwd_blocks_per_cu(d.lpg);
+  F->bwd_blocks = F->n_cu * shade_bwd_blocks_per_cu(d.lpg);
+  CF_TRY(hipStreamSynchronize(s));
+#undef CF_TRY
+  *out = F;
+  return PNERF_OK;
+}
+
+void pnerf_destroy_field(pnerf_field* F) {
+  if (!F) return;
+  (void)hipSetDevice(F->device);
+  (void)hipDeviceSynchronize();
+  for (auto& pe : F->pending) {
+    (void)hipEventDestroy(pe.a);
+    (void)hipEventDestroy(pe.b);
+  }
+  (void)hipFree(F->d_table);
+  (void)hipFree(F->d_wfwd);
+  (void)hipFree(F->d_wbwd);
+  (void)hipFree(F->d_wd1);
+  (void)hipFree(F->d_wd2);
+  (void)hipFree(F->d_occ);
+  (void)hipFree(F->d_ws);
+  (void)hipFree(F->d_totals);
+  delete F;
+}
+
+pnerf_status pnerf_render_loss_grad(pnerf_field* F, int32_t K, const float* poses, int32_t P,
+                                    const int32_t* pixel_ids, const float* observed,
+                                    const pnerf_intrinsics* intr, float* loss, float* dpose,
+                                    void* stream) {
+  pnerf_status st = check_batch(F, K, poses, P, pixel_ids, intr);
+  if (st != PNERF_OK) return st;
+  if (!observed || !loss || !dpose) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  return run(F, kLossGrad, K, poses, P, pixel_ids, observed, intr, loss, dpose, nullptr, nullptr,
+             nullptr, nullptr, 0, (hipStream_t)stream);
+}
+
+pnerf_status pnerf_render(pnerf_field* F, int32_t K, const float* poses, int32_t P,
+                          const int32_t* pixel_ids, const pnerf_intrinsics* intr, float* rgb,
+                          void* stream) {
+  pnerf_status st = check_batch(F, K, poses, P, pixel_ids, intr);
+  if (st != PNERF_OK) return st;
+  if (!rgb) return fail(PNERF_ERR_INVALID_ARG, "NULL rgb");
+  return run(F, kRender, K, poses, P, pixel_ids, nullptr, intr, nullptr, nullptr, rgb, nullptr,
+             nullptr, nullptr, 0, (hipStream_t)stream);
+}
+
+pnerf_status pnerf_march(pnerf_field* F, int32_t K, const float* poses, int32_t P,
+                         const int32_t* pixel_ids, const pnerf_intrinsics* intr,
+                         int64_t* ray_offset, float* t, int32_t* lattice_j, int64_t capacity,
+                         void* stream) {
+  pnerf_status st = check_batch(F, K, poses, P, pixel_ids, intr);
+  if (st != PNERF_OK) return st;
+  if (!ray_offset) return fail(PNERF_ERR_INVALID_ARG, "NULL ray_offset");
+  if (capacity < 0 || (capacity > 0 && (!t || !lattice_j)))
+    return fail(PNERF_ERR_INVALID_ARG, "capacity > 0 needs t and lattice_j");
+  return run(F, kMarch, K, poses, P, pixel_ids, nullptr, intr, nullptr, nullptr, nullptr,
+             ray_offset, t, lattice_j, capacity, (hipStream_t)stream);
+}
+
+pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum, const float* dpose,
+                                 float lr, float beta, void* stream) {
+  if (K < 1) return fail(PNERF_ERR_INVALID_ARG, "K=%d", K);
+  if (!poses || !momentum || !dpose) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (!std::isfinite(lr) || !std::isfinite(beta)) return fail(PNERF_ERR_INVALID_ARG, "lr/beta");
+  HIP_TRY(launch_step_momentum(K, poses, momentum, dpose, lr, beta, (hipStream_t)stream));
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
+                                       const float* loss, float keep_frac, float sigma_rot,
+                                       float sigma_trans, uint64_t seed, uint32_t round_idx,
+                                       void* stream) {
+  if (K < 1 || K > 65535) return fail(PNERF_ERR_INVALID_ARG, "K=%d outside 1..65535", K);
+  if (!poses || !momentum || !loss) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (!(keep_frac >= 0.0f && keep_frac <= 1.0f)) return fail(PNERF_ERR_INVALID_ARG, "keep_frac");
+  if (!(sigma_rot >= 0.0f) || !(sigma_trans >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "sigma");
+  int n_keep = (int)std::floor((double)K * (double)keep_frac);
+  n_keep = std::max(1, std::min(n_keep, K));
+  hipStream_t s = (hipStream_t)stream;
+  int32_t* scratch = nullptr;
+  HIP_TRY(hipMallocAsync((void**)&scratch, sizeof(int32_t) * 2 * (size_t)K, s));
+  hipError_t e = launch_resample(K, poses, momentum, loss, n_keep, sigma_rot, sigma_trans, seed,
+                                 round_idx, scratch, s);
+  hipError_t e2 = hipFreeAsync(scratch, s);
+  if (e != hipSuccess) return fail(PNERF_ERR_DEVICE, "resample launch: %s", hipGetErrorString(e));
+  HIP_TRY(e2);
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_field_occupancy(pnerf_field* F, uint32_t* bits_host, void* stream) {
+  if (!F || !bits_host) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
+  if (!F->d_occ) return fail(PNERF_ERR_INVALID_ARG, "field has no occupancy grid");
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(bits_host, F->d_occ, F->occ_words * 4, hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_field_last_sample_count(pnerf_field* F, int64_t* count, void* stream) {
+  if (!F || !count) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
+  *count = 0;
+  if (F->last_chunks == 0) return PNERF_OK;
+  std::vector<int32_t> h(F->last_chunks);
+  hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(h.data(), F->d_totals, sizeof(int32_t) * h.size(), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  for (int32_t v : h) *count += v;
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_field_set_profiling(pnerf_field* F, int32_t enable) {
+  if (!F) return fail(PNERF_ERR_INVALID_ARG, "NULL field");
+  pnerf_status st = resolve_profile(F);
+  if (st != PNERF_OK) return st;
+  if (enable) F->stats.clear();
+  F->profiling = enable != 0;
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_field_profile_read(pnerf_field* F, int32_t index, const char** name,
+                                      int64_t* launches, double* total_ms) {
+  if (!F) return fail(PNERF_ERR_INVALID_ARG, "NULL field");
+  pnerf_status st = resolve_profile(F);
+  if (st != PNERF_OK) return st;
+  if (index < 0 || index >= (int32_t)F->stats.size())
+    return fail(PNERF_ERR_INVALID_ARG, "profile index %d past the end", index);
+  if (name) *name = F->stats[index].name.c_str();
+  if (launches) *launches = F->stats[index].launches;
+  if (total_ms) *total_ms = F->stats[index].total_ms;
+  return PNERF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,203 @@
+// Front-to-back compositing of each ray's samples (classic volume rendering),
+// the robust photometric loss against the observed pixel, the backward pass of
+// the composite, and the deterministic per-hypothesis reduction.
+//
+// One wavefront per ray; 64 samples per step.  Transmittance comes from a
+// wavefront prefix sum of sigma*delta carried across steps; the backward pass
+// re-sweeps the ray and takes the colour still to come behind sample i as
+// C - (prefix of w c up to i).
+#include "pnerf_internal.h"
+
+namespace pnerf {
+namespace {
+
+constexpr int kBlock = 256;
+
+__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    float y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// Huber with threshold dl; returns the loss, writes its derivative.
+__device__ __forceinline__ float huber(float r, float dl, float& grad) {
+  float ar = fabsf(r);
+  if (ar <= dl) {
+    grad = r;
+    return 0.5f * r * r;
+  }
+  grad = r > 0.0f ? dl : -dl;
+  return dl * (ar - 0.5f * dl);
+}
+
+struct Chunk {
+  bool live;        // sample exists and is composited
+  float sig, tau, T_in, T_out, w, c[3];
+  bool stop_here;
+};
+
+// Evaluate one 64-sample step of a ray: transmittance in and out, weight.
+__device__ inline Chunk step_chunk(const DevField& f, const DevWork& w, int base, int n, int i0,
+                                   float delta, float carry, int lane, float& incl_out) {
+  Chunk ch;
+  int i = i0 + lane;
+  bool valid = i < n;
+  ch.sig = valid ? w.sig[base + i] : 0.0f;
+  ch.c[0] = valid ? w.cr[base + i] : 0.0f;
+  ch.c[1] = valid ? w.cg[base + i] : 0.0f;
+  ch.c[2] = valid ? w.cb[base + i] : 0.0f;
+  ch.tau = ch.sig * delta;
+  float incl = wave_incl_scan(ch.tau, lane) + carry;
+  incl_out = incl;
+  ch.T_in = __expf(-(incl - ch.tau));
+  ch.T_out = __expf(-incl);
+  float alpha = -expm1f(-ch.tau);
+  ch.w = valid ? ch.T_in * alpha : 0.0f;
+  ch.live = valid;
+  ch.stop_here = valid && f.t_stop > 0.0f && ch.T_out < f.t_stop;
+  return ch;
+}
+
+template <int WITH_GRAD>
+__global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, DevWork w,
+                                                      float* rgb_out) {
+  int lane = threadIdx.x & 63;
+  int ray = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  if (ray >= b.n_rays) return;
+  const int base = w.off[ray];
+  const int n = w.off[ray + 1] - base;
+  const float delta = w.rdelta[ray];
+
+  // pass 1: colour, transmittance, stop index
+  float C[3] = {0.f, 0.f, 0.f};
+  float carry = 0.0f;
+  int n_used = n;
+  for (int i0 = 0; i0 < n_used; i0 += 64) {
+    float incl;
+    Chunk ch = step_chunk(f, w, base, n, i0, delta, carry, lane, incl);
+    uint64_t st = __ballot(ch.stop_here);
+    int last = 63;
+    if (st) {
+      last = __ffsll((unsigned long long)st) - 1;
+      n_used = i0 + last + 1;
+    }
+    bool use = ch.live && lane <= last;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) C[q] += wave_sum(use ? ch.w * ch.c[q] : 0.0f);
+    carry = __shfl(incl, last);
+    if (st) break;
+  }
+  float T_end = __expf(-carry);
+  for (int q = 0; q < 3; ++q) C[q] += T_end * f.bg[q];
+
+  if (!WITH_GRAD) {
+    if (lane < 3) rgb_out[3 * ray + lane] = C[lane];
+    return;
+  }
+
+  // loss on the observed pixel: mean over the P pixels and 3 channels
+  int pix = b.pix[ray];
+  const int n_pix = b.W * b.H;
+  pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);
+  const float* I = b.obs + 3 * (size_t)pix;
+  const float norm = 1.0f / (3.0f * (float)b.P);
+  float gC[3], L = 0.0f;
+  for (int q = 0; q < 3; ++q) {
+    float gq;
+    L += huber(C[q] - I[q], f.loss_param, gq);
+    gC[q] = gq * norm;
+  }
+  if (lane == 0) w.ray_loss[ray] = L * norm;
+
+  // pass 2: d loss / d sigma_i and d loss / d c_i, written over sigma and c as
+  // d loss / d h_0 = g_sigma * sigma and d loss / d z = g_c * c (1 - c)
+  float carry2 = 0.0f, pre[3] = {0.f, 0.f, 0.f};
+  for (int i0 = 0; i0 < n; i0 += 64) {
+    int i = i0 + lane;
+    if (i0 >= n_used) {
+      if (i < n) {
+        w.sig[base + i] = 0.0f;
+        w.cr[base + i] = 0.0f;
+        w.cg[base + i] = 0.0f;
+        w.cb[base + i] = 0.0f;
+      }
+      continue;
+    }
+    float incl;
+    Chunk ch = step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
+    bool use = ch.live && i < n_used;
+    float gs = 0.0f, gz[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      float wc = use ? ch.w * ch.c[q] : 0.0f;
+      float p = wave_incl_scan(wc, lane) + pre[q];
+      pre[q] = __shfl(p, 63);
+      float S = C[q] - p;  // colour behind sample i (incl. background)
+      gs += gC[q] * (ch.T_out * ch.c[q] - S);
+      gz[q] = ch.w * gC[q] * ch.c[q] * (1.0f - ch.c[q]);
+    }
+    carry2 = __shfl(incl, 63);
+    if (i < n) {
+      w.sig[base + i] = use ? delta * gs * ch.sig : 0.0f;
+      w.cr[base + i] = use ? gz[0] : 0.0f;
+      w.cg[base + i] = use ? gz[1] : 0.0f;
+      w.cb[base + i] = use ? gz[2] : 0.0f;
+    }
+  }
+}
+
+// One workgroup per hypothesis: loss = sum of its rays' losses, dpose = sum of
+// its samples' (torque, force) terms; fixed assignment and tree order.
+__global__ __launch_bounds__(kBlock) void k_reduce(DevBatch b, DevWork w, float* loss,
+                                                   float* dpose) {
+  __shared__ float red[7][kBlock];
+  int k = blockIdx.x, tid = threadIdx.x;
+  int r0 = k * b.P, r1 = r0 + b.P;
+  int s0 = w.off[r0], s1 = w.off[r1];
+  float acc[7] = {0, 0, 0, 0, 0, 0, 0};
+  for (int r = r0 + tid; r < r1; r += kBlock) acc[6] += w.ray_loss[r];
+  const float* out = reinterpret_cast<const float*>(w.masks);
+  for (int s = s0 + tid; s < s1; s += kBlock) {
+    size_t t = (size_t)(s >> 6) * kMaskWords * 64 + (s & 63);
+#pragma unroll
+    for (int q = 0; q < 6; ++q) acc[q] += out[t + q * 64];
+  }
+  for (int q = 0; q < 7; ++q) red[q][tid] = acc[q];
+  __syncthreads();
+  for (int stride = kBlock / 2; stride > 0; stride >>= 1) {
+    if (tid < stride)
+      for (int q = 0; q < 7; ++q) red[q][tid] += red[q][tid + stride];
+    __syncthreads();
+  }
+  if (tid < 6) dpose[6 * k + tid] = red[tid][0];
+  if (tid == 6) loss[k] = red[6][0];
+}
+
+}  // namespace
+
+hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
+                            float* rgb_out, hipStream_t s) {
+  int n_blocks = (b.n_rays + (kBlock / 64) - 1) / (kBlock / 64);
+  if (with_grad)
+    hipLaunchKernelGGL(k_composite<1>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w, rgb_out);
+  else
+    hipLaunchKernelGGL(k_composite<0>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w, rgb_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(k_reduce, dim3(b.K), dim3(kBlock), 0, s, b, w, loss, dpose);
+  return hipGetLastError();
+}
+
+}  // namespace pnerf

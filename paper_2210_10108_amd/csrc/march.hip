@@ -1,0 +1,265 @@
+// Ray generation, box clipping, sample placement with occupancy skipping, and
+// deterministic compaction (count -> scan -> write) into SoA sample buffers.
+//
+// Every floating-point step that decides an integer (which samples exist, their
+// distance t, the occupancy cell) uses a fixed operation order with correctly
+// rounded division and square root and no contraction, so the sample set is
+// reproducible bit for bit by any implementation following the same order.
+#include "pnerf_internal.h"
+
+namespace pnerf {
+namespace {
+
+constexpr int kRayBlock = 256;
+
+struct RayGeom {
+  float o[3], d[3], tn, tf, delta;
+  int hit;
+};
+
+// Pixel -> ray (Sec. IV-A: the ray origin is the camera centre) and its
+// clip against the scene box.
+__device__ inline RayGeom make_ray(const DevField& f, const DevBatch& b, int ray) {
+#pragma clang fp contract(off)
+  RayGeom g;
+  const float* pose = b.poses + 12 * (ray / b.P);
+  int pix = b.pix[ray];
+  const int n_pix = b.W * b.H;
+  pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);  // out-of-range ids are clamped
+  int u = pix % b.W, v = pix / b.W;
+  float xc = __fdiv_rn((float)u + 0.5f - b.cx, b.fx);
+  float yc = __fdiv_rn((float)v + 0.5f - b.cy, b.fy);
+  float dw[3];
+  for (int a = 0; a < 3; ++a) {
+    dw[a] = (pose[4 * a] * xc + pose[4 * a + 1] * yc) + pose[4 * a + 2];
+    g.o[a] = pose[4 * a + 3];
+  }
+  float n = __fsqrt_rn((dw[0] * dw[0] + dw[1] * dw[1]) + dw[2] * dw[2]);
+  for (int a = 0; a < 3; ++a) g.d[a] = __fdiv_rn(dw[a], n);
+  float t_entry = -INFINITY, t_exit = INFINITY;
+  bool empty = false;
+  for (int a = 0; a < 3; ++a) {
+    if (g.d[a] != 0.0f) {
+      float t1 = __fdiv_rn(f.mn[a] - g.o[a], g.d[a]);
+      float t2 = __fdiv_rn(f.mx[a] - g.o[a], g.d[a]);
+      float lo = t1 < t2 ? t1 : t2, hi = t1 < t2 ? t2 : t1;
+      if (lo > t_entry) t_entry = lo;
+      if (hi < t_exit) t_exit = hi;
+    } else if (g.o[a] < f.mn[a] || g.o[a] > f.mx[a]) {
+      empty = true;
+    }
+  }
+  if (empty) {
+    g.tn = 0.0f;
+    g.tf = 0.0f;
+    g.hit = 0;
+  } else {
+    g.tn = t_entry > 0.0f ? t_entry : 0.0f;
+    g.tf = t_exit;
+    g.hit = g.tf > g.tn;
+  }
+  if (f.march_mode == 0)
+    g.delta = g.hit ? __fdiv_rn(g.tf - g.tn, (float)f.n_uniform) : 0.0f;
+  else
+    g.delta = f.step;
+  return g;
+}
+
+__device__ inline float sample_t(const DevField& f, float tn, float delta, int j) {
+#pragma clang fp contract(off)
+  float s = f.march_mode == 0 ? delta : f.step;
+  return tn + ((float)j + 0.5f) * s;
+}
+
+__device__ inline bool occupied(const DevField& f, const float o[3], const float d[3], float t) {
+#pragma clang fp contract(off)
+  if (f.occ_res <= 0) return true;
+  int R = f.occ_res;
+  uint32_t c[3];
+  for (int a = 0; a < 3; ++a) {
+    float p = o[a] + t * d[a];
+    float ext = f.mx[a] - f.mn[a];
+    float sc = __fdiv_rn((float)R, ext);
+    float q = (p - f.mn[a]) * sc;
+    int ci = q < 0.0f ? 0 : (q >= (float)R ? R - 1 : (int)q);
+    c[a] = (uint32_t)ci;
+  }
+  uint64_t idx = (uint64_t)c[0] + (uint64_t)R * ((uint64_t)c[1] + (uint64_t)R * c[2]);
+  return (f.occ[idx >> 5] >> (idx & 31u)) & 1u;
+}
+
+// One wavefront marches one ray, 64 candidate samples per step: each lane
+// tests one candidate, a ballot compacts the kept ones in order.
+template <bool EMIT>
+__device__ inline int march_wave(const DevField& f, const RayGeom& g, int lane, int cap,
+                                 float* t_out, int32_t* j_out, int32_t* ray_out, int ray) {
+  if (!g.hit) return 0;
+  int kept = 0;
+  int limit = f.march_mode == 0 ? f.n_uniform : f.max_samples;
+  if (limit > cap) limit = cap;
+  for (int j0 = 0;; j0 += 64) {
+    int j = j0 + lane;
+    float t = sample_t(f, g.tn, g.delta, j);
+    bool valid = f.march_mode == 0 ? (j < f.n_uniform) : (t < g.tf);
+    bool occ = valid && occupied(f, g.o, g.d, t);
+    uint64_t bal = __ballot(occ);
+    int rank = __popcll(bal & ((1ull << lane) - 1ull));
+    if (EMIT && occ && kept + rank < limit) {
+      t_out[kept + rank] = t;
+      if (j_out) j_out[kept + rank] = j;
+      ray_out[kept + rank] = ray;
+    }
+    int n = __popcll(bal);
+    kept = kept + n < limit ? kept + n : limit;
+    bool last_valid = __shfl(valid ? 1 : 0, 63) != 0;
+    if (kept >= limit || !last_valid || j0 + 64 >= kMaxLatticeCandidates + 64) break;
+  }
+  return kept;
+}
+
+__global__ __launch_bounds__(kRayBlock) void k_ray_count(DevField f, DevBatch b, DevWork w) {
+  __shared__ int s_cnt[kRayBlock];
+  int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int base = blockIdx.x * kRayBlock;
+  // per-lane ray geometry for the rays of this wave, then march them one by one
+  for (int q = 0; q < 64; ++q) {
+    int ray = base + wv * 64 + q;
+    if (ray >= b.n_rays) {
+      if (lane == 0) s_cnt[wv * 64 + q] = 0;
+      continue;
+    }
+    RayGeom g = make_ray(f, b, ray);
+    int n = march_wave<false>(f, g, lane, f.max_per_ray, nullptr, nullptr, nullptr, ray);
+    if (lane == 0) {
+      s_cnt[wv * 64 + q] = n;
+      w.count[ray] = n;
+      w.rdx[ray] = g.d[0];
+      w.rdy[ray] = g.d[1];
+      w.rdz[ray] = g.d[2];
+      w.rtn[ray] = g.tn;
+      w.rtf[ray] = g.tf;
+      w.rdelta[ray] = g.delta;
+    }
+  }
+  __syncthreads();
+  // block total (fixed-order tree)
+  for (int stride = kRayBlock / 2; stride > 0; stride >>= 1) {
+    if (threadIdx.x < stride) s_cnt[threadIdx.x] += s_cnt[threadIdx.x + stride];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) w.blocksum[blockIdx.x] = s_cnt[0];
+}
+
+// Exclusive scan of the block totals in one workgroup (n_blocks <= 8192).
+__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks) {
+  __shared__ int s[1024];
+  constexpr int kPer = 8;
+  int tid = threadIdx.x;
+  int v[kPer], acc = 0;
+  for (int q = 0; q < kPer; ++q) {
+    int i = tid * kPer + q;
+    v[q] = i < n_blocks ? w.blocksum[i] : 0;
+    acc += v[q];
+  }
+  s[tid] = acc;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    int x = tid >= off ? s[tid - off] : 0;
+    __syncthreads();
+    s[tid] += x;
+    __syncthreads();
+  }
+  int run = s[tid] - acc;  // exclusive prefix of this thread's chunk
+  for (int q = 0; q < kPer; ++q) {
+    int i = tid * kPer + q;
+    if (i < n_blocks) w.blocksum[i] = run;
+    run += v[q];
+  }
+  if (tid == 1023) *w.total = s[1023];
+}
+
+__global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork w,
+                                                         int32_t* j_out) {
+  __shared__ int s_off[kRayBlock];
+  int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  int base = blockIdx.x * kRayBlock;
+  int ray0 = base + tid;
+  int c = ray0 < b.n_rays ? w.count[ray0] : 0;
+  s_off[tid] = c;
+  __syncthreads();
+  for (int off = 1; off < kRayBlock; off <<= 1) {
+    int x = tid >= off ? s_off[tid - off] : 0;
+    __syncthreads();
+    s_off[tid] += x;
+    __syncthreads();
+  }
+  int block_base = w.blocksum[blockIdx.x];
+  if (ray0 < b.n_rays) {
+    w.off[ray0] = block_base + s_off[tid] - c;
+    if (ray0 == b.n_rays - 1) w.off[b.n_rays] = block_base + s_off[tid];
+  }
+  __syncthreads();
+  for (int q = 0; q < 64; ++q) {
+    int slot = wv * 64 + q;
+    int ray = base + slot;
+    if (ray >= b.n_rays) break;
+    int o = block_base + s_off[slot] - w.count[ray];
+    RayGeom g;
+    g.o[0] = b.poses[12 * (ray / b.P) + 3];
+    g.o[1] = b.poses[12 * (ray / b.P) + 7];
+    g.o[2] = b.poses[12 * (ray / b.P) + 11];
+    g.d[0] = w.rdx[ray];
+    g.d[1] = w.rdy[ray];
+    g.d[2] = w.rdz[ray];
+    g.tn = w.rtn[ray];
+    g.tf = w.rtf[ray];
+    g.delta = w.rdelta[ray];
+    g.hit = w.count[ray] > 0;
+    march_wave<true>(f, g, lane, w.count[ray], w.t + o, j_out ? j_out + o : nullptr, w.sray + o,
+                     ray);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
+                        int32_t* lattice_j_out, hipStream_t s) {
+  int n_blocks = (b.n_rays + kRayBlock - 1) / kRayBlock;
+  if (n_blocks > 8192) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_ray_count, dim3(n_blocks), dim3(kRayBlock), 0, s, f, b, w);
+  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_blocks);
+  hipLaunchKernelGGL(k_ray_write, dim3(n_blocks), dim3(kRayBlock), 0, s, f, b, w, lattice_j_out);
+  return hipGetLastError();
+}
+
+__global__ void k_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = base + off[i];
+}
+
+// Copy t and lattice index of every sample when the total fits `capacity`.
+__global__ void k_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
+                               const int32_t* total, int64_t capacity) {
+  int64_t n = *total;
+  if (n > capacity) return;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    t_out[i] = t[i];
+    j_out[i] = j[i];
+  }
+}
+
+hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
+                               const int32_t* total, int64_t capacity, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_samples, dim3(1024), dim3(256), 0, s, t, j, t_out, j_out, total,
+                     capacity);
+  return hipGetLastError();
+}
+
+hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(k_offsets_i64, dim3((n + 255) / 256), dim3(256), 0, s, off, out, n, base);
+  return hipGetLastError();
+}
+
+}  // namespace pnerf

@@ -1,0 +1,114 @@
+// Internal declarations of the HIP implementation (gfx950 / CDNA4).
+// Device-side views of a field, of one batch chunk and of its workspace, plus
+// the host launchers each kernel source file exports.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace pnerf {
+
+constexpr int kMaxLevels = 16;
+constexpr int kHidden = 64;
+constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
+constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile (aliased by 6 outputs)
+constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
+
+// Sizes (in floats) of the MFMA A-operand weight tiles, see the layout built in api.hip.
+__host__ __device__ constexpr int fwd_tile_floats(int lpg) {
+  return (4 * 2 * lpg + 16 + 4 * 8 + 4 * 16 + 16) * 64;
+}
+__host__ __device__ constexpr int bwd_tile_floats(int lpg) {
+  return (4 * 1 + 4 * 16 + 2 * 16 + 4 * 4 + ((lpg + 1) / 2) * 16) * 64;
+}
+// offsets (in 64-float K-step units) of each layer inside the tile blocks
+__host__ __device__ constexpr int fwd_off_d1(int) { return 0; }
+__host__ __device__ constexpr int fwd_off_d2(int lpg) { return 4 * 2 * lpg; }
+__host__ __device__ constexpr int fwd_off_c1(int lpg) { return fwd_off_d2(lpg) + 16; }
+__host__ __device__ constexpr int fwd_off_c2(int lpg) { return fwd_off_c1(lpg) + 4 * 8; }
+__host__ __device__ constexpr int fwd_off_c3(int lpg) { return fwd_off_c2(lpg) + 4 * 16; }
+__host__ __device__ constexpr int bwd_off_c3(int) { return 0; }
+__host__ __device__ constexpr int bwd_off_c2(int) { return 4; }
+__host__ __device__ constexpr int bwd_off_c1(int) { return 4 + 64; }        // 2 M-tiles (h rows, SH rows)
+__host__ __device__ constexpr int bwd_off_d2(int) { return 4 + 64 + 32; }
+__host__ __device__ constexpr int bwd_off_d1(int) { return 4 + 64 + 32 + 16; }
+
+struct DevField {
+  int32_t L, lpg;               // levels, levels per lane group (L / 4)
+  uint32_t T;                   // table entries per level (power of two)
+  int32_t res[kMaxLevels];
+  uint32_t dense[kMaxLevels];   // 1: vertex index i + j n1 + k n1^2
+  uint32_t n1[kMaxLevels];      // res + 1
+  int32_t f16;                  // table and weights stored as fp16
+  const float* table32;         // [L][T][2]
+  const __half* table16;        // [L][T][2]
+  const float* wfwd;            // forward A-operand tiles (fp32)
+  const float* wbwd;            // backward A-operand tiles (fp32)
+  const float* wd1;             // plain W_d1 [2L][64] and W_d2 [64][16] (occupancy build)
+  const float* wd2;
+  float density_bias;
+  float mn[3], mx[3], inv_ext[3];
+  int32_t march_mode, n_uniform;
+  float step;
+  int32_t max_samples;
+  float t_stop;
+  int32_t occ_res;
+  const uint32_t* occ;
+  float bg[3];
+  int32_t loss_type;
+  float loss_param;
+  int32_t sh_dir_grad;
+  int32_t max_per_ray;          // hard cap on kept samples per ray (buffer bound)
+};
+
+struct DevBatch {
+  int32_t K, P, n_rays;         // hypotheses, pixels per hypothesis, K*P (this chunk)
+  const float* poses;           // [K][12]
+  const int32_t* pix;           // [K][P]
+  const float* obs;             // [H][W][3]
+  int32_t W, H;
+  float fx, fy, cx, cy;
+};
+
+struct DevWork {
+  // per ray (SoA)
+  float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta;
+  int32_t* count;               // kept samples per ray
+  int32_t* off;                 // [n_rays + 1] exclusive offsets
+  int32_t* blocksum;            // per 256-ray block
+  int32_t* total;               // device scalar: samples in this chunk
+  float* ray_loss;              // [n_rays]
+  // per sample
+  float* t;
+  int32_t* sray;                // ray of each sample
+  float* sig;                   // sigma (forward) -> d loss / d h0 (after composite)
+  float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
+  uint32_t* masks;              // [tiles][6][64] ReLU masks -> 6 float outputs per sample
+  int64_t cap;                  // sample capacity
+};
+
+// ---- launchers (all enqueue on `s`, no synchronisation)
+hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
+                        int32_t* lattice_j_out, hipStream_t s);
+hipError_t launch_shade_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                            hipStream_t s);
+hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
+                            float* rgb_out, hipStream_t s);
+hipError_t launch_shade_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                            hipStream_t s);
+hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
+                         hipStream_t s);
+hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s);
+hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
+                               const int32_t* total, int64_t capacity, hipStream_t s);
+hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base, hipStream_t s);
+hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dpose, float lr,
+                                float beta, hipStream_t s);
+hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, int n_keep,
+                           float sr, float st, uint64_t seed, uint32_t round, int32_t* scratch,
+                           hipStream_t s);
+
+int shade_fwd_blocks_per_cu(int lpg);
+int shade_bwd_blocks_per_cu(int lpg);
+
+}  // namespace pnerf
