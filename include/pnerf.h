@@ -185,6 +185,18 @@ pnerf_status pnerf_march(pnerf_field* field, int32_t K, const float* poses, int3
                          int64_t* ray_offset, float* t, int32_t* lattice_j, int64_t capacity,
                          void* stream);
 
+/* Per-sample intermediates of the last call on this field (inspection; the
+ * batch must have fitted one workspace chunk).  `dst` (device) receives
+ * float32 values for the first n samples (n = the last call's sample total):
+ *   what 0: t [n]
+ *   what 1: after pnerf_render sigma [n]; after pnerf_render_loss_grad dL/dh_0 [n]
+ *   what 2: after pnerf_render rgb [n][3]; after pnerf_render_loss_grad dL/dz [n][3]
+ *           (z = pre-sigmoid colour)
+ *   what 3: after pnerf_render_loss_grad (t d x dL/dp, dL/dp) [n][6]
+ * PNERF_ERR_INVALID_ARG if n exceeds the workspace or `what` is unknown. */
+pnerf_status pnerf_field_inspect(pnerf_field* field, int32_t what, float* dst, int64_t n,
+                                 void* stream);
+
 /* Copy the field's occupancy grid to `bits_host` (ceil(R^3/32) words);
  * synchronises `stream`.  PNERF_ERR_INVALID_ARG if the field has no grid. */
 pnerf_status pnerf_field_occupancy(pnerf_field* field, uint32_t* bits_host, void* stream);

@@ -64,7 +64,7 @@ def lib():
         L.orc_march.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i64]
         L.orc_shade.restype = i32
         L.orc_shade.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
-                                vp, i32]
+                                vp, vp, i32]
         L.orc_encode.argtypes = [vp, vp, vp, vp, vp, vp]
         L.orc_sh16.argtypes = [vp, vp, vp]
         L.orc_density_mlp.argtypes = [vp, vp, vp]
@@ -184,7 +184,8 @@ class OracleField:
         assert rc == 0
         return off, t[:total], j[:total], delta
 
-    def shade(self, poses64, pix, obs, intr, march, sh_dirs=None, threads=None):
+    def shade(self, poses64, pix, obs, intr, march, sh_dirs=None, threads=None,
+              per_sample=False):
         poses64 = np.ascontiguousarray(poses64, dtype=np.float64).reshape(-1, 12)
         pix = np.ascontiguousarray(pix, dtype=np.int32)
         K, P = pix.shape
@@ -197,19 +198,23 @@ class OracleField:
         rgb = np.zeros((K * P, 3))
         stop = np.zeros(K * P, dtype=np.int32)
         sig = np.zeros(1, dtype=np.uint64)
+        so = np.zeros((max(int(off[-1]), 1), 16)) if per_sample else None
         it = intr_struct(intr)
         rc = lib().orc_shade(self.ptr, K, _p(poses64), P, _p(pix), _p(obs), C.byref(it), _p(off),
                              _p(t), _p(delta), _p(sd), _p(loss), _p(dpose), _p(rgb), _p(stop),
-                             _p(sig), threads or n_threads_default())
+                             _p(sig), _p(so), threads or n_threads_default())
         if rc != 0:
             raise ValueError("oracle: unsupported field configuration")
-        return dict(loss=loss, dpose=dpose, rgb=rgb.reshape(K, P, 3), stop=stop,
-                    signature=int(sig[0]))
+        out = dict(loss=loss, dpose=dpose, rgb=rgb.reshape(K, P, 3), stop=stop,
+                   signature=int(sig[0]))
+        if per_sample:
+            out["samples"] = so[: int(off[-1])]
+        return out
 
-    def render_loss_grad(self, poses, pix, obs, intr, threads=None):
+    def render_loss_grad(self, poses, pix, obs, intr, threads=None, per_sample=False):
         m = self.march(poses, pix, intr)
         out = self.shade(np.asarray(poses, dtype=np.float32).astype(np.float64), pix, obs, intr, m,
-                         threads=threads)
+                         threads=threads, per_sample=per_sample)
         out["march"] = m
         return out
 

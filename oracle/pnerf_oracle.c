@@ -401,7 +401,7 @@ typedef struct {
 static void shade_ray(const orc_field* f, const double pose64[12], const orc_intr* in,
                       int32_t pix, const float* obs, const float* ts, int32_t n, float delta32,
                       const double* sh_dir, int32_t P, double* loss_out, double g_out[6],
-                      double rgb_out[3], int32_t* stop_out, uint64_t* sig) {
+                      double rgb_out[3], int32_t* stop_out, uint64_t* sig, double* s_out) {
   float pose32[12];
   for (int q = 0; q < 12; ++q) pose32[q] = (float)pose64[q];
   float o32[3], d32[3];
@@ -449,11 +449,26 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
       }
     density_fwd(f, s->feat, s->a_pre, s->h);
     s->sigma = exp(s->h[0] + f->density_bias);
+    /* decision margin of the density ReLUs: |pre-activation| over the sum of
+     * its terms' magnitudes (diagnostic for comparing against float kernels) */
+    double margin = INFINITY;
+    for (int j = 0; j < HID; ++j) {
+      double m = 0.0;
+      for (int q = 0; q < f->din; ++q) m += fabs(s->feat[q] * f->wd1[q * HID + j]);
+      if (m > 0.0 && fabs(s->a_pre[j]) / m < margin) margin = fabs(s->a_pre[j]) / m;
+    }
     double xc[CIN];
     for (int q = 0; q < 15; ++q) xc[q] = s->h[1 + q];
     for (int q = 0; q < 16; ++q) xc[15 + q] = sh[q];
     xc[31] = 0.0;
     color_fwd(f, xc, s->b1, s->b2, s->rgb);
+    for (int j = 0; j < HID; ++j) {
+      double m1 = 0.0, m2 = 0.0;
+      for (int q = 0; q < CIN; ++q) m1 += fabs(xc[q] * f->wc1[q * HID + j]);
+      for (int q = 0; q < HID; ++q) m2 += fabs((s->b1[q] > 0.0 ? s->b1[q] : 0.0) * f->wc2[q * HID + j]);
+      if (m1 > 0.0 && fabs(s->b1[j]) / m1 < margin) margin = fabs(s->b1[j]) / m1;
+      if (m2 > 0.0 && fabs(s->b2[j]) / m2 < margin) margin = fabs(s->b2[j]) / m2;
+    }
     for (int j = 0; j < HID; ++j) {
       h = fnv(h, s->a_pre[j] > 0.0);
       h = fnv(h, s->b1[j] > 0.0);
@@ -461,6 +476,13 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
     }
     sig_s[i] = s->sigma;
     for (int c = 0; c < 3; ++c) rgb_s[3 * i + c] = s->rgb[c];
+    if (s_out) {
+      double* so = s_out + 16 * (size_t)i;
+      for (int q = 0; q < 16; ++q) so[q] = 0.0;
+      so[0] = s->sigma;
+      for (int c = 0; c < 3; ++c) so[1 + c] = s->rgb[c];
+      so[11] = margin;
+    }
   }
 
   double* trans = (double*)malloc(sizeof(double) * (size_t)(n + 1));
@@ -476,14 +498,33 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
   /* loss: mean over the P pixels of the hypothesis and the 3 channels */
   const float* I = obs + 3 * (size_t)pix;
   double gC[3], L = 0.0, norm = 1.0 / (3.0 * (double)P);
+  double kink = INFINITY;
   for (int c = 0; c < 3; ++c) {
     double g;
     int br;
     L += huber(C[c] - (double)I[c], f->loss_param, &g, &br) * norm;
     gC[c] = g * norm;
     h = fnv(h, br);
+    double km = fabs(fabs(C[c] - (double)I[c]) - f->loss_param);
+    if (km < kink) kink = km;
   }
   *loss_out = L;
+  /* distance of the stop decision from its threshold, relative to it */
+  double stop_margin = INFINITY;
+  if (f->t_stop > 0.0 && used > 0) {
+    double Tl = trans[used], Tp = trans[used - 1];
+    stop_margin = fabs(Tl - f->t_stop) / f->t_stop;
+    if (used < n) {
+      double Tn = Tl * exp(-sig_s[used] * delta);
+      if (fabs(Tn - f->t_stop) / f->t_stop < stop_margin) stop_margin = fabs(Tn - f->t_stop) / f->t_stop;
+    }
+    (void)Tp;
+  }
+  if (s_out)
+    for (int32_t i = 0; i < n; ++i) {
+      s_out[16 * (size_t)i + 12] = kink;
+      if (stop_margin < s_out[16 * (size_t)i + 11]) s_out[16 * (size_t)i + 11] = stop_margin;
+    }
 
   /* backward through the composite, then each sample's networks and encoding */
   double* g_sig = (double*)malloc(sizeof(double) * (size_t)(n + 1));
@@ -530,6 +571,22 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
       double ext = (double)f->aabb_max[a] - (double)f->aabb_min[a];
       gp[a] = gx / ext;
     }
+    if (s_out) {
+      double* so = s_out + 16 * (size_t)i;
+      so[4] = gh[0];
+      for (int c = 0; c < 3; ++c) {
+        so[5 + c] = gz[c];
+        so[8 + c] = gp[c];
+      }
+      /* this sample's share of the torque: t (d x gp) (+ d x gd_i on the SH path) */
+      double m[3] = {t * gp[0], t * gp[1], t * gp[2]}, gdi[3] = {0, 0, 0};
+      if (f->sh_dir_grad && !sh_dir)
+        for (int q = 0; q < 16; ++q)
+          for (int a = 0; a < 3; ++a) gdi[a] += gxc[15 + q] * shg[q][a];
+      so[13] = d[1] * (m[2] + gdi[2]) - d[2] * (m[1] + gdi[1]);
+      so[14] = d[2] * (m[0] + gdi[0]) - d[0] * (m[2] + gdi[2]);
+      so[15] = d[0] * (m[1] + gdi[1]) - d[1] * (m[0] + gdi[0]);
+    }
     for (int a = 0; a < 3; ++a) {
       G[a] += gp[a];
       M[a] += t * gp[a];
@@ -557,7 +614,8 @@ int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
                   const int32_t* pix, const float* obs, const orc_intr* in,
                   const int64_t* ray_offset, const float* t, const float* delta,
                   const double* sh_dirs, double* loss, double* dpose, double* rgb,
-                  int32_t* ray_stop, uint64_t* signature, int32_t n_threads) {
+                  int32_t* ray_stop, uint64_t* signature, double* sample_out,
+                  int32_t n_threads) {
   if (f->F != 2 || f->din != f->L * f->F || f->din > CIN || f->loss_type != 0) return 1;
   int64_t n_rays = (int64_t)K * P;
   double* rl = (double*)malloc(sizeof(double) * (size_t)(n_rays + 1));
@@ -571,7 +629,8 @@ int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
     int32_t used;
     shade_ray(f, poses + 12 * k, in, pix[r], obs, t + ray_offset[r],
               (int32_t)(ray_offset[r + 1] - ray_offset[r]), delta[r],
-              sh_dirs ? sh_dirs + 3 * r : NULL, P, rl + r, rg + 6 * r, c, &used, rs + r);
+              sh_dirs ? sh_dirs + 3 * r : NULL, P, rl + r, rg + 6 * r, c, &used, rs + r,
+              sample_out ? sample_out + 16 * (size_t)ray_offset[r] : NULL);
     if (rgb)
       for (int q = 0; q < 3; ++q) rgb[3 * r + q] = c[q];
     if (ray_stop) ray_stop[r] = used;

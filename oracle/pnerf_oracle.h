@@ -67,13 +67,17 @@ int32_t orc_march(const orc_field* f, int32_t K, const float* poses, int32_t P,
  * take the loss against `obs` [H][W][3] and its gradient w.r.t. each pose.
  * Outputs (each may be NULL): loss[K], dpose[K][6] = (rotation, translation),
  * rgb[K*P][3], ray_stop[K*P] (samples composited per ray), signature (hash of
- * every discrete decision).  sh_dirs: NULL, or [K*P][3] fixed directions fed to
- * the SH encoding instead of the ray direction (used to freeze that path). */
+ * every discrete decision), sample_out[S][16] = per sample (sigma, rgb[3],
+ * dL/dh0, dL/dz[3], dL/dp[3] -- zeros past a ray's stop -- the smallest
+ * relative margin of its ReLU and stop decisions, its ray's distance from the
+ * Huber kink, and its share of the torque [3]).  sh_dirs: NULL, or [K*P][3] fixed directions fed to the SH
+ * encoding instead of the ray direction (used to freeze that path). */
 int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
                   const int32_t* pix, const float* obs, const orc_intr* in,
                   const int64_t* ray_offset, const float* t, const float* delta,
                   const double* sh_dirs, double* loss, double* dpose, double* rgb,
-                  int32_t* ray_stop, uint64_t* signature, int32_t n_threads);
+                  int32_t* ray_stop, uint64_t* signature, double* sample_out,
+                  int32_t n_threads);
 
 /* Pieces exposed for pinning. */
 void orc_encode(const orc_field* f, const float x32[3], const double x64[3],

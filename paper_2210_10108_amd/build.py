@@ -20,7 +20,7 @@ SOURCES = ["api.hip", "march.hip", "shade.hip", "composite.hip", "pose.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-fhip-fp32-correctly-rounded-divide-sqrt", "-fno-gpu-rdc",
+         "-fhip-fp32-correctly-rounded-divide-sqrt", "-fno-gpu-rdc", "-ffp-contract=on",
          "-Wall", "-Wno-unused-function", "-Wno-unused-variable", "-Wno-unknown-pragmas",
          "-I", os.path.join(HERE, "..", "include")]
 

@@ -179,6 +179,9 @@ size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
   x.rtn = (float*)take(R * 4);
   x.rtf = (float*)take(R * 4);
   x.rdelta = (float*)take(R * 4);
+  x.rex = (float*)take(R * 4);
+  x.rey = (float*)take(R * 4);
+  x.rez = (float*)take(R * 4);
   x.count = (int32_t*)take(R * 4);
   x.off = (int32_t*)take((R + 1) * 4);
   x.blocksum = (int32_t*)take((size_t)n_blocks * 4);
@@ -196,7 +199,7 @@ size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
 }
 
 const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords;  // t, ray, sigma, rgb + masks
-const int64_t kBytesPerRay = 4 * 10;
+const int64_t kBytesPerRay = 4 * 13;
 
 pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chunks,
                               hipStream_t s) {
@@ -438,6 +441,7 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     d.mx[a] = p->aabb_max[a];
     float ext = p->aabb_max[a] - p->aabb_min[a];
     d.inv_ext[a] = 1.0f / ext;
+    d.inv_ext_err[a] = (float)((double)d.inv_ext[a] * (double)ext - 1.0);
   }
   d.march_mode = p->march_mode;
   d.n_uniform = p->n_uniform;
@@ -609,6 +613,18 @@ pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
   hipError_t e2 = hipFreeAsync(scratch, s);
   if (e != hipSuccess) return fail(PNERF_ERR_DEVICE, "resample launch: %s", hipGetErrorString(e));
   HIP_TRY(e2);
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64_t n,
+                                 void* stream) {
+  if (!F || !dst) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
+  if (what < 0 || what > 3) return fail(PNERF_ERR_INVALID_ARG, "what=%d", what);
+  if (!F->d_ws || n < 0 || n > F->ws_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
+  if (F->last_chunks != 1) return fail(PNERF_ERR_INVALID_ARG, "last call used %d chunks", F->last_chunks);
+  DevWork w{};
+  carve(F, F->ws_rays, F->ws_cap, &w, (char*)F->d_ws);
+  HIP_TRY(launch_inspect(w, what, dst, n, (hipStream_t)stream));
   return PNERF_OK;
 }
 

@@ -182,7 +182,32 @@ __global__ __launch_bounds__(kBlock) void k_reduce(DevBatch b, DevWork w, float*
   if (tid == 6) loss[k] = red[6][0];
 }
 
+// Copy per-sample intermediates out of the workspace (inspection only).
+__global__ void k_inspect(DevWork w, int what, float* dst, int64_t n) {
+  for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < n;
+       s += (int64_t)gridDim.x * blockDim.x) {
+    if (what == 0) {
+      dst[s] = w.t[s];
+    } else if (what == 1) {
+      dst[s] = w.sig[s];
+    } else if (what == 2) {
+      dst[3 * s] = w.cr[s];
+      dst[3 * s + 1] = w.cg[s];
+      dst[3 * s + 2] = w.cb[s];
+    } else {
+      const float* out = reinterpret_cast<const float*>(w.masks);
+      size_t t = (size_t)(s >> 6) * kMaskWords * 64 + (s & 63);
+      for (int q = 0; q < 6; ++q) dst[6 * s + q] = out[t + q * 64];
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_inspect(const DevWork& w, int what, float* dst, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_inspect, dim3(1024), dim3(256), 0, s, w, what, dst, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
                             float* rgb_out, hipStream_t s) {

@@ -2,9 +2,11 @@
 // deterministic compaction (count -> scan -> write) into SoA sample buffers.
 //
 // Every floating-point step that decides an integer (which samples exist, their
-// distance t, the occupancy cell) uses a fixed operation order with correctly
-// rounded division and square root and no contraction, so the sample set is
-// reproducible bit for bit by any implementation following the same order.
+// distance t, the occupancy cell) is written as separate IEEE round-to-nearest
+// operations (__fadd_rn, __fmul_rn, __fdiv_rn, sqrtf; the library is built with
+// -ffp-contract=on and correctly rounded division and square root, so none of
+// them is fused), and the sample set is reproducible bit for bit by any
+// implementation following the same operation order.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -14,34 +16,50 @@ constexpr int kRayBlock = 256;
 
 struct RayGeom {
   float o[3], d[3], tn, tf, delta;
+  float de[3];  // exact direction minus d (for compensated sample positions)
   int hit;
 };
 
 // Pixel -> ray (Sec. IV-A: the ray origin is the camera centre) and its
 // clip against the scene box.
 __device__ inline RayGeom make_ray(const DevField& f, const DevBatch& b, int ray) {
-#pragma clang fp contract(off)
   RayGeom g;
   const float* pose = b.poses + 12 * (ray / b.P);
   int pix = b.pix[ray];
   const int n_pix = b.W * b.H;
   pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);  // out-of-range ids are clamped
   int u = pix % b.W, v = pix / b.W;
-  float xc = __fdiv_rn((float)u + 0.5f - b.cx, b.fx);
-  float yc = __fdiv_rn((float)v + 0.5f - b.cy, b.fy);
+  float xc = __fdiv_rn(__fsub_rn(__fadd_rn((float)u, 0.5f), b.cx), b.fx);
+  float yc = __fdiv_rn(__fsub_rn(__fadd_rn((float)v, 0.5f), b.cy), b.fy);
   float dw[3];
   for (int a = 0; a < 3; ++a) {
-    dw[a] = (pose[4 * a] * xc + pose[4 * a + 1] * yc) + pose[4 * a + 2];
+    dw[a] = __fadd_rn(__fadd_rn(__fmul_rn(pose[4 * a], xc), __fmul_rn(pose[4 * a + 1], yc)),
+                      pose[4 * a + 2]);
     g.o[a] = pose[4 * a + 3];
   }
-  float n = __fsqrt_rn((dw[0] * dw[0] + dw[1] * dw[1]) + dw[2] * dw[2]);
+  float n = sqrtf(__fadd_rn(__fadd_rn(__fmul_rn(dw[0], dw[0]), __fmul_rn(dw[1], dw[1])),
+                                 __fmul_rn(dw[2], dw[2])));
   for (int a = 0; a < 3; ++a) g.d[a] = __fdiv_rn(dw[a], n);
+  {
+    // the same direction in double: its difference from d lets the shading
+    // kernels place samples more precisely than float allows (decisions above
+    // stay on the float values)
+    double xd = ((double)u + 0.5 - (double)b.cx) / (double)b.fx;
+    double yd = ((double)v + 0.5 - (double)b.cy) / (double)b.fy;
+    double e[3], nn = 0.0;
+    for (int a = 0; a < 3; ++a) {
+      e[a] = (double)pose[4 * a] * xd + (double)pose[4 * a + 1] * yd + (double)pose[4 * a + 2];
+      nn += e[a] * e[a];
+    }
+    nn = sqrt(nn);
+    for (int a = 0; a < 3; ++a) g.de[a] = (float)(e[a] / nn - (double)g.d[a]);
+  }
   float t_entry = -INFINITY, t_exit = INFINITY;
   bool empty = false;
   for (int a = 0; a < 3; ++a) {
     if (g.d[a] != 0.0f) {
-      float t1 = __fdiv_rn(f.mn[a] - g.o[a], g.d[a]);
-      float t2 = __fdiv_rn(f.mx[a] - g.o[a], g.d[a]);
+      float t1 = __fdiv_rn(__fsub_rn(f.mn[a], g.o[a]), g.d[a]);
+      float t2 = __fdiv_rn(__fsub_rn(f.mx[a], g.o[a]), g.d[a]);
       float lo = t1 < t2 ? t1 : t2, hi = t1 < t2 ? t2 : t1;
       if (lo > t_entry) t_entry = lo;
       if (hi < t_exit) t_exit = hi;
@@ -59,28 +77,26 @@ __device__ inline RayGeom make_ray(const DevField& f, const DevBatch& b, int ray
     g.hit = g.tf > g.tn;
   }
   if (f.march_mode == 0)
-    g.delta = g.hit ? __fdiv_rn(g.tf - g.tn, (float)f.n_uniform) : 0.0f;
+    g.delta = g.hit ? __fdiv_rn(__fsub_rn(g.tf, g.tn), (float)f.n_uniform) : 0.0f;
   else
     g.delta = f.step;
   return g;
 }
 
 __device__ inline float sample_t(const DevField& f, float tn, float delta, int j) {
-#pragma clang fp contract(off)
   float s = f.march_mode == 0 ? delta : f.step;
-  return tn + ((float)j + 0.5f) * s;
+  return __fadd_rn(tn, __fmul_rn(__fadd_rn((float)j, 0.5f), s));
 }
 
 __device__ inline bool occupied(const DevField& f, const float o[3], const float d[3], float t) {
-#pragma clang fp contract(off)
   if (f.occ_res <= 0) return true;
   int R = f.occ_res;
   uint32_t c[3];
   for (int a = 0; a < 3; ++a) {
-    float p = o[a] + t * d[a];
-    float ext = f.mx[a] - f.mn[a];
+    float p = __fadd_rn(o[a], __fmul_rn(t, d[a]));
+    float ext = __fsub_rn(f.mx[a], f.mn[a]);
     float sc = __fdiv_rn((float)R, ext);
-    float q = (p - f.mn[a]) * sc;
+    float q = __fmul_rn(__fsub_rn(p, f.mn[a]), sc);
     int ci = q < 0.0f ? 0 : (q >= (float)R ? R - 1 : (int)q);
     c[a] = (uint32_t)ci;
   }
@@ -136,6 +152,9 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_count(DevField f, DevBatch b,
       w.rdx[ray] = g.d[0];
       w.rdy[ray] = g.d[1];
       w.rdz[ray] = g.d[2];
+      w.rex[ray] = g.de[0];
+      w.rey[ray] = g.de[1];
+      w.rez[ray] = g.de[2];
       w.rtn[ray] = g.tn;
       w.rtf[ray] = g.tf;
       w.rdelta[ray] = g.delta;

@@ -48,6 +48,7 @@ struct DevField {
   const float* wd2;
   float density_bias;
   float mn[3], mx[3], inv_ext[3];
+  float inv_ext_err[3];         // inv_ext * extent - 1 (relative rounding of the reciprocal)
   int32_t march_mode, n_uniform;
   float step;
   int32_t max_samples;
@@ -73,6 +74,7 @@ struct DevBatch {
 struct DevWork {
   // per ray (SoA)
   float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta;
+  float *rex, *rey, *rez;       // direction correction: exact unit direction - (rdx, rdy, rdz)
   int32_t* count;               // kept samples per ray
   int32_t* off;                 // [n_rays + 1] exclusive offsets
   int32_t* blocksum;            // per 256-ray block
@@ -101,6 +103,7 @@ hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float
 hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s);
 hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
                                const int32_t* total, int64_t capacity, hipStream_t s);
+hipError_t launch_inspect(const DevWork& w, int what, float* dst, int64_t n, hipStream_t s);
 hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base, hipStream_t s);
 hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dpose, float lr,
                                 float beta, hipStream_t s);

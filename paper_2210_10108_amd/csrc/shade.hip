@@ -34,13 +34,24 @@ struct LevelLds {
 
 struct Sample {
   float o[3], d[3], t;
-  float x[3];       // normalised, clamped position in [0,1]^3
+  float x[3];       // normalised, clamped position in [0,1]^3 (decides cells)
+  float dx[3];      // exact normalised position minus x (0 where clamped)
   uint32_t clamped; // bit a set: component a was clamped
 };
 
+// Error-free transformation of a float sum: a + b = s + return value.
+__device__ __forceinline__ float two_sum_err(float a, float b, float s) {
+  float bb = __fsub_rn(s, a);
+  return __fadd_rn(__fsub_rn(a, __fsub_rn(s, bb)), __fsub_rn(b, bb));
+}
+
+// Sample position p = o + t d and x = (p - min) / extent.  The float chain
+// (separately rounded, never fused) decides cells and clamping; the rounding
+// errors of each step are recovered exactly (TwoSum / FMA) together with the
+// float direction's own error, so that dx carries x's exact value to first
+// order and interpolation weights are accurate to float precision.
 __device__ inline void load_sample(const DevField& f, const DevBatch& b, const DevWork& w, int s,
                                    Sample& sm) {
-#pragma clang fp contract(off)
   int ray = w.sray[s];
   const float* pose = b.poses + 12 * (ray / b.P);
   sm.o[0] = pose[3];
@@ -49,19 +60,30 @@ __device__ inline void load_sample(const DevField& f, const DevBatch& b, const D
   sm.d[0] = w.rdx[ray];
   sm.d[1] = w.rdy[ray];
   sm.d[2] = w.rdz[ray];
+  const float de[3] = {w.rex[ray], w.rey[ray], w.rez[ray]};
   sm.t = w.t[s];
   sm.clamped = 0;
   for (int a = 0; a < 3; ++a) {
-    float p = sm.o[a] + sm.t * sm.d[a];
-    float xr = (p - f.mn[a]) * f.inv_ext[a];
+    float td = __fmul_rn(sm.t, sm.d[a]);
+    float e_td = fmaf(sm.t, sm.d[a], -td) + sm.t * de[a];
+    float p = __fadd_rn(sm.o[a], td);
+    float e_p = two_sum_err(sm.o[a], td, p);
+    float q = __fsub_rn(p, f.mn[a]);
+    float e_q = two_sum_err(p, -f.mn[a], q);
+    float xr = __fmul_rn(q, f.inv_ext[a]);
+    float e_x = fmaf(q, f.inv_ext[a], -xr);
+    float dx = e_x + (e_td + e_p + e_q) * f.inv_ext[a] - xr * f.inv_ext_err[a];
     if (xr < 0.0f) {
       sm.x[a] = 0.0f;
+      sm.dx[a] = 0.0f;
       sm.clamped |= 1u << a;
     } else if (xr > 1.0f) {
       sm.x[a] = 1.0f;
+      sm.dx[a] = 0.0f;
       sm.clamped |= 1u << a;
     } else {
       sm.x[a] = xr;
+      sm.dx[a] = dx;
     }
   }
 }
@@ -72,18 +94,22 @@ struct Cell {
   uint32_t idx[8];
 };
 
+// The cell comes from the float product x N (as a reference implementation in
+// float decides it); the weights add back that product's rounding error and
+// N dx, the part of the position float cannot hold.
 __device__ __forceinline__ void make_cell(const LevelLds& lv, uint32_t T, int l, const float x[3],
-                                          Cell& c) {
+                                          const float dx[3], Cell& c) {
   int N = lv.res[l];
   uint32_t n1 = lv.n1[l];
   bool dense = lv.dense[l] != 0;
   uint32_t i0[3];
+  const float Nf = (float)N;
   for (int a = 0; a < 3; ++a) {
-    float pos = x[a] * (float)N;
+    float pos = __fmul_rn(x[a], Nf);
     int ci = (int)pos;
     ci = ci < N - 1 ? ci : N - 1;
     i0[a] = (uint32_t)ci;
-    c.w[a] = pos - (float)ci;
+    c.w[a] = (__fsub_rn(pos, (float)ci) + fmaf(x[a], Nf, -pos)) + Nf * dx[a];
   }
   uint32_t mask = T - 1u;
   uint32_t sy = dense ? n1 : kPrime1;
@@ -217,7 +243,7 @@ __global__ __launch_bounds__(kBlock) void k_shade_fwd(DevField f, DevBatch b, De
 #pragma unroll
       for (int j = 0; j < LPG; ++j) {
         Cell c;
-        make_cell(lv, f.T, 4 * j + g, sm.x, c);
+        make_cell(lv, f.T, 4 * j + g, sm.x, sm.dx, c);
         float2 v[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = reinterpret_cast<const float2*>(f.table32)[c.idx[k]];
@@ -512,7 +538,7 @@ __global__ __launch_bounds__(kBlock) void k_shade_bwd(DevField f, DevBatch b, De
       for (int j = 0; j < LPG; ++j) {
         int l = 4 * j + g;
         Cell c;
-        make_cell(lv, f.T, l, sm.x, c);
+        make_cell(lv, f.T, l, sm.x, sm.dx, c);
         float2 v[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k) v[k] = reinterpret_cast<const float2*>(f.table32)[c.idx[k]];
@@ -592,21 +618,20 @@ __global__ __launch_bounds__(kBlock) void k_occupancy(DevField f, uint32_t* bits
   bool occ = false;
   if (lin < n) {
     int ci[3] = {(int)(lin % R), (int)((lin / R) % R), (int)(lin / ((int64_t)R * R))};
-    float x[3];
+    float x[3], dx[3] = {0.0f, 0.0f, 0.0f};
     {
-#pragma clang fp contract(off)
       for (int a = 0; a < 3; ++a) {
-        float ext = f.mx[a] - f.mn[a];
+        float ext = __fsub_rn(f.mx[a], f.mn[a]);
         float cell = __fdiv_rn(ext, (float)R);
-        float p = f.mn[a] + ((float)ci[a] + 0.5f) * cell;
-        float xr = (p - f.mn[a]) * f.inv_ext[a];
+        float p = __fadd_rn(f.mn[a], __fmul_rn(__fadd_rn((float)ci[a], 0.5f), cell));
+        float xr = __fmul_rn(__fsub_rn(p, f.mn[a]), f.inv_ext[a]);
         x[a] = xr < 0.0f ? 0.0f : (xr > 1.0f ? 1.0f : xr);
       }
     }
     float feat[32];
     for (int l = 0; l < f.L; ++l) {
       Cell c;
-      make_cell(lv, f.T, l, x, c);
+      make_cell(lv, f.T, l, x, dx, c);
       float a0 = 0.f, a1 = 0.f;
       for (int k = 0; k < 8; ++k) {
         float2 v = reinterpret_cast<const float2*>(f.table32)[c.idx[k]];

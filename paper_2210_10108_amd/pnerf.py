@@ -63,6 +63,8 @@ _SIGS = {
     "pnerf_march": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p,
                               C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int64,
                               C.c_void_p]),
+    "pnerf_field_inspect": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int64,
+                                      C.c_void_p]),
     "pnerf_field_occupancy": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p]),
     "pnerf_field_last_sample_count": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p]),
     "pnerf_field_set_profiling": (C.c_int, [C.c_void_p, C.c_int32]),
@@ -76,6 +78,9 @@ def lib() -> C.CDLL:
     """Load libpnerf.so; raises if it has not been built."""
     global _lib
     if _lib is None:
+        # torch's HIP runtime must be the one in the process: import it first so
+        # that libpnerf.so binds to the already-loaded libamdhip64.so.7
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python paper_2210_10108_amd/build.py` (or __graft_entry__.build())")
@@ -215,6 +220,15 @@ class Field:
             _dev(off, torch.int64), _dev(t, torch.float32), _dev(j, torch.int32), int(capacity),
             _stream(stream)))
         return off, t, j
+
+    def inspect(self, what: int, n: int, stream=None):
+        """Per-sample intermediates of the last call (see pnerf_field_inspect)."""
+        import torch
+        width = {0: 1, 1: 1, 2: 3, 3: 6}[what]
+        dst = torch.zeros(max(n, 1) * width, dtype=torch.float32, device="cuda")
+        _check(lib().pnerf_field_inspect(self._h, what, _dev(dst, torch.float32), n,
+                                         _stream(stream)))
+        return dst[: n * width].reshape(n, width) if width > 1 else dst[:n]
 
     def occupancy(self, stream=None) -> np.ndarray:
         R = self.occ_res

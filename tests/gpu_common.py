@@ -69,11 +69,54 @@ def rel_l2(a, b):
     return np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30)
 
 
-def assert_loss_grad_close(loss_gpu, dpose_gpu, ref, hyps=None, loss_rtol=LOSS_RTOL,
-                           grad_rtol=GRAD_RTOL):
-    hyps = range(len(ref["loss"])) if hyps is None else hyps
+# A sample whose ReLU pre-activation (or stop test) lies within this relative
+# margin of its threshold, or whose ray's residual lies this close to the Huber
+# kink, has two valid derivatives: float32 accumulation on the GPU and double in
+# the oracle may legitimately pick different sides.  Such samples are compared
+# for validity only; everything else is compared element by element.
+MARGIN_RELU = 2e-5
+MARGIN_KINK = 1e-5
+MAX_AMBIGUOUS = 0.03
+
+
+def ambiguous(samples):
+    return (samples[:, 11] < MARGIN_RELU) | (samples[:, 12] < MARGIN_KINK)
+
+
+def assert_loss_grad_close(loss_gpu, dpose_gpu, ref, hyps=None, gpu_samples=None,
+                           gpu_ranges=None, loss_rtol=LOSS_RTOL, grad_rtol=GRAD_RTOL):
+    """Per-hypothesis parity.  With per-sample GPU outputs (pnerf_field_inspect,
+    what=3: torque and force share of every sample) and the oracle's per-sample
+    outputs, the ambiguous samples' own shares are taken out of both totals
+    before comparing, and every other sample's force is compared element-wise."""
+    hyps = list(range(len(ref["loss"])) if hyps is None else hyps)
+    K_sub = len(ref["loss"])
+    off = ref["march"][0]
+    P = (len(off) - 1) // K_sub
+    stats = dict(samples=0, ambiguous=0)
     for i, k in enumerate(hyps):
         lo, lg = ref["loss"][i], float(loss_gpu[k])
         assert abs(lg - lo) <= loss_rtol * abs(lo) + 1e-12, (k, lg, lo)
-        e = rel_l2(dpose_gpu[k], ref["dpose"][i])
-        assert e <= grad_rtol, (k, e, dpose_gpu[k], ref["dpose"][i])
+        g_orc = np.asarray(ref["dpose"][i], np.float64)
+        g_gpu = np.asarray(dpose_gpu[k], np.float64)
+        if gpu_samples is not None:
+            s0, s1 = int(off[i * P]), int(off[(i + 1) * P])
+            g0, g1 = gpu_ranges[i] if gpu_ranges is not None else (s0, s1)
+            assert g1 - g0 == s1 - s0, (k, g1 - g0, s1 - s0)
+            so = ref["samples"][s0:s1]
+            sg = np.asarray(gpu_samples[g0:g1], np.float64)
+            amb = ambiguous(so)
+            stats["samples"] += s1 - s0
+            stats["ambiguous"] += int(amb.sum())
+            g_orc = g_orc - np.concatenate([so[amb, 13:16].sum(0), so[amb, 8:11].sum(0)])
+            g_gpu = g_gpu - sg[amb].sum(0)
+            ok = ~amb
+            if ok.any():
+                scale = np.abs(so[ok, 8:11]).max()
+                err = np.abs(sg[ok, 3:6] - so[ok, 8:11]).max()
+                assert err <= 2e-3 * scale, (k, "per-sample force", err, scale)
+        e = rel_l2(g_gpu, g_orc)
+        assert e <= grad_rtol, (k, e, g_gpu, g_orc)
+    if stats["samples"]:
+        assert stats["ambiguous"] <= MAX_AMBIGUOUS * stats["samples"], stats
+    return stats
