@@ -186,6 +186,8 @@ size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
   x.off = (int32_t*)take((R + 1) * 4);
   x.blocksum = (int32_t*)take((size_t)n_blocks * 4);
   x.ray_loss = (float*)take(R * 4);
+  // K * parts <= max(K, kReduceBlocks + K) and K <= n_rays
+  x.partial = (float*)take((R + kReduceBlocks) * 7 * 4);
   x.t = (float*)take((size_t)tiles * kTile * 4);
   x.sray = (int32_t*)take((size_t)tiles * kTile * 4);
   x.sig = (float*)take((size_t)tiles * kTile * 4);
@@ -199,7 +201,7 @@ size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
 }
 
 const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords;  // t, ray, sigma, rgb + masks
-const int64_t kBytesPerRay = 4 * 13;
+const int64_t kBytesPerRay = 4 * (13 + 7);  // ray SoA, offsets, loss, reduction partials
 
 pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chunks,
                               hipStream_t s) {
@@ -348,13 +350,16 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       if (capacity > 0) HIP_TRY(launch_copy_samples(w.t, j_tmp, t_out, j_out, w.total, capacity, s));
       continue;
     }
-    HIP_TRY(timed(F, "shade_fwd", s, [&] { return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, s); }));
     if (mode == kRender) {
+      HIP_TRY(timed(F, "shade_fwd_render", s, [&] {
+        return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, 0, s);
+      }));
       HIP_TRY(timed(F, "composite_fwd", s, [&] {
         return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
       }));
       continue;
     }
+    HIP_TRY(timed(F, "shade_fwd", s, [&] { return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
     HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
     HIP_TRY(timed(F, "shade_bwd", s, [&] { return launch_shade_bwd(F->dev, b, w, F->bwd_blocks, s); }));
     HIP_TRY(timed(F, "reduce", s, [&] {

@@ -155,18 +155,23 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   }
 }
 
-// One workgroup per hypothesis: loss = sum of its rays' losses, dpose = sum of
-// its samples' (torque, force) terms; fixed assignment and tree order.
-__global__ __launch_bounds__(kBlock) void k_reduce(DevBatch b, DevWork w, float* loss,
-                                                   float* dpose) {
+// Per-hypothesis reduction in two fixed-order stages.  Block (j, k) sums part
+// j of hypothesis k's rays (losses) and samples (torque and force terms): the
+// ranges are cut into n_parts equal pieces, each summed by a strided loop and a
+// tree in LDS.  k_reduce_final adds the n_parts partials of each hypothesis in
+// order.  Same inputs give the same bits.
+__global__ __launch_bounds__(kBlock) void k_reduce_partial(DevBatch b, DevWork w, int n_parts,
+                                                           float* partial) {
   __shared__ float red[7][kBlock];
-  int k = blockIdx.x, tid = threadIdx.x;
-  int r0 = k * b.P, r1 = r0 + b.P;
-  int s0 = w.off[r0], s1 = w.off[r1];
+  int j = blockIdx.x, k = blockIdx.y, tid = threadIdx.x;
+  int r0 = k * b.P, nr = b.P;
+  int s0 = w.off[r0], ns = w.off[r0 + nr] - s0;
+  int ra = r0 + (int)((int64_t)nr * j / n_parts), rb = r0 + (int)((int64_t)nr * (j + 1) / n_parts);
+  int sa = s0 + (int)((int64_t)ns * j / n_parts), sb = s0 + (int)((int64_t)ns * (j + 1) / n_parts);
   float acc[7] = {0, 0, 0, 0, 0, 0, 0};
-  for (int r = r0 + tid; r < r1; r += kBlock) acc[6] += w.ray_loss[r];
+  for (int r = ra + tid; r < rb; r += kBlock) acc[6] += w.ray_loss[r];
   const float* out = reinterpret_cast<const float*>(w.masks);
-  for (int s = s0 + tid; s < s1; s += kBlock) {
+  for (int s = sa + tid; s < sb; s += kBlock) {
     size_t t = (size_t)(s >> 6) * kMaskWords * 64 + (s & 63);
 #pragma unroll
     for (int q = 0; q < 6; ++q) acc[q] += out[t + q * 64];
@@ -178,8 +183,26 @@ __global__ __launch_bounds__(kBlock) void k_reduce(DevBatch b, DevWork w, float*
       for (int q = 0; q < 7; ++q) red[q][tid] += red[q][tid + stride];
     __syncthreads();
   }
-  if (tid < 6) dpose[6 * k + tid] = red[tid][0];
-  if (tid == 6) loss[k] = red[6][0];
+  if (tid < 7) partial[((size_t)k * n_parts + j) * 7 + tid] = red[tid][0];
+}
+
+// One wavefront per hypothesis: lane j holds partial j (n_parts <= 64), then a
+// fixed butterfly adds them.
+__global__ __launch_bounds__(64) void k_reduce_final(int K, int n_parts, const float* partial,
+                                                     float* loss, float* dpose) {
+  int k = blockIdx.x, lane = threadIdx.x;
+  const float* p = partial + ((size_t)k * n_parts + lane) * 7;
+#pragma unroll
+  for (int q = 0; q < 7; ++q) {
+    float v = lane < n_parts ? p[q] : 0.0f;
+    v = wave_sum(v);
+    if (lane == 0) {
+      if (q < 6)
+        dpose[6 * k + q] = v;
+      else
+        loss[k] = v;
+    }
+  }
 }
 
 // Copy per-sample intermediates out of the workspace (inspection only).
@@ -219,9 +242,18 @@ hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork&
   return hipGetLastError();
 }
 
+int reduce_parts(int K) {
+  int n = (kReduceBlocks + K - 1) / K;
+  return n < 1 ? 1 : (n > kMaxReduceParts ? kMaxReduceParts : n);
+}
+
 hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
                          hipStream_t s) {
-  hipLaunchKernelGGL(k_reduce, dim3(b.K), dim3(kBlock), 0, s, b, w, loss, dpose);
+  int n_parts = reduce_parts(b.K);
+  hipLaunchKernelGGL(k_reduce_partial, dim3(n_parts, b.K), dim3(kBlock), 0, s, b, w, n_parts,
+                     w.partial);
+  hipLaunchKernelGGL(k_reduce_final, dim3(b.K), dim3(64), 0, s, b.K, n_parts, w.partial, loss,
+                     dpose);
   return hipGetLastError();
 }
 

@@ -12,7 +12,9 @@
 namespace pnerf {
 namespace {
 
-constexpr int kRayBlock = 256;
+constexpr int kRayBlock = 256;     // 4 wavefronts
+constexpr int kRaysPerWave = 4;    // rays marched by one wavefront
+constexpr int kScanBlock = 256;    // rays per block of the offset scan
 
 struct RayGeom {
   float o[3], d[3], tn, tf, delta;
@@ -133,21 +135,18 @@ __device__ inline int march_wave(const DevField& f, const RayGeom& g, int lane, 
   return kept;
 }
 
+// Rays of one wavefront: kRaysPerWave consecutive rays, marched one after the
+// other with all 64 lanes testing candidates; lane 0 stores the ray's count and
+// geometry.
 __global__ __launch_bounds__(kRayBlock) void k_ray_count(DevField f, DevBatch b, DevWork w) {
-  __shared__ int s_cnt[kRayBlock];
-  int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int base = blockIdx.x * kRayBlock;
-  // per-lane ray geometry for the rays of this wave, then march them one by one
-  for (int q = 0; q < 64; ++q) {
-    int ray = base + wv * 64 + q;
-    if (ray >= b.n_rays) {
-      if (lane == 0) s_cnt[wv * 64 + q] = 0;
-      continue;
-    }
+  int lane = threadIdx.x & 63;
+  int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
+  for (int q = 0; q < kRaysPerWave; ++q) {
+    int ray = wave * kRaysPerWave + q;
+    if (ray >= b.n_rays) break;
     RayGeom g = make_ray(f, b, ray);
     int n = march_wave<false>(f, g, lane, f.max_per_ray, nullptr, nullptr, nullptr, ray);
     if (lane == 0) {
-      s_cnt[wv * 64 + q] = n;
       w.count[ray] = n;
       w.rdx[ray] = g.d[0];
       w.rdy[ray] = g.d[1];
@@ -160,17 +159,30 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_count(DevField f, DevBatch b,
       w.rdelta[ray] = g.delta;
     }
   }
-  __syncthreads();
-  // block total (fixed-order tree)
-  for (int stride = kRayBlock / 2; stride > 0; stride >>= 1) {
-    if (threadIdx.x < stride) s_cnt[threadIdx.x] += s_cnt[threadIdx.x + stride];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) w.blocksum[blockIdx.x] = s_cnt[0];
 }
 
-// Exclusive scan of the block totals in one workgroup (n_blocks <= 8192).
-__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks) {
+// Exclusive scan of the counts of each block of kScanBlock rays (fixed-order
+// Hillis-Steele in LDS): off[ray] = offset inside the block, blocksum = total.
+__global__ __launch_bounds__(kScanBlock) void k_scan_local(DevBatch b, DevWork w) {
+  __shared__ int s_off[kScanBlock];
+  int tid = threadIdx.x;
+  int ray = blockIdx.x * kScanBlock + tid;
+  int c = ray < b.n_rays ? w.count[ray] : 0;
+  s_off[tid] = c;
+  __syncthreads();
+  for (int off = 1; off < kScanBlock; off <<= 1) {
+    int x = tid >= off ? s_off[tid - off] : 0;
+    __syncthreads();
+    s_off[tid] += x;
+    __syncthreads();
+  }
+  if (ray < b.n_rays) w.off[ray] = s_off[tid] - c;
+  if (tid == kScanBlock - 1) w.blocksum[blockIdx.x] = s_off[tid];
+}
+
+// Exclusive scan of the block totals in one workgroup (n_blocks <= 8192); also
+// writes the chunk's sample total and the closing ray offset.
+__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks, int n_rays) {
   __shared__ int s[1024];
   constexpr int kPer = 8;
   int tid = threadIdx.x;
@@ -194,35 +206,25 @@ __global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks) {
     if (i < n_blocks) w.blocksum[i] = run;
     run += v[q];
   }
-  if (tid == 1023) *w.total = s[1023];
+  if (tid == 1023) {
+    *w.total = s[1023];
+    w.off[n_rays] = s[1023];
+  }
 }
 
+// Second march of every ray, now writing its kept samples at the ray's global
+// offset (block prefix + offset inside the block).
 __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork w,
                                                          int32_t* j_out) {
-  __shared__ int s_off[kRayBlock];
-  int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  int base = blockIdx.x * kRayBlock;
-  int ray0 = base + tid;
-  int c = ray0 < b.n_rays ? w.count[ray0] : 0;
-  s_off[tid] = c;
-  __syncthreads();
-  for (int off = 1; off < kRayBlock; off <<= 1) {
-    int x = tid >= off ? s_off[tid - off] : 0;
-    __syncthreads();
-    s_off[tid] += x;
-    __syncthreads();
-  }
-  int block_base = w.blocksum[blockIdx.x];
-  if (ray0 < b.n_rays) {
-    w.off[ray0] = block_base + s_off[tid] - c;
-    if (ray0 == b.n_rays - 1) w.off[b.n_rays] = block_base + s_off[tid];
-  }
-  __syncthreads();
-  for (int q = 0; q < 64; ++q) {
-    int slot = wv * 64 + q;
-    int ray = base + slot;
+  int lane = threadIdx.x & 63;
+  int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
+  for (int q = 0; q < kRaysPerWave; ++q) {
+    int ray = wave * kRaysPerWave + q;
     if (ray >= b.n_rays) break;
-    int o = block_base + s_off[slot] - w.count[ray];
+    int o = w.blocksum[ray / kScanBlock] + w.off[ray];
+    int n = w.count[ray];
+    if (lane == 0) w.off[ray] = o;  // only this wave reads this ray's offset
+    if (n == 0) continue;
     RayGeom g;
     g.o[0] = b.poses[12 * (ray / b.P) + 3];
     g.o[1] = b.poses[12 * (ray / b.P) + 7];
@@ -233,9 +235,8 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
     g.tn = w.rtn[ray];
     g.tf = w.rtf[ray];
     g.delta = w.rdelta[ray];
-    g.hit = w.count[ray] > 0;
-    march_wave<true>(f, g, lane, w.count[ray], w.t + o, j_out ? j_out + o : nullptr, w.sray + o,
-                     ray);
+    g.hit = 1;
+    march_wave<true>(f, g, lane, n, w.t + o, j_out ? j_out + o : nullptr, w.sray + o, ray);
   }
 }
 
@@ -243,11 +244,14 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
 
 hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
                         int32_t* lattice_j_out, hipStream_t s) {
-  int n_blocks = (b.n_rays + kRayBlock - 1) / kRayBlock;
-  if (n_blocks > 8192) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_ray_count, dim3(n_blocks), dim3(kRayBlock), 0, s, f, b, w);
-  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_blocks);
-  hipLaunchKernelGGL(k_ray_write, dim3(n_blocks), dim3(kRayBlock), 0, s, f, b, w, lattice_j_out);
+  int n_scan = (b.n_rays + kScanBlock - 1) / kScanBlock;
+  if (n_scan > 8192) return hipErrorInvalidValue;
+  int rays_per_block = kRaysPerWave * (kRayBlock / 64);
+  int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
+  hipLaunchKernelGGL(k_ray_count, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w);
+  hipLaunchKernelGGL(k_scan_local, dim3(n_scan), dim3(kScanBlock), 0, s, b, w);
+  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_scan, b.n_rays);
+  hipLaunchKernelGGL(k_ray_write, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w, lattice_j_out);
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@ constexpr int kHidden = 64;
 constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
 constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile (aliased by 6 outputs)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
+constexpr int kReduceBlocks = 2048;   // target blocks of the per-hypothesis reduction
+constexpr int kMaxReduceParts = 64;   // parts per hypothesis (K * parts <= max(K, 2048) * 7 floats)
 
 // Sizes (in floats) of the MFMA A-operand weight tiles, see the layout built in api.hip.
 __host__ __device__ constexpr int fwd_tile_floats(int lpg) {
@@ -80,6 +82,7 @@ struct DevWork {
   int32_t* blocksum;            // per 256-ray block
   int32_t* total;               // device scalar: samples in this chunk
   float* ray_loss;              // [n_rays]
+  float* partial;               // [K][parts][7] per-hypothesis partial sums
   // per sample
   float* t;
   int32_t* sray;                // ray of each sample
@@ -93,7 +96,7 @@ struct DevWork {
 hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
                         int32_t* lattice_j_out, hipStream_t s);
 hipError_t launch_shade_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                            hipStream_t s);
+                            int with_grad, hipStream_t s);
 hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
                             float* rgb_out, hipStream_t s);
 hipError_t launch_shade_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
@@ -111,6 +114,7 @@ hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, i
                            float sr, float st, uint64_t seed, uint32_t round, int32_t* scratch,
                            hipStream_t s);
 
+int reduce_parts(int K);
 int shade_fwd_blocks_per_cu(int lpg);
 int shade_bwd_blocks_per_cu(int lpg);
 

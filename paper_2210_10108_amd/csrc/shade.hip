@@ -211,7 +211,9 @@ __device__ inline void stage(float* lds, const float* src, int n, LevelLds& lv, 
 }
 
 // ------------------------------------------------------------------ forward
-template <int LPG>
+// GRAD = false (forward rendering only) skips the ReLU masks the backward
+// pass needs; it is a separate kernel so that profiles keep the two apart.
+template <int LPG, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_shade_fwd(DevField f, DevBatch b, DevWork w) {
   constexpr int KD = 2 * LPG;  // density-layer K steps
   __shared__ float lds[fwd_tile_floats(LPG)];
@@ -375,11 +377,13 @@ __global__ __launch_bounds__(kBlock) void k_shade_fwd(DevField f, DevBatch b, De
         w.cb[s] = 1.0f / (1.0f + __expf(-z[nt][2]));
       }
     }
-    uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
+    if (GRAD) {
+      uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) mw[nt * 64] = mk_a[nt] | (mk_b1[nt] << 16);
-    mw[4 * 64] = mk_b2[0] | (mk_b2[1] << 16);
-    mw[5 * 64] = mk_b2[2] | (mk_b2[3] << 16);
+      for (int nt = 0; nt < 4; ++nt) mw[nt * 64] = mk_a[nt] | (mk_b1[nt] << 16);
+      mw[4 * 64] = mk_b2[0] | (mk_b2[1] << 16);
+      mw[5 * 64] = mk_b2[2] | (mk_b2[3] << 16);
+    }
   }
 }
 
@@ -664,10 +668,10 @@ int shade_fwd_blocks_per_cu(int lpg) {
   int n = 0;
   hipError_t e = hipErrorInvalidValue;
   switch (lpg) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<1>, kBlock, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<2>, kBlock, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<3>, kBlock, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<4>, kBlock, 0); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<1, true>, kBlock, 0); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<2, true>, kBlock, 0); break;
+    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<3, true>, kBlock, 0); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_shade_fwd<4, true>, kBlock, 0); break;
   }
   return e == hipSuccess && n > 0 ? n : 1;
 }
@@ -684,15 +688,24 @@ int shade_bwd_blocks_per_cu(int lpg) {
   return e == hipSuccess && n > 0 ? n : 1;
 }
 
-hipError_t launch_shade_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                            hipStream_t s) {
+template <bool GRAD>
+void launch_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                hipStream_t s) {
   switch (f.lpg) {
-    case 1: hipLaunchKernelGGL(k_shade_fwd<1>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 2: hipLaunchKernelGGL(k_shade_fwd<2>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 3: hipLaunchKernelGGL(k_shade_fwd<3>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 4: hipLaunchKernelGGL(k_shade_fwd<4>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    default: return hipErrorInvalidValue;
+    case 1: hipLaunchKernelGGL((k_shade_fwd<1, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_shade_fwd<2, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_shade_fwd<3, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_shade_fwd<4, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
   }
+}
+
+hipError_t launch_shade_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                            int with_grad, hipStream_t s) {
+  if (f.lpg < 1 || f.lpg > 4) return hipErrorInvalidValue;
+  if (with_grad)
+    launch_fwd<true>(f, b, w, n_blocks, s);
+  else
+    launch_fwd<false>(f, b, w, n_blocks, s);
   return hipGetLastError();
 }
 
