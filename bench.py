@@ -26,13 +26,8 @@ sys.path.insert(0, ROOT)
 
 from paper_2210_10108_amd import synth  # noqa: E402
 
-PEAK_FP32_MFMA = 157.3e12     # dense fp32 MFMA, FLOP/s
-PEAK_HBM = 8.0e12             # bytes/s
-# algorithmic multiply-accumulates per sample (input-gradient only, frozen field):
-# density fwd 32*64 + 64*16, colour fwd 15*64 + 64*64 + 64*3 (+ SH rows 16*64 per ray),
-# and the same layers transposed backward (colour 3*64 + 64*64 + 64*15, density 16*64 + 64*32)
-MAC_FWD = 3072 + 5312
-MAC_BWD = 5248 + 3072
+PEAK_FP32_MFMA = 157.3e12     # MI355X dense fp32 MFMA, FLOP/s
+PEAK_HBM = 8.0e12             # MI355X HBM3E, bytes/s
 
 
 def parse():
@@ -44,6 +39,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (3 times), whose "
+                         "FETCH_SIZE / WRITE_SIZE calibrate the profiler's byte counters")
     return ap.parse_args()
 
 
@@ -105,6 +103,14 @@ def main():
     from paper_2210_10108_amd import pnerf
 
     dev = torch.device("cuda:0")
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     w = synth.WORKLOADS[args.workload]
     fa = synth.make_field(w, args.seed)
     spec = synth.field_spec(w, fa)        # occupancy (if any) built on the device
@@ -163,24 +169,33 @@ def main():
     field.set_profiling(False)
 
     samples_per_step = timed_samples / S
-    dom = max(prof.items(), key=lambda kv: kv[1]["avg_ms"] * kv[1]["launches"])
-    dom_name, dom_v = dom
-    if dom_name == "shade_fwd":
-        ach = samples_per_step * 2 * MAC_FWD / (dom_v["avg_ms"] * 1e-3)
-    elif dom_name == "shade_bwd":
-        ach = samples_per_step * 2 * MAC_BWD / (dom_v["avg_ms"] * 1e-3)
-    else:
-        ach = float("nan")
-    roof = {"kernel": dom_name, "bound": "mfma", "achieved": ach / 1e12, "peak": PEAK_FP32_MFMA / 1e12,
-            "unit": "TFLOP/s", "frac": ach / PEAK_FP32_MFMA, "traffic": None,
-            "avg_ms": dom_v["avg_ms"],
-            "flops_per_sample": 2 * (MAC_FWD if dom_name == "shade_fwd" else MAC_BWD)}
-    gather_bytes = 8 * w.n_levels * w.n_features * (2 if w.param_dtype == "f16" else 4)
-    enc = {}
-    for kname in ("shade_fwd", "shade_bwd"):
-        if kname in prof:
-            gbs = samples_per_step * gather_bytes / (prof[kname]["avg_ms"] * 1e-3)
-            enc[kname] = {"gather_GBps": gbs / 1e9, "frac_hbm": gbs / PEAK_HBM}
+    # roofline of every per-sample kernel: algorithmic units per sample x samples
+    # per launch / average launch time (HIP events on the call's stream)
+    elem = 2 if w.param_dtype == "f16" else 4
+    gather_bytes = 8 * w.n_levels * w.n_features * elem      # one gather pass per sample
+    din = w.n_levels * w.n_features
+    # algorithmic multiply-accumulates per sample (input gradient only, frozen
+    # field; the SH rows of the first colour layer count once per ray, not here):
+    # density din*64 + 64*16, colour 16*64 + 64*64 + 64*3; backward colour
+    # 3*64 + 64*64 + 64*15, density 16*64 + 64*din
+    mac_fwd = din * 64 + 64 * 16 + 16 * 64 + 64 * 64 + 64 * 3
+    mac_bwd = 3 * 64 + 64 * 64 + 64 * 15 + 16 * 64 + 64 * din
+    units = {"encode_fwd": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
+             "encode_bwd": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
+             "mlp_fwd": ("mfma", 2 * mac_fwd, PEAK_FP32_MFMA, "TFLOP/s", 1e12),
+             "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_FP32_MFMA, "TFLOP/s", 1e12)}
+    rooflines = {}
+    for kname, (bound, per, peak, unit, scale) in units.items():
+        if kname not in prof:
+            continue
+        launches_per_step = prof[kname]["launches"] / S
+        avg_s = prof[kname]["avg_ms"] * 1e-3
+        ach = samples_per_step / launches_per_step * per / avg_s
+        rooflines[kname] = {"bound": bound, "achieved": ach / scale, "peak": peak / scale,
+                            "unit": unit, "frac": ach / peak, "traffic": None,
+                            "avg_ms": prof[kname]["avg_ms"], "per_sample": per}
+    dom_name = max(rooflines, key=lambda k: prof[k]["avg_ms"] * prof[k]["launches"])
+    roof = dict(kernel=dom_name, **rooflines[dom_name])
 
     res = {
         "metric": "ray-samples/sec fwd+bwd to pose grads",
@@ -203,7 +218,7 @@ def main():
         "samples_per_step": samples_per_step,
         "mean_samples_per_ray": samples_per_step / w.n_rays,
         "roofline": roof,
-        "encoding_gather": enc,
+        "kernel_rooflines": rooflines,
         "kernels_avg_ms": {k: v["avg_ms"] for k, v in prof.items()},
     }
     if not args.no_cpu_baseline:

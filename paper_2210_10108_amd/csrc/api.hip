@@ -83,7 +83,7 @@ struct pnerf_field {
   int max_chunks = 0;
   int last_chunks = 0;
   int64_t budget = 0;
-  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0;
+  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0;
   // profiling
   bool profiling = false;
   std::vector<KernelStat> stats;
@@ -195,12 +195,14 @@ size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
   x.cg = (float*)take((size_t)tiles * kTile * 4);
   x.cb = (float*)take((size_t)tiles * kTile * 4);
   x.masks = (uint32_t*)take((size_t)tiles * kMaskWords * 64 * 4);
+  x.feat = (float*)take((size_t)2 * F->dev.L * tiles * kTile * 4);
+  x.gd = (float*)take((size_t)3 * tiles * kTile * 4);
   x.cap = tiles * kTile;
-  (void)F;
   return off;
 }
 
-const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords;  // t, ray, sigma, rgb + masks
+// t, ray, sigma, rgb, masks, gd (+ 2L feature rows, added per field)
+const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords + 4 * 3;
 const int64_t kBytesPerRay = 4 * (13 + 7);  // ray SoA, offsets, loss, reduction partials
 
 pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chunks,
@@ -313,7 +315,8 @@ DevBatch make_batch(int32_t K, const float* poses, int32_t P, const int32_t* pix
 // (and int32 sample indexing).
 int chunk_hyps(pnerf_field* F, int32_t K, int32_t P) {
   int64_t per_hyp = (int64_t)P * F->dev.max_per_ray;
-  int64_t by_budget = F->budget / std::max<int64_t>(1, per_hyp * kBytesPerSample + (int64_t)P * kBytesPerRay);
+  int64_t per_sample = kBytesPerSample + 8 * (int64_t)F->dev.L;
+  int64_t by_budget = F->budget / std::max<int64_t>(1, per_hyp * per_sample + (int64_t)P * kBytesPerRay);
   int64_t by_index = (((int64_t)1 << 31) - 4096) / std::max<int64_t>(1, per_hyp);
   int64_t kc = std::min<int64_t>({(int64_t)K, by_budget, by_index});
   return (int)std::max<int64_t>(kc, 0);
@@ -350,20 +353,22 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       if (capacity > 0) HIP_TRY(launch_copy_samples(w.t, j_tmp, t_out, j_out, w.total, capacity, s));
       continue;
     }
+    HIP_TRY(timed(F, "encode_fwd", s, [&] { return launch_encode_fwd(F->dev, b, w, F->enc_blocks, s); }));
     if (mode == kRender) {
-      HIP_TRY(timed(F, "shade_fwd_render", s, [&] {
-        return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, 0, s);
+      HIP_TRY(timed(F, "mlp_fwd_render", s, [&] {
+        return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 0, s);
       }));
       HIP_TRY(timed(F, "composite_fwd", s, [&] {
         return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
       }));
       continue;
     }
-    HIP_TRY(timed(F, "shade_fwd", s, [&] { return launch_shade_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
+    HIP_TRY(timed(F, "mlp_fwd", s, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
     HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
-    HIP_TRY(timed(F, "shade_bwd", s, [&] { return launch_shade_bwd(F->dev, b, w, F->bwd_blocks, s); }));
+    HIP_TRY(timed(F, "mlp_bwd", s, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, s); }));
+    HIP_TRY(timed(F, "encode_bwd", s, [&] { return launch_encode_bwd(F->dev, b, w, F->enc_blocks, s); }));
     HIP_TRY(timed(F, "reduce", s, [&] {
-      return launch_reduce(b, w, loss + k0, dpose + (size_t)6 * k0, s);
+      return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, s);
     }));
   }
   F->last_chunks = n_chunks;
@@ -387,7 +392,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   if (p->n_features != 2) return fail(PNERF_ERR_NOT_SUPPORTED, "n_features=%d (supported: 2)", p->n_features);
   if (p->log2_table_size < 4 || p->log2_table_size > 24)
     return fail(PNERF_ERR_INVALID_ARG, "log2_table_size=%d outside 4..24", p->log2_table_size);
-  if (p->param_dtype != 0) return fail(PNERF_ERR_NOT_SUPPORTED, "param_dtype=%d (fp16 storage not built)", p->param_dtype);
+  if (p->param_dtype != 0 && p->param_dtype != 1)
+    return fail(PNERF_ERR_INVALID_ARG, "param_dtype=%d (0 float32, 1 float16)", p->param_dtype);
   if (!p->level_res || !p->table || !p->w_density1 || !p->w_density2 || !p->w_color1 ||
       !p->w_color2 || !p->w_color3)
     return fail(PNERF_ERR_INVALID_ARG, "NULL field array");
@@ -439,7 +445,27 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     d.n1[l] = (uint32_t)n1;
     d.dense[l] = (p->dense_coarse_levels && n1 * n1 * n1 <= d.T) ? 1u : 0u;
   }
-  d.f16 = 0;
+  d.f16 = p->param_dtype == 1;
+  // level groups of the encoding kernels: two levels each, hashed levels spread
+  // first so that every group (and so every XCD) gets its share of them
+  {
+    std::vector<int> order;
+    for (int l = 0; l < L; ++l)
+      if (!d.dense[l]) order.push_back(l);
+    for (int l = 0; l < L; ++l)
+      if (d.dense[l]) order.push_back(l);
+    d.n_groups = L / 2;
+    for (int g = 0; g < d.n_groups; ++g) {
+      d.grp_lv[g][0] = order[g];
+      d.grp_lv[g][1] = order[g + d.n_groups];
+      // reuse the rows of the group's own d loss / d feature values for its
+      // three position-gradient partials: (l0, q0), (l0, q1), (l1, q0)
+      auto row = [&](int l, int q) { return (l % 4) * 2 * (L / 4) + (l / 4) * 2 + q; };
+      d.part_row[g][0] = row(d.grp_lv[g][0], 0);
+      d.part_row[g][1] = row(d.grp_lv[g][0], 1);
+      d.part_row[g][2] = row(d.grp_lv[g][1], 0);
+    }
+  }
   d.density_bias = p->density_bias;
   for (int a = 0; a < 3; ++a) {
     d.mn[a] = p->aabb_min[a];
@@ -469,7 +495,7 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     int64_t lat = (int64_t)std::ceil(std::sqrt(diag) / (double)p->step) + 2;
     d.max_per_ray = (int)std::min<int64_t>(lat, p->max_samples);
   }
-  F->budget = p->max_workspace_bytes > 0 ? p->max_workspace_bytes : ((int64_t)16 << 30);
+  F->budget = p->max_workspace_bytes > 0 ? p->max_workspace_bytes : ((int64_t)64 << 30);
 
   // weights -> float, then MFMA tiles
   Weights W;
@@ -510,8 +536,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   CF_TRY(hipMemcpyAsync(F->d_wd1, W.d1.data(), W.d1.size() * 4, hipMemcpyHostToDevice, s));
   CF_TRY(hipMalloc(&F->d_wd2, W.d2.size() * 4));
   CF_TRY(hipMemcpyAsync(F->d_wd2, W.d2.data(), W.d2.size() * 4, hipMemcpyHostToDevice, s));
-  d.table32 = (const float*)F->d_table;
-  d.table16 = nullptr;
+  d.table32 = p->param_dtype == 0 ? (const float*)F->d_table : nullptr;
+  d.table16 = p->param_dtype == 1 ? (const __half*)F->d_table : nullptr;
   d.wfwd = F->d_wfwd;
   d.wbwd = F->d_wbwd;
   d.wd1 = F->d_wd1;
@@ -530,8 +556,9 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   hipDeviceProp_t prop;
   CF_TRY(hipGetDeviceProperties(&prop, F->device));
   F->n_cu = prop.multiProcessorCount;
-  F->fwd_blocks = F->n_cu * shade_fwd_blocks_per_cu(d.lpg);
-  F->bwd_blocks = F->n_cu * shade_bwd_blocks_per_cu(d.lpg);
+  F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
+  F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg);
+  F->enc_blocks = encode_blocks(d, F->n_cu);
   CF_TRY(hipStreamSynchronize(s));
 #undef CF_TRY
   *out = F;
@@ -629,7 +656,8 @@ pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64
   if (F->last_chunks != 1) return fail(PNERF_ERR_INVALID_ARG, "last call used %d chunks", F->last_chunks);
   DevWork w{};
   carve(F, F->ws_rays, F->ws_cap, &w, (char*)F->d_ws);
-  HIP_TRY(launch_inspect(w, what, dst, n, (hipStream_t)stream));
+  w.total = F->d_totals;  // the single chunk of the last call
+  HIP_TRY(launch_inspect(F->dev, DevBatch{}, w, what, dst, n, (hipStream_t)stream));
   return PNERF_OK;
 }
 

@@ -155,13 +155,38 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   }
 }
 
+// Torque and force terms of one sample (Eq. 3 and Eq. 2 before the sums):
+// dL/dp_i is the fixed-order sum of the encoding groups' partials, the torque
+// t_i d x dL/dp_i (plus d x dL/dd through SH on the view-direction path).
+__device__ __forceinline__ void sample_terms(const DevField& f, const DevWork& w, int s,
+                                             float out[6]) {
+  float gp[3] = {0.f, 0.f, 0.f};
+  for (int grp = 0; grp < f.n_groups; ++grp)
+#pragma unroll
+    for (int a = 0; a < 3; ++a) gp[a] += w.feat[(int64_t)f.part_row[grp][a] * w.cap + s];
+  const int ray = w.sray[s];
+  const float d[3] = {w.rdx[ray], w.rdy[ray], w.rdz[ray]};
+  const float t = w.t[s];
+  float m[3] = {t * gp[0], t * gp[1], t * gp[2]};
+  if (f.sh_dir_grad) {
+#pragma unroll
+    for (int a = 0; a < 3; ++a) m[a] += w.gd[(int64_t)a * w.cap + s];
+  }
+  out[0] = d[1] * m[2] - d[2] * m[1];
+  out[1] = d[2] * m[0] - d[0] * m[2];
+  out[2] = d[0] * m[1] - d[1] * m[0];
+  out[3] = gp[0];
+  out[4] = gp[1];
+  out[5] = gp[2];
+}
+
 // Per-hypothesis reduction in two fixed-order stages.  Block (j, k) sums part
 // j of hypothesis k's rays (losses) and samples (torque and force terms): the
 // ranges are cut into n_parts equal pieces, each summed by a strided loop and a
 // tree in LDS.  k_reduce_final adds the n_parts partials of each hypothesis in
 // order.  Same inputs give the same bits.
-__global__ __launch_bounds__(kBlock) void k_reduce_partial(DevBatch b, DevWork w, int n_parts,
-                                                           float* partial) {
+__global__ __launch_bounds__(kBlock) void k_reduce_partial(DevField f, DevBatch b, DevWork w,
+                                                           int n_parts, float* partial) {
   __shared__ float red[7][kBlock];
   int j = blockIdx.x, k = blockIdx.y, tid = threadIdx.x;
   int r0 = k * b.P, nr = b.P;
@@ -170,11 +195,11 @@ __global__ __launch_bounds__(kBlock) void k_reduce_partial(DevBatch b, DevWork w
   int sa = s0 + (int)((int64_t)ns * j / n_parts), sb = s0 + (int)((int64_t)ns * (j + 1) / n_parts);
   float acc[7] = {0, 0, 0, 0, 0, 0, 0};
   for (int r = ra + tid; r < rb; r += kBlock) acc[6] += w.ray_loss[r];
-  const float* out = reinterpret_cast<const float*>(w.masks);
   for (int s = sa + tid; s < sb; s += kBlock) {
-    size_t t = (size_t)(s >> 6) * kMaskWords * 64 + (s & 63);
+    float o[6];
+    sample_terms(f, w, s, o);
 #pragma unroll
-    for (int q = 0; q < 6; ++q) acc[q] += out[t + q * 64];
+    for (int q = 0; q < 6; ++q) acc[q] += o[q];
   }
   for (int q = 0; q < 7; ++q) red[q][tid] = acc[q];
   __syncthreads();
@@ -206,10 +231,14 @@ __global__ __launch_bounds__(64) void k_reduce_final(int K, int n_parts, const f
 }
 
 // Copy per-sample intermediates out of the workspace (inspection only).
-__global__ void k_inspect(DevWork w, int what, float* dst, int64_t n) {
+__global__ void k_inspect(DevField f, DevWork w, int what, float* dst, int64_t n) {
+  const int64_t total = *w.total;
   for (int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; s < n;
        s += (int64_t)gridDim.x * blockDim.x) {
-    if (what == 0) {
+    if (s >= total) {  // past the last call's samples: nothing there
+      const int width = what == 2 ? 3 : (what == 3 ? 6 : 1);
+      for (int q = 0; q < width; ++q) dst[width * s + q] = 0.0f;
+    } else if (what == 0) {
       dst[s] = w.t[s];
     } else if (what == 1) {
       dst[s] = w.sig[s];
@@ -218,17 +247,19 @@ __global__ void k_inspect(DevWork w, int what, float* dst, int64_t n) {
       dst[3 * s + 1] = w.cg[s];
       dst[3 * s + 2] = w.cb[s];
     } else {
-      const float* out = reinterpret_cast<const float*>(w.masks);
-      size_t t = (size_t)(s >> 6) * kMaskWords * 64 + (s & 63);
-      for (int q = 0; q < 6; ++q) dst[6 * s + q] = out[t + q * 64];
+      float o[6];
+      sample_terms(f, w, (int)s, o);
+      for (int q = 0; q < 6; ++q) dst[6 * s + q] = o[q];
     }
   }
 }
 
 }  // namespace
 
-hipError_t launch_inspect(const DevWork& w, int what, float* dst, int64_t n, hipStream_t s) {
-  hipLaunchKernelGGL(k_inspect, dim3(1024), dim3(256), 0, s, w, what, dst, n);
+hipError_t launch_inspect(const DevField& f, const DevBatch& b, const DevWork& w, int what,
+                          float* dst, int64_t n, hipStream_t s) {
+  (void)b;
+  hipLaunchKernelGGL(k_inspect, dim3(1024), dim3(256), 0, s, f, w, what, dst, n);
   return hipGetLastError();
 }
 
@@ -247,10 +278,10 @@ int reduce_parts(int K) {
   return n < 1 ? 1 : (n > kMaxReduceParts ? kMaxReduceParts : n);
 }
 
-hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
-                         hipStream_t s) {
+hipError_t launch_reduce(const DevField& f, const DevBatch& b, const DevWork& w, float* loss,
+                         float* dpose, hipStream_t s) {
   int n_parts = reduce_parts(b.K);
-  hipLaunchKernelGGL(k_reduce_partial, dim3(n_parts, b.K), dim3(kBlock), 0, s, b, w, n_parts,
+  hipLaunchKernelGGL(k_reduce_partial, dim3(n_parts, b.K), dim3(kBlock), 0, s, f, b, w, n_parts,
                      w.partial);
   hipLaunchKernelGGL(k_reduce_final, dim3(b.K), dim3(64), 0, s, b.K, n_parts, w.partial, loss,
                      dpose);

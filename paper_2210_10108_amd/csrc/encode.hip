@@ -1,0 +1,327 @@
+// Multiresolution hash encoding of the samples (Sec. III, Instant NGP): the
+// forward gather of every level's 8 vertex features and their trilinear blend,
+// and -- backward -- the derivative of the blend with respect to the sample
+// position, contracted with d loss / d feature.  The table is frozen, so the
+// backward pass re-gathers and scatters nothing.
+//
+// Work split: the levels are partitioned into NG groups of two levels each,
+// and block b works on group b % NG.  Workgroups are dispatched round-robin
+// over the XCDs, so every XCD (own 4 MB L2) serves the same one or two level
+// groups for the whole launch and its L2 holds only those levels' tables.  One
+// thread handles one sample of its group; blocks are persistent and stride
+// over the compacted sample array.
+//
+// Features are stored SoA, row p = (l % 4) * 2 LPG + (l / 4) * 2 + q for
+// feature q of level l (the order in which the MLP kernels feed them to MFMA),
+// row stride = the workspace sample capacity.  The backward pass writes each
+// group's three position-gradient partials over the d loss / d feature rows of
+// that group's own levels (read first by the same thread).
+#include "pnerf_internal.h"
+
+namespace pnerf {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr uint32_t kPrime1 = 2654435761u, kPrime2 = 805459861u;
+
+struct Pos {
+  float x[3];        // normalised, clamped position in [0,1]^3 (decides cells)
+  float dx[3];       // exact normalised position minus x (0 where clamped)
+  uint32_t clamped;  // bit a set: component a was clamped
+};
+
+// Error-free transformation of a float sum: a + b = s + return value.
+__device__ __forceinline__ float two_sum_err(float a, float b, float s) {
+  float bb = __fsub_rn(s, a);
+  return __fadd_rn(__fsub_rn(a, __fsub_rn(s, bb)), __fsub_rn(b, bb));
+}
+
+// Sample position p = o + t d and x = (p - min) / extent.  The float chain
+// (separately rounded, never fused) decides cells and clamping; the rounding
+// errors of each step are recovered exactly (TwoSum / FMA) together with the
+// float direction's own error, so that dx carries x's exact value to first
+// order and interpolation weights are accurate to float precision.
+__device__ inline Pos sample_pos(const DevField& f, const DevBatch& b, const DevWork& w, int s) {
+  Pos ps;
+  int ray = w.sray[s];
+  const float* pose = b.poses + 12 * (ray / b.P);
+  const float o[3] = {pose[3], pose[7], pose[11]};
+  const float d[3] = {w.rdx[ray], w.rdy[ray], w.rdz[ray]};
+  const float de[3] = {w.rex[ray], w.rey[ray], w.rez[ray]};
+  const float t = w.t[s];
+  ps.clamped = 0;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    float td = __fmul_rn(t, d[a]);
+    float e_td = fmaf(t, d[a], -td) + t * de[a];
+    float p = __fadd_rn(o[a], td);
+    float e_p = two_sum_err(o[a], td, p);
+    float q = __fsub_rn(p, f.mn[a]);
+    float e_q = two_sum_err(p, -f.mn[a], q);
+    float xr = __fmul_rn(q, f.inv_ext[a]);
+    float e_x = fmaf(q, f.inv_ext[a], -xr);
+    float dx = e_x + (e_td + e_p + e_q) * f.inv_ext[a] - xr * f.inv_ext_err[a];
+    if (!(xr >= 0.0f)) {  // below the box (or NaN from a non-finite pose)
+      ps.x[a] = 0.0f;
+      ps.dx[a] = 0.0f;
+      ps.clamped |= 1u << a;
+    } else if (xr > 1.0f) {
+      ps.x[a] = 1.0f;
+      ps.dx[a] = 0.0f;
+      ps.clamped |= 1u << a;
+    } else {
+      ps.x[a] = xr;
+      ps.dx[a] = dx;
+    }
+  }
+  return ps;
+}
+
+// Cell of one level and the 8 corner table indices (in vertex units).
+struct Cell {
+  float w[3];
+  uint32_t idx[8];
+};
+
+// The cell comes from the float product x N (as a reference implementation in
+// float decides it); the weights add back that product's rounding error and
+// N dx, the part of the position float cannot hold.
+__device__ __forceinline__ void make_cell(const DevField& f, int l, const float x[3],
+                                          const float dx[3], Cell& c) {
+  const int N = f.res[l];
+  const uint32_t n1 = f.n1[l];
+  const bool dense = f.dense[l] != 0;
+  uint32_t i0[3];
+  const float Nf = (float)N;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    float pos = __fmul_rn(x[a], Nf);
+    int ci = (int)pos;
+    ci = ci < N - 1 ? ci : N - 1;
+    i0[a] = (uint32_t)ci;
+    c.w[a] = (__fsub_rn(pos, (float)ci) + fmaf(x[a], Nf, -pos)) + Nf * dx[a];
+  }
+  const uint32_t mask = f.T - 1u;
+  const uint32_t sy = dense ? n1 : kPrime1;
+  const uint32_t sz = dense ? n1 * n1 : kPrime2;
+  const uint32_t y0 = i0[1] * sy, y1 = y0 + sy;
+  const uint32_t z0 = i0[2] * sz, z1 = z0 + sz;
+  const uint32_t base = (uint32_t)l * f.T;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t xi = i0[0] + (k & 1);
+    uint32_t yi = (k & 2) ? y1 : y0;
+    uint32_t zi = (k & 4) ? z1 : z0;
+    uint32_t h = dense ? (xi + yi + zi) : ((xi ^ yi ^ zi) & mask);
+    c.idx[k] = base + h;
+  }
+}
+
+template <bool F16>
+__device__ __forceinline__ float2 vertex(const DevField& f, uint32_t idx) {
+  if (F16) {
+    __half2 v = reinterpret_cast<const __half2*>(f.table16)[idx];
+    return __half22float2(v);
+  }
+  return reinterpret_cast<const float2*>(f.table32)[idx];
+}
+
+// Feature (2 values) of level l at position x: blend of the 8 vertices.
+template <bool F16>
+__device__ __forceinline__ float2 level_feature(const DevField& f, int l, const float x[3],
+                                                const float dx[3]) {
+  Cell c;
+  make_cell(f, l, x, dx, c);
+  float2 v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, c.idx[k]);
+  const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
+  const float ux = 1.0f - wx, uy = 1.0f - wy, uz = 1.0f - wz;
+  float2 r;
+  r.x = uz * (uy * (ux * v[0].x + wx * v[1].x) + wy * (ux * v[2].x + wx * v[3].x)) +
+        wz * (uy * (ux * v[4].x + wx * v[5].x) + wy * (ux * v[6].x + wx * v[7].x));
+  r.y = uz * (uy * (ux * v[0].y + wx * v[1].y) + wy * (ux * v[2].y + wx * v[3].y)) +
+        wz * (uy * (ux * v[4].y + wx * v[5].y) + wy * (ux * v[6].y + wx * v[7].y));
+  return r;
+}
+
+__device__ __forceinline__ int feat_row(const DevField& f, int l, int q) {
+  return (l & 3) * 2 * f.lpg + (l >> 2) * 2 + q;
+}
+
+// ------------------------------------------------------------------ forward
+template <bool F16>
+__global__ __launch_bounds__(kBlock) void k_encode_fwd(DevField f, DevBatch b, DevWork w) {
+  const int S = *w.total;
+  const int grp = blockIdx.x % f.n_groups;
+  const int l0 = f.grp_lv[grp][0], l1 = f.grp_lv[grp][1];
+  const int stride = gridDim.x / f.n_groups;
+  const int64_t cap = w.cap;
+  float* r00 = w.feat + (int64_t)feat_row(f, l0, 0) * cap;
+  float* r01 = w.feat + (int64_t)feat_row(f, l0, 1) * cap;
+  float* r10 = w.feat + (int64_t)feat_row(f, l1, 0) * cap;
+  float* r11 = w.feat + (int64_t)feat_row(f, l1, 1) * cap;
+  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
+    const int s = sb * kBlock + threadIdx.x;
+    if (s >= S) break;
+    Pos ps = sample_pos(f, b, w, s);
+    float2 a = level_feature<F16>(f, l0, ps.x, ps.dx);
+    float2 c = level_feature<F16>(f, l1, ps.x, ps.dx);
+    r00[s] = a.x;
+    r01[s] = a.y;
+    r10[s] = c.x;
+    r11[s] = c.y;
+  }
+}
+
+// ----------------------------------------------------------------- backward
+// d loss / d x of one level: sum over the 8 vertices of
+// <d loss / d feature, vertex value> times the derivative of its trilinear
+// weight, times N (x is the normalised position, pos = x N).
+template <bool F16>
+__device__ __forceinline__ void level_grad(const DevField& f, int l, const float x[3],
+                                           const float dx[3], float g0, float g1, float gx[3]) {
+  Cell c;
+  make_cell(f, l, x, dx, c);
+  float2 v[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, c.idx[k]);
+  float dt[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) dt[k] = g0 * v[k].x + g1 * v[k].y;
+  const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
+  const float ux = 1.f - wx, uy = 1.f - wy, uz = 1.f - wz;
+  const float ddx = uy * uz * (dt[1] - dt[0]) + wy * uz * (dt[3] - dt[2]) +
+                    uy * wz * (dt[5] - dt[4]) + wy * wz * (dt[7] - dt[6]);
+  const float ddy = ux * uz * (dt[2] - dt[0]) + wx * uz * (dt[3] - dt[1]) +
+                    ux * wz * (dt[6] - dt[4]) + wx * wz * (dt[7] - dt[5]);
+  const float ddz = ux * uy * (dt[4] - dt[0]) + wx * uy * (dt[5] - dt[1]) +
+                    ux * wy * (dt[6] - dt[2]) + wx * wy * (dt[7] - dt[3]);
+  const float N = (float)f.res[l];
+  gx[0] += N * ddx;
+  gx[1] += N * ddy;
+  gx[2] += N * ddz;
+}
+
+// Writes this group's share of d loss / d p (world units, zero along clamped
+// components) into rows part_row[grp][0..2] (= rows of the group's own d loss /
+// d feature values, which this thread has read first).
+template <bool F16>
+__global__ __launch_bounds__(kBlock) void k_encode_bwd(DevField f, DevBatch b, DevWork w) {
+  const int S = *w.total;
+  const int grp = blockIdx.x % f.n_groups;
+  const int l0 = f.grp_lv[grp][0], l1 = f.grp_lv[grp][1];
+  const int stride = gridDim.x / f.n_groups;
+  const int64_t cap = w.cap;
+  float* g00 = w.feat + (int64_t)feat_row(f, l0, 0) * cap;
+  float* g01 = w.feat + (int64_t)feat_row(f, l0, 1) * cap;
+  float* g10 = w.feat + (int64_t)feat_row(f, l1, 0) * cap;
+  float* g11 = w.feat + (int64_t)feat_row(f, l1, 1) * cap;
+  float* out0 = w.feat + (int64_t)f.part_row[grp][0] * cap;
+  float* out1 = w.feat + (int64_t)f.part_row[grp][1] * cap;
+  float* out2 = w.feat + (int64_t)f.part_row[grp][2] * cap;
+  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
+    const int s = sb * kBlock + threadIdx.x;
+    if (s >= S) break;
+    const float a0 = g00[s], a1 = g01[s], c0 = g10[s], c1 = g11[s];
+    float gx[3] = {0.f, 0.f, 0.f};
+    Pos ps = sample_pos(f, b, w, s);
+    if (a0 != 0.0f || a1 != 0.0f || c0 != 0.0f || c1 != 0.0f) {
+      level_grad<F16>(f, l0, ps.x, ps.dx, a0, a1, gx);
+      level_grad<F16>(f, l1, ps.x, ps.dx, c0, c1, gx);
+    }
+    out0[s] = (ps.clamped & 1u) ? 0.0f : gx[0] * f.inv_ext[0];
+    out1[s] = (ps.clamped & 2u) ? 0.0f : gx[1] * f.inv_ext[1];
+    out2[s] = (ps.clamped & 4u) ? 0.0f : gx[2] * f.inv_ext[2];
+  }
+}
+
+// ---------------------------------------------------------------- occupancy
+// Occupancy grid: bit set iff the density at the cell centre exceeds `thr`.
+// One thread per cell (linear index x + R(y + Rz)), plain FMA arithmetic; run
+// once at field creation.
+template <bool F16>
+__global__ __launch_bounds__(kBlock) void k_occupancy(DevField f, uint32_t* bits, int R,
+                                                      float thr) {
+  __shared__ float s_w1[2 * kMaxLevels * kHidden];
+  __shared__ float s_w2[kHidden];
+  const int din = 2 * f.L;
+  for (int i = threadIdx.x; i < din * kHidden; i += kBlock) s_w1[i] = f.wd1[i];
+  if (threadIdx.x < kHidden) s_w2[threadIdx.x] = f.wd2[threadIdx.x * 16];
+  __syncthreads();
+  const int64_t n = (int64_t)R * R * R;
+  const int64_t lin = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  bool occ = false;
+  if (lin < n) {
+    const int ci[3] = {(int)(lin % R), (int)((lin / R) % R), (int)(lin / ((int64_t)R * R))};
+    float x[3];
+    const float dx[3] = {0.0f, 0.0f, 0.0f};
+    for (int a = 0; a < 3; ++a) {
+      float ext = __fsub_rn(f.mx[a], f.mn[a]);
+      float cell = __fdiv_rn(ext, (float)R);
+      float p = __fadd_rn(f.mn[a], __fmul_rn(__fadd_rn((float)ci[a], 0.5f), cell));
+      float xr = __fmul_rn(__fsub_rn(p, f.mn[a]), f.inv_ext[a]);
+      x[a] = xr < 0.0f ? 0.0f : (xr > 1.0f ? 1.0f : xr);
+    }
+    float feat[2 * kMaxLevels];
+    for (int l = 0; l < f.L; ++l) {
+      float2 v = level_feature<F16>(f, l, x, dx);
+      feat[2 * l] = v.x;
+      feat[2 * l + 1] = v.y;
+    }
+    float h0 = 0.0f;
+    for (int j = 0; j < kHidden; ++j) {
+      float a = 0.0f;
+      for (int i = 0; i < din; ++i) a += feat[i] * s_w1[i * kHidden + j];
+      h0 += (a > 0.0f ? a : 0.0f) * s_w2[j];
+    }
+    occ = __expf(h0 + f.density_bias) > thr;
+  }
+  const uint64_t bal = __ballot(occ);
+  const int lane = threadIdx.x & 63;
+  const int64_t word = (lin - lane) / 32 + (lane == 32 ? 1 : 0);
+  const int64_t n_words = (n + 31) / 32;
+  if ((lane == 0 || lane == 32) && word < n_words)
+    bits[word] = lane == 0 ? (uint32_t)(bal & 0xFFFFFFFFu) : (uint32_t)(bal >> 32);
+}
+
+}  // namespace
+
+int encode_blocks(const DevField& f, int n_cu) {
+  // 8 resident blocks of 256 threads per CU, rounded to a multiple of the
+  // group count and of 8 (XCDs) so that each block keeps its group's XCD
+  int unit = 8;
+  while (unit % f.n_groups) unit += 8;
+  int want = n_cu * 8;
+  return ((want + unit - 1) / unit) * unit;
+}
+
+hipError_t launch_encode_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                             hipStream_t s) {
+  if (f.f16)
+    hipLaunchKernelGGL(k_encode_fwd<true>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  else
+    hipLaunchKernelGGL(k_encode_fwd<false>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_encode_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                             hipStream_t s) {
+  if (f.f16)
+    hipLaunchKernelGGL(k_encode_bwd<true>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  else
+    hipLaunchKernelGGL(k_encode_bwd<false>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s) {
+  const int64_t n = (int64_t)R * R * R;
+  const int64_t nb = (n + kBlock - 1) / kBlock;
+  if (f.f16)
+    hipLaunchKernelGGL(k_occupancy<true>, dim3((unsigned)nb), dim3(kBlock), 0, s, f, bits, R, thr);
+  else
+    hipLaunchKernelGGL(k_occupancy<false>, dim3((unsigned)nb), dim3(kBlock), 0, s, f, bits, R, thr);
+  return hipGetLastError();
+}
+
+}  // namespace pnerf

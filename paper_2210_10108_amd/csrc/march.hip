@@ -99,7 +99,7 @@ __device__ inline bool occupied(const DevField& f, const float o[3], const float
     float ext = __fsub_rn(f.mx[a], f.mn[a]);
     float sc = __fdiv_rn((float)R, ext);
     float q = __fmul_rn(__fsub_rn(p, f.mn[a]), sc);
-    int ci = q < 0.0f ? 0 : (q >= (float)R ? R - 1 : (int)q);
+    int ci = !(q >= 0.0f) ? 0 : (q >= (float)R ? R - 1 : (int)q);  // NaN -> cell 0
     c[a] = (uint32_t)ci;
   }
   uint64_t idx = (uint64_t)c[0] + (uint64_t)R * ((uint64_t)c[1] + (uint64_t)R * c[2]);

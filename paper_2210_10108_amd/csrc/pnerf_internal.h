@@ -11,7 +11,8 @@ namespace pnerf {
 constexpr int kMaxLevels = 16;
 constexpr int kHidden = 64;
 constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
-constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile (aliased by 6 outputs)
+constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile
+constexpr int kMaxGroups = 8;      // level groups of the encoding kernels (two levels each)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
 constexpr int kReduceBlocks = 2048;   // target blocks of the per-hypothesis reduction
 constexpr int kMaxReduceParts = 64;   // parts per hypothesis (K * parts <= max(K, 2048) * 7 floats)
@@ -41,7 +42,10 @@ struct DevField {
   int32_t res[kMaxLevels];
   uint32_t dense[kMaxLevels];   // 1: vertex index i + j n1 + k n1^2
   uint32_t n1[kMaxLevels];      // res + 1
-  int32_t f16;                  // table and weights stored as fp16
+  int32_t f16;                  // table stored as fp16
+  int32_t n_groups;             // level groups (L / 2) of the encoding kernels
+  int32_t grp_lv[kMaxGroups][2];   // the two levels of each group
+  int32_t part_row[kMaxGroups][3]; // feature rows reused for the group's d loss / d p
   const float* table32;         // [L][T][2]
   const __half* table16;        // [L][T][2]
   const float* wfwd;            // forward A-operand tiles (fp32)
@@ -88,25 +92,32 @@ struct DevWork {
   int32_t* sray;                // ray of each sample
   float* sig;                   // sigma (forward) -> d loss / d h0 (after composite)
   float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
-  uint32_t* masks;              // [tiles][6][64] ReLU masks -> 6 float outputs per sample
-  int64_t cap;                  // sample capacity
+  uint32_t* masks;              // [tiles][6][64] ReLU masks
+  float* feat;                  // [2L][cap] features -> d loss / d feature -> d loss / d p partials
+  float* gd;                    // [3][cap] d loss / d direction through SH (view-direction path)
+  int64_t cap;                  // sample capacity (row stride of feat and gd)
 };
 
 // ---- launchers (all enqueue on `s`, no synchronisation)
 hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
                         int32_t* lattice_j_out, hipStream_t s);
-hipError_t launch_shade_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                            int with_grad, hipStream_t s);
+hipError_t launch_encode_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                             hipStream_t s);
+hipError_t launch_encode_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                             hipStream_t s);
+hipError_t launch_mlp_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                          int with_grad, hipStream_t s);
 hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
                             float* rgb_out, hipStream_t s);
-hipError_t launch_shade_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                            hipStream_t s);
-hipError_t launch_reduce(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
-                         hipStream_t s);
+hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                          hipStream_t s);
+hipError_t launch_reduce(const DevField& f, const DevBatch& b, const DevWork& w, float* loss,
+                         float* dpose, hipStream_t s);
 hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s);
 hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
                                const int32_t* total, int64_t capacity, hipStream_t s);
-hipError_t launch_inspect(const DevWork& w, int what, float* dst, int64_t n, hipStream_t s);
+hipError_t launch_inspect(const DevField& f, const DevBatch& b, const DevWork& w, int what,
+                          float* dst, int64_t n, hipStream_t s);
 hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base, hipStream_t s);
 hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dpose, float lr,
                                 float beta, hipStream_t s);
@@ -115,7 +126,8 @@ hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, i
                            hipStream_t s);
 
 int reduce_parts(int K);
-int shade_fwd_blocks_per_cu(int lpg);
-int shade_bwd_blocks_per_cu(int lpg);
+int mlp_fwd_blocks_per_cu(int lpg);
+int mlp_bwd_blocks_per_cu(int lpg);
+int encode_blocks(const DevField& f, int n_cu);
 
 }  // namespace pnerf

@@ -86,6 +86,10 @@ def test_host_validation_rejects_bad_arguments(pn):
     p.n_levels = 4
     p.log2_table_size = 30
     assert L.pnerf_create_field(C.byref(p), None, C.byref(out)) == pn.ERR_INVALID_ARG
+    p.log2_table_size = 12
+    p.param_dtype = 2
+    assert L.pnerf_create_field(C.byref(p), None, C.byref(out)) == pn.ERR_INVALID_ARG
+    assert b"param_dtype" in L.pnerf_last_error()
 
 
 def test_product_path_does_not_reference_the_oracle():

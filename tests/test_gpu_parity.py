@@ -240,7 +240,7 @@ def test_loss_grad_chunked_matches_single_chunk(pn):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     l1, g1, _ = run_loss_grad(pn, case, obs)
-    l2, g2, _ = run_loss_grad(pn, case, obs, max_ws=500_000)  # forces one hypothesis per chunk
+    l2, g2, _ = run_loss_grad(pn, case, obs, max_ws=1_000_000)  # forces one hypothesis per chunk
     assert np.allclose(l1, l2, rtol=1e-5) and np.allclose(g1, g2, rtol=1e-4, atol=1e-9)
 
 
@@ -318,3 +318,62 @@ def test_device_occupancy_build_matches_oracle(pn):
         feat, _ = of.encode(c.astype(np.float32), c)
         s = math.exp(of.density_mlp(feat)[0] - 1.0)
         assert abs(s - thr) <= 1e-5 * thr
+
+
+# ----------------------------------------------------- fp16 storage, large scene
+def f16_case(name, **kw):
+    """A workload's case with the hash table and MLP weights stored in fp16."""
+    case = G.make_case(name, **kw)
+    sp = case.spec
+    h = lambda a: np.asarray(a).astype(np.float16)
+    spec = dataclasses.replace(sp, param_dtype="f16", table=h(sp.table),
+                               w_density1=h(sp.w_density1), w_density2=h(sp.w_density2),
+                               w_color1=h(sp.w_color1), w_color2=h(sp.w_color2),
+                               w_color3=h(sp.w_color3))
+    return dataclasses.replace(case, spec=spec)
+
+
+@pytest.mark.parametrize("overrides", [dict(), dict(sh_dir_grad=1)])
+def test_loss_grad_tiny_fp16_storage(pn, overrides):
+    case = f16_case("tiny32", **overrides)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, ex = check_full(pn, case, obs, ref)
+    assert stats["samples"] == int(ref["march"][0][-1])
+
+
+def with_oracle_occupancy(case, R, thr):
+    of0 = O.OracleField(dataclasses.replace(case.spec, occ_res=0, occ_bits=None))
+    bits = of0.build_occupancy(R, thr)
+    return dataclasses.replace(case, spec=dataclasses.replace(case.spec, occ_bits=bits))
+
+
+def check_sampled_hypotheses(pn, case, hyps):
+    """The whole batch on the GPU (chunked over hypotheses as the library
+    decides), the oracle on a few hypotheses; per-hypothesis loss and gradient."""
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix[hyps], case.intr)
+    ref = oracle_subset(of, case, obs, hyps)
+    loss, dpose, n = run_loss_grad(pn, case, obs)
+    G.assert_loss_grad_close(loss, dpose, ref, hyps=hyps)
+    return n
+
+
+def test_loss_grad_cam640_f16_full_batch_sampled_hypotheses(pn):
+    # 256 x 2048 rays, 640x480 camera with principal point (325.3, 242.0),
+    # table and weights in fp16, 128^3 occupancy, lattice marching with early stop
+    w = synth.WORKLOADS["cam640_f16_occ128"]
+    case = with_oracle_occupancy(G.make_case("cam640_f16_occ128"), w.occ_res, w.occ_threshold)
+    assert case.spec.table.dtype == np.float16
+    n = check_sampled_hypotheses(pn, case, [0, 128, 255])
+    assert n > 10_000_000
+
+
+def test_loss_grad_large_scene_full_batch_sampled_hypotheses(pn):
+    # 1024 x 512 rays in the [-2,2]^3 box, T = 2^21, 256^3 occupancy, up to 2048
+    # samples per ray (processed in several hypothesis chunks)
+    w = synth.WORKLOADS["large4m_occ256"]
+    case = with_oracle_occupancy(G.make_case("large4m_occ256"), w.occ_res, w.occ_threshold)
+    n = check_sampled_hypotheses(pn, case, [0, 511, 1023])
+    assert n > 100_000_000
