@@ -180,8 +180,7 @@ def main():
     # 3*64 + 64*64 + 64*15, density 16*64 + 64*din
     mac_fwd = din * 64 + 64 * 16 + 16 * 64 + 64 * 64 + 64 * 3
     mac_bwd = 3 * 64 + 64 * 64 + 64 * 15 + 16 * 64 + 64 * din
-    units = {"encode_fwd": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
-             "encode_bwd": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
+    units = {"encode": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
              "mlp_fwd": ("mfma", 2 * mac_fwd, PEAK_FP32_MFMA, "TFLOP/s", 1e12),
              "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_FP32_MFMA, "TFLOP/s", 1e12)}
     rooflines = {}

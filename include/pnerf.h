@@ -21,9 +21,13 @@
  *  - Array arguments marked (device) are device pointers owned by the caller;
  *    they must stay valid until the work queued on `stream` has finished.
  *    Arguments marked (host) are read before the call returns.
- *  - `stream` is a hipStream_t (NULL = the default stream).  Every call only
- *    enqueues work on it and returns without synchronising, except
- *    pnerf_create_field and the pnerf_field_* queries, which synchronise it.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  pnerf_step_momentum
+ *    and pnerf_resample_hypotheses only enqueue work and return.  The calls that
+ *    render (pnerf_render_loss_grad, pnerf_render, pnerf_march) synchronise the
+ *    stream once per 2^21 rays: after counting every ray's samples they read the
+ *    per-hypothesis sample counts back, size the workspace to them and cut the
+ *    batch into chunks of whole hypotheses, then enqueue the rest and return.
+ *    pnerf_create_field and pnerf_field_occupancy synchronise the stream.
  *  - Arguments are validated on the host before anything is enqueued; a
  *    failed validation returns PNERF_ERR_INVALID_ARG (or NOT_SUPPORTED) and
  *    enqueues nothing.  HIP errors map to PNERF_ERR_DEVICE.  The message of
@@ -117,8 +121,10 @@ typedef struct {
   int32_t loss_type;            /* 0 = Huber */
   float loss_param;             /* Huber threshold > 0 */
   int32_t sh_dir_grad;          /* 0 or 1 */
-  int64_t max_workspace_bytes;  /* sample-buffer budget; 0 = 16 GiB.  Larger
-                                   batches are processed in hypothesis chunks. */
+  int64_t max_workspace_bytes;  /* workspace budget; 0 = 96 GiB.  A batch whose
+                                   samples need more is processed in chunks of
+                                   whole hypotheses (about 48 + 32 L bytes per
+                                   sample). */
 } pnerf_field_params;
 
 /* Create a field: validates `params`, copies every array to the device (builds
@@ -179,14 +185,14 @@ pnerf_status pnerf_render(pnerf_field* field, int32_t K, const float* poses, int
  * float32 and lattice_j (device) int32 [capacity] receive each sample's
  * distance and lattice / segment index; otherwise only ray_offset is written
  * and the call still returns PNERF_OK (compare the total with capacity).
- * Requires the batch to fit one workspace chunk (else PNERF_ERR_CAPACITY). */
+ * Requires K*P <= 2^21 (else PNERF_ERR_CAPACITY). */
 pnerf_status pnerf_march(pnerf_field* field, int32_t K, const float* poses, int32_t P,
                          const int32_t* pixel_ids, const pnerf_intrinsics* intr,
                          int64_t* ray_offset, float* t, int32_t* lattice_j, int64_t capacity,
                          void* stream);
 
 /* Per-sample intermediates of the last call on this field (inspection; the
- * batch must have fitted one workspace chunk).  `dst` (device) receives
+ * last call must have run as one chunk, else PNERF_ERR_INVALID_ARG).  `dst` (device) receives
  * float32 values for the first n samples (n = the last call's sample total):
  *   what 0: t [n]
  *   what 1: after pnerf_render sigma [n]; after pnerf_render_loss_grad dL/dh_0 [n]
@@ -202,7 +208,8 @@ pnerf_status pnerf_field_inspect(pnerf_field* field, int32_t what, float* dst, i
 pnerf_status pnerf_field_occupancy(pnerf_field* field, uint32_t* bits_host, void* stream);
 
 /* Total number of samples processed by the last render_loss_grad / render /
- * march call on this field (sum over hypothesis chunks); synchronises `stream`. */
+ * march call on this field (sum over hypothesis chunks; known on the host, so
+ * `stream` is not used). */
 pnerf_status pnerf_field_last_sample_count(pnerf_field* field, int64_t* count, void* stream);
 
 /* Per-kernel timing with HIP events recorded on the call's stream around every

@@ -74,14 +74,19 @@ struct pnerf_field {
   float* d_wd2 = nullptr;
   uint32_t* d_occ = nullptr;
   int64_t occ_words = 0;
-  // workspace
-  void* d_ws = nullptr;
-  size_t ws_bytes = 0;
-  int ws_rays = 0;
-  int64_t ws_cap = 0;
-  int32_t* d_totals = nullptr;  // per-chunk sample totals
+  // workspace: per-ray arrays of one counted batch, per-sample arrays of one chunk
+  void* d_rays = nullptr;
+  size_t rays_bytes = 0;
+  int rays_cap = 0;
+  void* d_samp = nullptr;
+  size_t samp_bytes = 0;
+  int64_t samp_cap = 0;
+  int32_t* d_totals = nullptr;  // [max_chunks] sample totals of the chunks, + 1 counted total
   int max_chunks = 0;
+  int32_t* h_hyp = nullptr;     // pinned host copy of the per-hypothesis sample counts
+  int h_hyp_cap = 0;
   int last_chunks = 0;
+  int64_t last_total = 0;
   int64_t budget = 0;
   int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0;
   // profiling
@@ -160,53 +165,142 @@ void build_bwd_tiles(const Weights& W, int lpg, std::vector<float>& t) {
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace layout for n_rays rays and cap samples.
-size_t carve(pnerf_field* F, int n_rays, int64_t cap, DevWork* w, char* base) {
+struct Carver {
+  char* base;
   size_t off = 0;
-  auto take = [&](size_t bytes) {
-    char* p = base ? base + off : nullptr;
-    off += align_up(bytes);
+  template <class T>
+  T* take(size_t n) {
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += align_up(n * sizeof(T));
     return p;
-  };
-  size_t R = (size_t)n_rays;
-  int n_blocks = (n_rays + 255) / 256;
-  int64_t tiles = (cap + kTile - 1) / kTile;
-  DevWork tmp{};
-  DevWork& x = w ? *w : tmp;
-  x.rdx = (float*)take(R * 4);
-  x.rdy = (float*)take(R * 4);
-  x.rdz = (float*)take(R * 4);
-  x.rtn = (float*)take(R * 4);
-  x.rtf = (float*)take(R * 4);
-  x.rdelta = (float*)take(R * 4);
-  x.rex = (float*)take(R * 4);
-  x.rey = (float*)take(R * 4);
-  x.rez = (float*)take(R * 4);
-  x.count = (int32_t*)take(R * 4);
-  x.off = (int32_t*)take((R + 1) * 4);
-  x.blocksum = (int32_t*)take((size_t)n_blocks * 4);
-  x.ray_loss = (float*)take(R * 4);
+  }
+};
+
+// Per-ray arrays for n_rays rays (one counted batch).  `offc` receives the
+// sample chunks' own exclusive offsets.
+struct RayWs {
+  float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta, *rex, *rey, *rez;
+  int32_t *count, *off, *offc, *blocksum, *hyp_total;
+  float *ray_loss, *partial;
+};
+
+size_t carve_rays(int n_rays, RayWs* r, char* base) {
+  Carver c{base};
+  const size_t R = (size_t)n_rays;
+  RayWs tmp{};
+  RayWs& x = r ? *r : tmp;
+  x.rdx = c.take<float>(R);
+  x.rdy = c.take<float>(R);
+  x.rdz = c.take<float>(R);
+  x.rtn = c.take<float>(R);
+  x.rtf = c.take<float>(R);
+  x.rdelta = c.take<float>(R);
+  x.rex = c.take<float>(R);
+  x.rey = c.take<float>(R);
+  x.rez = c.take<float>(R);
+  x.count = c.take<int32_t>(R);
+  x.off = c.take<int32_t>(R + 1);
+  x.offc = c.take<int32_t>(R + 1);
+  x.blocksum = c.take<int32_t>((R + 255) / 256);
+  x.hyp_total = c.take<int32_t>(R);
+  x.ray_loss = c.take<float>(R);
   // K * parts <= max(K, kReduceBlocks + K) and K <= n_rays
-  x.partial = (float*)take((R + kReduceBlocks) * 7 * 4);
-  x.t = (float*)take((size_t)tiles * kTile * 4);
-  x.sray = (int32_t*)take((size_t)tiles * kTile * 4);
-  x.sig = (float*)take((size_t)tiles * kTile * 4);
-  x.cr = (float*)take((size_t)tiles * kTile * 4);
-  x.cg = (float*)take((size_t)tiles * kTile * 4);
-  x.cb = (float*)take((size_t)tiles * kTile * 4);
-  x.masks = (uint32_t*)take((size_t)tiles * kMaskWords * 64 * 4);
-  x.feat = (float*)take((size_t)2 * F->dev.L * tiles * kTile * 4);
-  x.gd = (float*)take((size_t)3 * tiles * kTile * 4);
-  x.cap = tiles * kTile;
-  return off;
+  x.partial = c.take<float>((R + kReduceBlocks) * 7);
+  return c.off;
 }
 
-// t, ray, sigma, rgb, masks, gd (+ 2L feature rows, added per field)
-const int64_t kBytesPerSample = 4 * 6 + 4 * kMaskWords + 4 * 3;
-const int64_t kBytesPerRay = 4 * (13 + 7);  // ray SoA, offsets, loss, reduction partials
+// Per-sample arrays for cap samples (one chunk); cap is a multiple of kTile.
+size_t carve_samples(const DevField& f, int64_t cap, DevWork* w, char* base) {
+  Carver c{base};
+  const size_t n = (size_t)cap;
+  DevWork tmp{};
+  DevWork& x = w ? *w : tmp;
+  x.t = c.take<float>(n);
+  x.sray = c.take<int32_t>(n);
+  x.sig = c.take<float>(n);
+  x.cr = c.take<float>(n);
+  x.cg = c.take<float>(n);
+  x.cb = c.take<float>(n);
+  x.masks = c.take<uint32_t>(n / kTile * kMaskWords * 64);
+  x.feat = c.take<float>((size_t)std::max(2 * f.L, 6) * n);
+  x.jac = c.take<float>((size_t)6 * f.L * n);
+  x.cap = cap;
+  return c.off;
+}
 
-pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chunks,
-                              hipStream_t s) {
+// Device views: the counted batch (all per-ray arrays from ray 0) and one
+// sample chunk (per-ray arrays from the chunk's first ray, its own offsets).
+DevWork counted_work(pnerf_field* F) {
+  RayWs r{};
+  carve_rays(F->rays_cap, &r, (char*)F->d_rays);
+  DevWork w{};
+  w.rdx = r.rdx; w.rdy = r.rdy; w.rdz = r.rdz;
+  w.rtn = r.rtn; w.rtf = r.rtf; w.rdelta = r.rdelta;
+  w.rex = r.rex; w.rey = r.rey; w.rez = r.rez;
+  w.count = r.count;
+  w.off = r.off;
+  w.blocksum = r.blocksum;
+  w.hyp_total = r.hyp_total;
+  w.ray_loss = r.ray_loss;
+  w.partial = r.partial;
+  w.total = F->d_totals + F->max_chunks;
+  return w;
+}
+
+DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id) {
+  RayWs r{};
+  carve_rays(F->rays_cap, &r, (char*)F->d_rays);
+  DevWork w{};
+  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp);
+  w.rdx = r.rdx + ray_base; w.rdy = r.rdy + ray_base; w.rdz = r.rdz + ray_base;
+  w.rtn = r.rtn + ray_base; w.rtf = r.rtf + ray_base; w.rdelta = r.rdelta + ray_base;
+  w.rex = r.rex + ray_base; w.rey = r.rey + ray_base; w.rez = r.rez + ray_base;
+  w.count = r.count + ray_base;
+  w.off = r.offc;
+  w.blocksum = nullptr;
+  w.hyp_total = nullptr;
+  w.ray_loss = r.ray_loss;
+  w.partial = r.partial;
+  w.total = F->d_totals + chunk_id;
+  return w;
+}
+
+int64_t bytes_per_sample(const DevField& f) {
+  return (int64_t)carve_samples(f, 64 * kTile, nullptr, nullptr) / (64 * kTile) + 1;
+}
+
+pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s) {
+  if (n_rays > F->rays_cap) {
+    if (F->d_rays) {
+      HIP_TRY(hipStreamSynchronize(s));
+      HIP_TRY(hipFree(F->d_rays));
+      F->d_rays = nullptr;
+      F->rays_cap = 0;
+    }
+    size_t bytes = carve_rays(n_rays, nullptr, nullptr);
+    hipError_t e = hipMalloc(&F->d_rays, bytes);
+    if (e != hipSuccess)
+      return fail(PNERF_ERR_OUT_OF_MEMORY, "ray workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
+    F->rays_bytes = bytes;
+    F->rays_cap = n_rays;
+  }
+  if (n_hyp > F->h_hyp_cap) {
+    if (F->h_hyp) {
+      HIP_TRY(hipStreamSynchronize(s));
+      HIP_TRY(hipHostFree(F->h_hyp));
+      F->h_hyp = nullptr;
+      F->h_hyp_cap = 0;
+    }
+    HIP_TRY(hipHostMalloc((void**)&F->h_hyp, sizeof(int32_t) * (size_t)n_hyp));
+    F->h_hyp_cap = n_hyp;
+  }
+  return PNERF_OK;
+}
+
+// Grow the sample workspace to hold `need` samples (a quarter more than asked
+// when it grows, within `limit`), and the per-chunk totals to n_chunks.
+pnerf_status ensure_samples(pnerf_field* F, int64_t need, int64_t limit, int n_chunks,
+                            hipStream_t s) {
   if (n_chunks > F->max_chunks) {
     if (F->d_totals) {
       HIP_TRY(hipStreamSynchronize(s));
@@ -214,27 +308,25 @@ pnerf_status ensure_workspace(pnerf_field* F, int n_rays, int64_t cap, int n_chu
       F->d_totals = nullptr;
     }
     int nc = std::max(n_chunks, 16);
-    HIP_TRY(hipMalloc(&F->d_totals, sizeof(int32_t) * nc));
+    HIP_TRY(hipMalloc(&F->d_totals, sizeof(int32_t) * (nc + 1)));
     F->max_chunks = nc;
   }
-  if (n_rays <= F->ws_rays && cap <= F->ws_cap) return PNERF_OK;
-  int nr = std::max(n_rays, F->ws_rays);
-  int64_t nc = std::max(cap, F->ws_cap);
-  size_t bytes = carve(F, nr, nc, nullptr, nullptr);
-  if (F->d_ws) {
+  need = std::max<int64_t>(need, 1);
+  if (need <= F->samp_cap) return PNERF_OK;
+  int64_t cap = std::max(need, std::min(limit, F->samp_cap + F->samp_cap / 4));
+  cap = (cap + kTile - 1) / kTile * kTile;
+  if (F->d_samp) {
     HIP_TRY(hipStreamSynchronize(s));
-    HIP_TRY(hipFree(F->d_ws));
-    F->d_ws = nullptr;
-    F->ws_bytes = 0;
-    F->ws_rays = 0;
-    F->ws_cap = 0;
+    HIP_TRY(hipFree(F->d_samp));
+    F->d_samp = nullptr;
+    F->samp_cap = 0;
   }
-  hipError_t e = hipMalloc(&F->d_ws, bytes);
+  size_t bytes = carve_samples(F->dev, cap, nullptr, nullptr);
+  hipError_t e = hipMalloc(&F->d_samp, bytes);
   if (e != hipSuccess)
-    return fail(PNERF_ERR_OUT_OF_MEMORY, "workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
-  F->ws_bytes = bytes;
-  F->ws_rays = nr;
-  F->ws_cap = nc;
+    return fail(PNERF_ERR_OUT_OF_MEMORY, "sample workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
+  F->samp_bytes = bytes;
+  F->samp_cap = cap;
   return PNERF_OK;
 }
 
@@ -311,67 +403,102 @@ DevBatch make_batch(int32_t K, const float* poses, int32_t P, const int32_t* pix
   return b;
 }
 
-// Hypotheses per chunk so that one chunk's worst-case samples fit the budget
-// (and int32 sample indexing).
-int chunk_hyps(pnerf_field* F, int32_t K, int32_t P) {
-  int64_t per_hyp = (int64_t)P * F->dev.max_per_ray;
-  int64_t per_sample = kBytesPerSample + 8 * (int64_t)F->dev.L;
-  int64_t by_budget = F->budget / std::max<int64_t>(1, per_hyp * per_sample + (int64_t)P * kBytesPerRay);
-  int64_t by_index = (((int64_t)1 << 31) - 4096) / std::max<int64_t>(1, per_hyp);
-  int64_t kc = std::min<int64_t>({(int64_t)K, by_budget, by_index});
-  return (int)std::max<int64_t>(kc, 0);
-}
-
 enum Mode { kLossGrad, kRender, kMarch };
 
+// One call: the rays of up to kMaxScanBlocks * 256 rays (whole hypotheses) are
+// counted at a time; the host reads their per-hypothesis sample counts (one
+// stream synchronisation) and cuts them into chunks of whole hypotheses whose
+// samples fit the workspace budget; every chunk then runs the write pass and
+// the shading pipeline.
 pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32_t P,
                  const int32_t* pix, const float* obs, const pnerf_intrinsics* intr, float* loss,
                  float* dpose, float* rgb, int64_t* ray_offset, float* t_out, int32_t* j_out,
                  int64_t capacity, hipStream_t s) {
   HIP_TRY(hipSetDevice(F->device));
-  int kc = chunk_hyps(F, K, P);
-  if (kc < 1)
-    return fail(PNERF_ERR_CAPACITY, "one hypothesis (%d rays x %d samples) exceeds the workspace budget",
-                P, F->dev.max_per_ray);
-  int n_chunks = (K + kc - 1) / kc;
-  if (mode == kMarch && n_chunks > 1)
-    return fail(PNERF_ERR_CAPACITY, "march inspection needs the batch in one chunk");
-  int64_t cap = (int64_t)kc * P * F->dev.max_per_ray + kTile;
-  pnerf_status st = ensure_workspace(F, kc * P, cap, n_chunks, s);
+  const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
+  if (P > max_rays)
+    return fail(PNERF_ERR_CAPACITY, "P=%d rays per hypothesis exceeds %lld", P, (long long)max_rays);
+  const int kr = (int)std::min<int64_t>(K, max_rays / P);
+  if (mode == kMarch && kr < K)
+    return fail(PNERF_ERR_CAPACITY, "march inspection needs K*P <= %lld rays", (long long)max_rays);
+  pnerf_status st = ensure_rays(F, kr * P, kr, s);
   if (st != PNERF_OK) return st;
-  for (int c = 0; c < n_chunks; ++c) {
-    int k0 = c * kc, kn = std::min(kc, K - k0);
-    DevBatch b = make_batch(kn, poses + (size_t)12 * k0, P, pix + (size_t)P * k0, obs, intr);
-    DevWork w{};
-    carve(F, F->ws_rays, F->ws_cap, &w, (char*)F->d_ws);
-    w.total = F->d_totals + c;
-    // inspection: lattice indices go to the (otherwise unused) blue-channel buffer
-    int32_t* j_tmp = mode == kMarch ? reinterpret_cast<int32_t*>(w.cb) : nullptr;
-    HIP_TRY(timed(F, "march", s, [&] { return launch_march(F->dev, b, w, j_tmp, s); }));
-    if (mode == kMarch) {
-      HIP_TRY(launch_offsets_i64(w.off, ray_offset, b.n_rays + 1, 0, s));
-      if (capacity > 0) HIP_TRY(launch_copy_samples(w.t, j_tmp, t_out, j_out, w.total, capacity, s));
-      continue;
+  const int64_t per_sample = bytes_per_sample(F->dev);
+  const int64_t limit = std::min<int64_t>(
+      std::max<int64_t>((F->budget - (int64_t)F->rays_bytes) / per_sample, kTile),
+      ((int64_t)1 << 31) - 4 * kTile);
+  int chunk_id = 0;
+  int64_t grand = 0;
+  for (int h0 = 0; h0 < K; h0 += kr) {
+    const int hn = std::min(kr, K - h0);
+    DevBatch bb = make_batch(hn, poses + (size_t)12 * h0, P, pix + (size_t)P * h0, obs, intr);
+    st = ensure_samples(F, 0, limit, chunk_id + 1, s);  // totals array for the counted batch
+    if (st != PNERF_OK) return st;
+    DevWork wb = counted_work(F);
+    HIP_TRY(timed(F, "march", s, [&] { return launch_march_count(F->dev, bb, wb, s); }));
+    HIP_TRY(hipMemcpyAsync(F->h_hyp, wb.hyp_total, sizeof(int32_t) * hn, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    // chunks of whole hypotheses
+    std::vector<int> cut{0};
+    std::vector<int64_t> sums;
+    int64_t biggest = 0, counted = 0;
+    for (int a = 0; a < hn;) {
+      int64_t sum = 0;
+      int b = a;
+      while (b < hn && sum + F->h_hyp[b] <= limit) sum += F->h_hyp[b++];
+      if (b == a)
+        return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace budget "
+                    "holds (%lld)", h0 + a, F->h_hyp[a], (long long)limit);
+      cut.push_back(b);
+      sums.push_back(sum);
+      biggest = std::max(biggest, sum);
+      counted += sum;
+      a = b;
     }
-    HIP_TRY(timed(F, "encode_fwd", s, [&] { return launch_encode_fwd(F->dev, b, w, F->enc_blocks, s); }));
-    if (mode == kRender) {
-      HIP_TRY(timed(F, "mlp_fwd_render", s, [&] {
-        return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 0, s);
+    const int n_chunks = (int)sums.size();
+    st = ensure_samples(F, biggest, limit, chunk_id + n_chunks, s);
+    if (st != PNERF_OK) return st;
+    wb = counted_work(F);
+    int64_t base = 0;  // samples of the counted batch before this chunk
+    for (int c = 0; c < n_chunks; ++c, ++chunk_id) {
+      const int a = cut[c], kn = cut[c + 1] - cut[c], k0 = h0 + a;
+      DevBatch b = make_batch(kn, poses + (size_t)12 * k0, P, pix + (size_t)P * k0, obs, intr);
+      DevWork w = chunk_work(F, a * P, chunk_id);
+      // inspection: lattice indices go to the (otherwise unused) blue-channel buffer
+      int32_t* j_tmp = mode == kMarch ? reinterpret_cast<int32_t*>(w.cb) : nullptr;
+      HIP_TRY(timed(F, "march_write", s, [&] {
+        return launch_march_write(F->dev, b, wb, w, a * P, (int)base, (int)sums[c], j_tmp, s);
       }));
-      HIP_TRY(timed(F, "composite_fwd", s, [&] {
-        return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
-      }));
-      continue;
+      if (mode == kMarch) {
+        const bool last = k0 + kn == K;
+        HIP_TRY(launch_offsets_i64(w.off, ray_offset + (size_t)P * k0, b.n_rays + (last ? 1 : 0),
+                                   grand + base, s));
+        if (capacity >= counted && sums[c] > 0)
+          HIP_TRY(launch_copy_samples(w.t, j_tmp, t_out + grand + base, j_out + grand + base,
+                                      sums[c], s));
+      } else if (mode == kRender) {
+        HIP_TRY(timed(F, "encode_render", s, [&] { return launch_encode(F->dev, b, w, F->enc_blocks, 0, s); }));
+        HIP_TRY(timed(F, "mlp_fwd_render", s, [&] {
+          return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 0, s);
+        }));
+        HIP_TRY(timed(F, "composite_fwd", s, [&] {
+          return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
+        }));
+      } else {
+        HIP_TRY(timed(F, "encode", s, [&] { return launch_encode(F->dev, b, w, F->enc_blocks, 1, s); }));
+        HIP_TRY(timed(F, "mlp_fwd", s, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
+        HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
+        HIP_TRY(timed(F, "mlp_bwd", s, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, s); }));
+        HIP_TRY(timed(F, "reduce", s, [&] {
+          return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, s);
+        }));
+      }
+      base += sums[c];
     }
-    HIP_TRY(timed(F, "mlp_fwd", s, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
-    HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
-    HIP_TRY(timed(F, "mlp_bwd", s, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, s); }));
-    HIP_TRY(timed(F, "encode_bwd", s, [&] { return launch_encode_bwd(F->dev, b, w, F->enc_blocks, s); }));
-    HIP_TRY(timed(F, "reduce", s, [&] {
-      return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, s);
-    }));
+    grand += counted;
   }
-  F->last_chunks = n_chunks;
+  F->last_chunks = chunk_id;
+  F->last_total = grand;
   return PNERF_OK;
 }
 
@@ -458,12 +585,6 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     for (int g = 0; g < d.n_groups; ++g) {
       d.grp_lv[g][0] = order[g];
       d.grp_lv[g][1] = order[g + d.n_groups];
-      // reuse the rows of the group's own d loss / d feature values for its
-      // three position-gradient partials: (l0, q0), (l0, q1), (l1, q0)
-      auto row = [&](int l, int q) { return (l % 4) * 2 * (L / 4) + (l / 4) * 2 + q; };
-      d.part_row[g][0] = row(d.grp_lv[g][0], 0);
-      d.part_row[g][1] = row(d.grp_lv[g][0], 1);
-      d.part_row[g][2] = row(d.grp_lv[g][1], 0);
     }
   }
   d.density_bias = p->density_bias;
@@ -495,7 +616,7 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     int64_t lat = (int64_t)std::ceil(std::sqrt(diag) / (double)p->step) + 2;
     d.max_per_ray = (int)std::min<int64_t>(lat, p->max_samples);
   }
-  F->budget = p->max_workspace_bytes > 0 ? p->max_workspace_bytes : ((int64_t)64 << 30);
+  F->budget = p->max_workspace_bytes > 0 ? p->max_workspace_bytes : ((int64_t)96 << 30);
 
   // weights -> float, then MFMA tiles
   Weights W;
@@ -579,8 +700,10 @@ void pnerf_destroy_field(pnerf_field* F) {
   (void)hipFree(F->d_wd1);
   (void)hipFree(F->d_wd2);
   (void)hipFree(F->d_occ);
-  (void)hipFree(F->d_ws);
+  (void)hipFree(F->d_rays);
+  (void)hipFree(F->d_samp);
   (void)hipFree(F->d_totals);
+  if (F->h_hyp) (void)hipHostFree(F->h_hyp);
   delete F;
 }
 
@@ -652,10 +775,10 @@ pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64
                                  void* stream) {
   if (!F || !dst) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
   if (what < 0 || what > 3) return fail(PNERF_ERR_INVALID_ARG, "what=%d", what);
-  if (!F->d_ws || n < 0 || n > F->ws_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
+  if (!F->d_samp || n < 0 || n > F->samp_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
   if (F->last_chunks != 1) return fail(PNERF_ERR_INVALID_ARG, "last call used %d chunks", F->last_chunks);
   DevWork w{};
-  carve(F, F->ws_rays, F->ws_cap, &w, (char*)F->d_ws);
+  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp);
   w.total = F->d_totals;  // the single chunk of the last call
   HIP_TRY(launch_inspect(F->dev, DevBatch{}, w, what, dst, n, (hipStream_t)stream));
   return PNERF_OK;
@@ -672,13 +795,8 @@ pnerf_status pnerf_field_occupancy(pnerf_field* F, uint32_t* bits_host, void* st
 
 pnerf_status pnerf_field_last_sample_count(pnerf_field* F, int64_t* count, void* stream) {
   if (!F || !count) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
-  *count = 0;
-  if (F->last_chunks == 0) return PNERF_OK;
-  std::vector<int32_t> h(F->last_chunks);
-  hipStream_t s = (hipStream_t)stream;
-  HIP_TRY(hipMemcpyAsync(h.data(), F->d_totals, sizeof(int32_t) * h.size(), hipMemcpyDeviceToHost, s));
-  HIP_TRY(hipStreamSynchronize(s));
-  for (int32_t v : h) *count += v;
+  (void)stream;
+  *count = F->last_total;  // counted on the host when the call planned its chunks
   return PNERF_OK;
 }
 

@@ -155,29 +155,13 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   }
 }
 
-// Torque and force terms of one sample (Eq. 3 and Eq. 2 before the sums):
-// dL/dp_i is the fixed-order sum of the encoding groups' partials, the torque
-// t_i d x dL/dp_i (plus d x dL/dd through SH on the view-direction path).
+// Torque and force terms of one sample (Eq. 3 and Eq. 2 before the sums), as
+// the MLP backward kernel left them in rows 0..5 of the feature array.
 __device__ __forceinline__ void sample_terms(const DevField& f, const DevWork& w, int s,
                                              float out[6]) {
-  float gp[3] = {0.f, 0.f, 0.f};
-  for (int grp = 0; grp < f.n_groups; ++grp)
+  (void)f;
 #pragma unroll
-    for (int a = 0; a < 3; ++a) gp[a] += w.feat[(int64_t)f.part_row[grp][a] * w.cap + s];
-  const int ray = w.sray[s];
-  const float d[3] = {w.rdx[ray], w.rdy[ray], w.rdz[ray]};
-  const float t = w.t[s];
-  float m[3] = {t * gp[0], t * gp[1], t * gp[2]};
-  if (f.sh_dir_grad) {
-#pragma unroll
-    for (int a = 0; a < 3; ++a) m[a] += w.gd[(int64_t)a * w.cap + s];
-  }
-  out[0] = d[1] * m[2] - d[2] * m[1];
-  out[1] = d[2] * m[0] - d[0] * m[2];
-  out[2] = d[0] * m[1] - d[1] * m[0];
-  out[3] = gp[0];
-  out[4] = gp[1];
-  out[5] = gp[2];
+  for (int q = 0; q < 6; ++q) out[q] = w.feat[(int64_t)q * w.cap + s];
 }
 
 // Per-hypothesis reduction in two fixed-order stages.  Block (j, k) sums part

@@ -1,8 +1,9 @@
 // Multiresolution hash encoding of the samples (Sec. III, Instant NGP): the
-// forward gather of every level's 8 vertex features and their trilinear blend,
-// and -- backward -- the derivative of the blend with respect to the sample
-// position, contracted with d loss / d feature.  The table is frozen, so the
-// backward pass re-gathers and scatters nothing.
+// gather of every level's 8 vertex features, their trilinear blend, and the
+// blend's derivative with respect to the sample position (the table is frozen,
+// so the backward pass needs nothing else from it: the MLP backward kernel
+// contracts this Jacobian with d loss / d feature, and nothing is re-gathered
+// or scattered).
 //
 // Work split: the levels are partitioned into NG groups of two levels each,
 // and block b works on group b % NG.  Workgroups are dispatched round-robin
@@ -13,9 +14,10 @@
 //
 // Features are stored SoA, row p = (l % 4) * 2 LPG + (l / 4) * 2 + q for
 // feature q of level l (the order in which the MLP kernels feed them to MFMA),
-// row stride = the workspace sample capacity.  The backward pass writes each
-// group's three position-gradient partials over the d loss / d feature rows of
-// that group's own levels (read first by the same thread).
+// row stride = the workspace sample capacity.  The Jacobian d feature / d p
+// (world units, zero along clamped components) is stored SoA too, row
+// ((l % 4) LPG + l / 4) * 6 + 3 q + a, so that lane group l % 4 of the MLP
+// backward kernel reads one contiguous block of rows.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -126,10 +128,12 @@ __device__ __forceinline__ float2 vertex(const DevField& f, uint32_t idx) {
   return reinterpret_cast<const float2*>(f.table32)[idx];
 }
 
-// Feature (2 values) of level l at position x: blend of the 8 vertices.
+// Feature (2 values) of level l at position x -- blend of the 8 vertices --
+// and, when jac != nullptr, its derivative with respect to x (jac[3 q + a] =
+// N d feature_q / d pos_a, pos = x N).
 template <bool F16>
 __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const float x[3],
-                                                const float dx[3]) {
+                                                const float dx[3], float* jac) {
   Cell c;
   make_cell(f, l, x, dx, c);
   float2 v[8];
@@ -142,6 +146,21 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
         wz * (uy * (ux * v[4].x + wx * v[5].x) + wy * (ux * v[6].x + wx * v[7].x));
   r.y = uz * (uy * (ux * v[0].y + wx * v[1].y) + wy * (ux * v[2].y + wx * v[3].y)) +
         wz * (uy * (ux * v[4].y + wx * v[5].y) + wy * (ux * v[6].y + wx * v[7].y));
+  if (jac) {
+    const float N = (float)f.res[l];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      float t[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) t[k] = q ? v[k].y : v[k].x;
+      jac[3 * q + 0] = N * (uy * uz * (t[1] - t[0]) + wy * uz * (t[3] - t[2]) +
+                            uy * wz * (t[5] - t[4]) + wy * wz * (t[7] - t[6]));
+      jac[3 * q + 1] = N * (ux * uz * (t[2] - t[0]) + wx * uz * (t[3] - t[1]) +
+                            ux * wz * (t[6] - t[4]) + wx * wz * (t[7] - t[5]));
+      jac[3 * q + 2] = N * (ux * uy * (t[4] - t[0]) + wx * uy * (t[5] - t[1]) +
+                            ux * wy * (t[6] - t[2]) + wx * wy * (t[7] - t[3]));
+    }
+  }
   return r;
 }
 
@@ -149,90 +168,43 @@ __device__ __forceinline__ int feat_row(const DevField& f, int l, int q) {
   return (l & 3) * 2 * f.lpg + (l >> 2) * 2 + q;
 }
 
+__device__ __forceinline__ int jac_row(const DevField& f, int l, int q, int a) {
+  return ((l & 3) * f.lpg + (l >> 2)) * 6 + 3 * q + a;
+}
+
 // ------------------------------------------------------------------ forward
-template <bool F16>
-__global__ __launch_bounds__(kBlock) void k_encode_fwd(DevField f, DevBatch b, DevWork w) {
+// Level-outer: a block first blends its group's first level for all its
+// samples, then the second, so that an XCD's L2 holds one level's table at a
+// time.  GRAD: also store the Jacobian rows.
+template <bool F16, bool GRAD>
+__global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWork w) {
   const int S = *w.total;
   const int grp = blockIdx.x % f.n_groups;
-  const int l0 = f.grp_lv[grp][0], l1 = f.grp_lv[grp][1];
   const int stride = gridDim.x / f.n_groups;
   const int64_t cap = w.cap;
-  float* r00 = w.feat + (int64_t)feat_row(f, l0, 0) * cap;
-  float* r01 = w.feat + (int64_t)feat_row(f, l0, 1) * cap;
-  float* r10 = w.feat + (int64_t)feat_row(f, l1, 0) * cap;
-  float* r11 = w.feat + (int64_t)feat_row(f, l1, 1) * cap;
-  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
-    const int s = sb * kBlock + threadIdx.x;
-    if (s >= S) break;
-    Pos ps = sample_pos(f, b, w, s);
-    float2 a = level_feature<F16>(f, l0, ps.x, ps.dx);
-    float2 c = level_feature<F16>(f, l1, ps.x, ps.dx);
-    r00[s] = a.x;
-    r01[s] = a.y;
-    r10[s] = c.x;
-    r11[s] = c.y;
-  }
-}
-
-// ----------------------------------------------------------------- backward
-// d loss / d x of one level: sum over the 8 vertices of
-// <d loss / d feature, vertex value> times the derivative of its trilinear
-// weight, times N (x is the normalised position, pos = x N).
-template <bool F16>
-__device__ __forceinline__ void level_grad(const DevField& f, int l, const float x[3],
-                                           const float dx[3], float g0, float g1, float gx[3]) {
-  Cell c;
-  make_cell(f, l, x, dx, c);
-  float2 v[8];
+  for (int li = 0; li < 2; ++li) {
+    const int l = f.grp_lv[grp][li];
+    float* r0 = w.feat + (int64_t)feat_row(f, l, 0) * cap;
+    float* r1 = w.feat + (int64_t)feat_row(f, l, 1) * cap;
+    float* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
+    for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
+      const int s = sb * kBlock + threadIdx.x;
+      if (s >= S) break;
+      Pos ps = sample_pos(f, b, w, s);
+      float jac[6];
+      float2 a = level_feature<F16>(f, l, ps.x, ps.dx, GRAD ? jac : nullptr);
+      r0[s] = a.x;
+      r1[s] = a.y;
+      if (GRAD) {
 #pragma unroll
-  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, c.idx[k]);
-  float dt[8];
+        for (int q = 0; q < 2; ++q)
 #pragma unroll
-  for (int k = 0; k < 8; ++k) dt[k] = g0 * v[k].x + g1 * v[k].y;
-  const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
-  const float ux = 1.f - wx, uy = 1.f - wy, uz = 1.f - wz;
-  const float ddx = uy * uz * (dt[1] - dt[0]) + wy * uz * (dt[3] - dt[2]) +
-                    uy * wz * (dt[5] - dt[4]) + wy * wz * (dt[7] - dt[6]);
-  const float ddy = ux * uz * (dt[2] - dt[0]) + wx * uz * (dt[3] - dt[1]) +
-                    ux * wz * (dt[6] - dt[4]) + wx * wz * (dt[7] - dt[5]);
-  const float ddz = ux * uy * (dt[4] - dt[0]) + wx * uy * (dt[5] - dt[1]) +
-                    ux * wy * (dt[6] - dt[2]) + wx * wy * (dt[7] - dt[3]);
-  const float N = (float)f.res[l];
-  gx[0] += N * ddx;
-  gx[1] += N * ddy;
-  gx[2] += N * ddz;
-}
-
-// Writes this group's share of d loss / d p (world units, zero along clamped
-// components) into rows part_row[grp][0..2] (= rows of the group's own d loss /
-// d feature values, which this thread has read first).
-template <bool F16>
-__global__ __launch_bounds__(kBlock) void k_encode_bwd(DevField f, DevBatch b, DevWork w) {
-  const int S = *w.total;
-  const int grp = blockIdx.x % f.n_groups;
-  const int l0 = f.grp_lv[grp][0], l1 = f.grp_lv[grp][1];
-  const int stride = gridDim.x / f.n_groups;
-  const int64_t cap = w.cap;
-  float* g00 = w.feat + (int64_t)feat_row(f, l0, 0) * cap;
-  float* g01 = w.feat + (int64_t)feat_row(f, l0, 1) * cap;
-  float* g10 = w.feat + (int64_t)feat_row(f, l1, 0) * cap;
-  float* g11 = w.feat + (int64_t)feat_row(f, l1, 1) * cap;
-  float* out0 = w.feat + (int64_t)f.part_row[grp][0] * cap;
-  float* out1 = w.feat + (int64_t)f.part_row[grp][1] * cap;
-  float* out2 = w.feat + (int64_t)f.part_row[grp][2] * cap;
-  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
-    const int s = sb * kBlock + threadIdx.x;
-    if (s >= S) break;
-    const float a0 = g00[s], a1 = g01[s], c0 = g10[s], c1 = g11[s];
-    float gx[3] = {0.f, 0.f, 0.f};
-    Pos ps = sample_pos(f, b, w, s);
-    if (a0 != 0.0f || a1 != 0.0f || c0 != 0.0f || c1 != 0.0f) {
-      level_grad<F16>(f, l0, ps.x, ps.dx, a0, a1, gx);
-      level_grad<F16>(f, l1, ps.x, ps.dx, c0, c1, gx);
+          for (int c = 0; c < 3; ++c) {
+            float v = (ps.clamped >> c) & 1u ? 0.0f : jac[3 * q + c] * f.inv_ext[c];
+            jr[(int64_t)(3 * q + c) * cap + s] = v;
+          }
+      }
     }
-    out0[s] = (ps.clamped & 1u) ? 0.0f : gx[0] * f.inv_ext[0];
-    out1[s] = (ps.clamped & 2u) ? 0.0f : gx[1] * f.inv_ext[1];
-    out2[s] = (ps.clamped & 4u) ? 0.0f : gx[2] * f.inv_ext[2];
   }
 }
 
@@ -265,7 +237,7 @@ __global__ __launch_bounds__(kBlock) void k_occupancy(DevField f, uint32_t* bits
     }
     float feat[2 * kMaxLevels];
     for (int l = 0; l < f.L; ++l) {
-      float2 v = level_feature<F16>(f, l, x, dx);
+      float2 v = level_feature<F16>(f, l, x, dx, nullptr);
       feat[2 * l] = v.x;
       feat[2 * l + 1] = v.y;
     }
@@ -296,21 +268,19 @@ int encode_blocks(const DevField& f, int n_cu) {
   return ((want + unit - 1) / unit) * unit;
 }
 
-hipError_t launch_encode_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                             hipStream_t s) {
-  if (f.f16)
-    hipLaunchKernelGGL(k_encode_fwd<true>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
-  else
-    hipLaunchKernelGGL(k_encode_fwd<false>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
-  return hipGetLastError();
-}
-
-hipError_t launch_encode_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                             hipStream_t s) {
-  if (f.f16)
-    hipLaunchKernelGGL(k_encode_bwd<true>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
-  else
-    hipLaunchKernelGGL(k_encode_bwd<false>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+hipError_t launch_encode(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                         int with_grad, hipStream_t s) {
+  if (f.f16) {
+    if (with_grad)
+      hipLaunchKernelGGL((k_encode<true, true>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+    else
+      hipLaunchKernelGGL((k_encode<true, false>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  } else {
+    if (with_grad)
+      hipLaunchKernelGGL((k_encode<false, true>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+    else
+      hipLaunchKernelGGL((k_encode<false, false>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w);
+  }
   return hipGetLastError();
 }
 

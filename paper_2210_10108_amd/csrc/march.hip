@@ -181,8 +181,8 @@ __global__ __launch_bounds__(kScanBlock) void k_scan_local(DevBatch b, DevWork w
 }
 
 // Exclusive scan of the block totals in one workgroup (n_blocks <= 8192); also
-// writes the chunk's sample total and the closing ray offset.
-__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks, int n_rays) {
+// writes the batch's sample total.
+__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks) {
   __shared__ int s[1024];
   constexpr int kPer = 8;
   int tid = threadIdx.x;
@@ -206,52 +206,77 @@ __global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks, i
     if (i < n_blocks) w.blocksum[i] = run;
     run += v[q];
   }
-  if (tid == 1023) {
-    *w.total = s[1023];
-    w.off[n_rays] = s[1023];
-  }
+  if (tid == 1023) *w.total = s[1023];
 }
 
-// Second march of every ray, now writing its kept samples at the ray's global
-// offset (block prefix + offset inside the block).
-__global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork w,
+// Samples of every hypothesis (difference of the offsets at its first ray and
+// past its last ray); the host reads these to size and plan the sample chunks.
+__global__ void k_hyp_totals(DevBatch b, DevWork w) {
+  int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= b.K) return;
+  auto excl = [&](int r) { return r < b.n_rays ? w.blocksum[r / kScanBlock] + w.off[r] : *w.total; };
+  w.hyp_total[k] = excl((k + 1) * b.P) - excl(k * b.P);
+}
+
+// Second march of the rays of one sample chunk (rays ray_base .. of the counted
+// batch `wb`), writing their kept samples into the chunk's sample arrays at
+// offset (exclusive offset in the counted batch) - sample_base, and the chunk's
+// ray offsets into wc.off (wc's per-ray arrays start at the chunk's first ray).
+__global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork wb,
+                                                         DevWork wc, int ray_base,
+                                                         int sample_base, int chunk_total,
                                                          int32_t* j_out) {
   int lane = threadIdx.x & 63;
   int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *wc.total = chunk_total;
+    wc.off[b.n_rays] = chunk_total;
+  }
   for (int q = 0; q < kRaysPerWave; ++q) {
     int ray = wave * kRaysPerWave + q;
     if (ray >= b.n_rays) break;
-    int o = w.blocksum[ray / kScanBlock] + w.off[ray];
-    int n = w.count[ray];
-    if (lane == 0) w.off[ray] = o;  // only this wave reads this ray's offset
+    int rb = ray_base + ray;
+    int o = wb.blocksum[rb / kScanBlock] + wb.off[rb] - sample_base;
+    int n = wc.count[ray];
+    if (lane == 0) wc.off[ray] = o;
     if (n == 0) continue;
     RayGeom g;
     g.o[0] = b.poses[12 * (ray / b.P) + 3];
     g.o[1] = b.poses[12 * (ray / b.P) + 7];
     g.o[2] = b.poses[12 * (ray / b.P) + 11];
-    g.d[0] = w.rdx[ray];
-    g.d[1] = w.rdy[ray];
-    g.d[2] = w.rdz[ray];
-    g.tn = w.rtn[ray];
-    g.tf = w.rtf[ray];
-    g.delta = w.rdelta[ray];
+    g.d[0] = wc.rdx[ray];
+    g.d[1] = wc.rdy[ray];
+    g.d[2] = wc.rdz[ray];
+    g.tn = wc.rtn[ray];
+    g.tf = wc.rtf[ray];
+    g.delta = wc.rdelta[ray];
     g.hit = 1;
-    march_wave<true>(f, g, lane, n, w.t + o, j_out ? j_out + o : nullptr, w.sray + o, ray);
+    march_wave<true>(f, g, lane, n, wc.t + o, j_out ? j_out + o : nullptr, wc.sray + o, ray);
   }
 }
 
 }  // namespace
 
-hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
-                        int32_t* lattice_j_out, hipStream_t s) {
+hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w,
+                              hipStream_t s) {
   int n_scan = (b.n_rays + kScanBlock - 1) / kScanBlock;
-  if (n_scan > 8192) return hipErrorInvalidValue;
+  if (n_scan > kMaxScanBlocks) return hipErrorInvalidValue;
   int rays_per_block = kRaysPerWave * (kRayBlock / 64);
   int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
   hipLaunchKernelGGL(k_ray_count, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w);
   hipLaunchKernelGGL(k_scan_local, dim3(n_scan), dim3(kScanBlock), 0, s, b, w);
-  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_scan, b.n_rays);
-  hipLaunchKernelGGL(k_ray_write, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w, lattice_j_out);
+  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_scan);
+  hipLaunchKernelGGL(k_hyp_totals, dim3((b.K + 255) / 256), dim3(256), 0, s, b, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_march_write(const DevField& f, const DevBatch& b, const DevWork& wb,
+                              const DevWork& wc, int ray_base, int sample_base, int chunk_total,
+                              int32_t* lattice_j_out, hipStream_t s) {
+  int rays_per_block = kRaysPerWave * (kRayBlock / 64);
+  int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
+  hipLaunchKernelGGL(k_ray_write, dim3(n_march), dim3(kRayBlock), 0, s, f, b, wb, wc, ray_base,
+                     sample_base, chunk_total, lattice_j_out);
   return hipGetLastError();
 }
 
@@ -260,11 +285,9 @@ __global__ void k_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t b
   if (i < n) out[i] = base + off[i];
 }
 
-// Copy t and lattice index of every sample when the total fits `capacity`.
+// Copy t and lattice index of n samples.
 __global__ void k_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
-                               const int32_t* total, int64_t capacity) {
-  int64_t n = *total;
-  if (n > capacity) return;
+                               int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * blockDim.x) {
     t_out[i] = t[i];
@@ -273,9 +296,8 @@ __global__ void k_copy_samples(const float* t, const int32_t* j, float* t_out, i
 }
 
 hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
-                               const int32_t* total, int64_t capacity, hipStream_t s) {
-  hipLaunchKernelGGL(k_copy_samples, dim3(1024), dim3(256), 0, s, t, j, t_out, j_out, total,
-                     capacity);
+                               int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_copy_samples, dim3(1024), dim3(256), 0, s, t, j, t_out, j_out, n);
   return hipGetLastError();
 }
 

@@ -1,8 +1,9 @@
 // Density and colour networks of the frozen field on MFMA (Sec. III: the
 // field's small MLPs), forward and -- backward -- the input gradient through
-// both networks: d loss / d feature for the encoding's backward pass and, when
-// the view-direction path is on, d loss / d direction through the SH input.
-// The hash-grid features are produced and consumed by the encoding kernels.
+// both networks to d loss / d feature, then through the encoding's stored
+// Jacobian to d loss / d p of every sample (and, on the view-direction path,
+// through the SH input to d loss / d direction), ending in each sample's force
+// and torque terms of Eq. 2 and Eq. 3.
 //
 // Work unit: one wavefront takes a tile of 64 consecutive compacted samples,
 // as four 16-sample column tiles of v_mfma_f32_16x16x4_f32.  The batch (sample)
@@ -411,31 +412,55 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
 #pragma unroll
           for (int nt = 0; nt < 4; ++nt) gf[m][nt] = mfma(a, ga[mp][nt][i], gf[m][nt]);
         }
-    // d loss / d feature of levels 4j + g -> rows 2 LPG g + 2j + q (the
-    // encoding's backward pass reads them); d loss / d direction via SH
-    float* grow = w.feat + (int64_t)(g * 2 * LPG) * w.cap;
+    // d loss / d p = sum over the lane group's levels 4j + g of
+    // d loss / d feature times the stored Jacobian, then over the 4 groups;
+    // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
+    const float* jrow = w.jac + (int64_t)(g * 6 * LPG) * w.cap;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      int s = sidx[nt];
+      const int s = sidx[nt];
+      const int sc = s < S ? s : S - 1;
+      float gx[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < LPG; ++j)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          const float gq = gf[j / 2][nt][2 * (j % 2) + q];
+#pragma unroll
+          for (int a = 0; a < 3; ++a) gx[a] += gq * jrow[(int64_t)(6 * j + 3 * q + a) * w.cap + sc];
+        }
       float gd[3] = {0.f, 0.f, 0.f};
+      float d[3];
+      sample_dir(w, sc, d);
       if (dir_grad) {
-        float d[3];
-        sample_dir(w, s < S ? s : S - 1, d);
         float gs[4] = {gsh[nt][0], gsh[nt][1], gsh[nt][2], gsh[nt][3]};
         sh4_vjp(d, g, gs, gd);
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-          gd[a] += __shfl_xor(gd[a], 16);
-          gd[a] += __shfl_xor(gd[a], 32);
-        }
       }
-      if (s < S) {
 #pragma unroll
-        for (int j = 0; j < LPG; ++j) {
-          grow[(int64_t)(2 * j) * w.cap + s] = gf[j / 2][nt][2 * (j % 2)];
-          grow[(int64_t)(2 * j + 1) * w.cap + s] = gf[j / 2][nt][2 * (j % 2) + 1];
+      for (int a = 0; a < 3; ++a) {
+        gx[a] += __shfl_xor(gx[a], 16);
+        gx[a] += __shfl_xor(gx[a], 32);
+        gd[a] += __shfl_xor(gd[a], 16);
+        gd[a] += __shfl_xor(gd[a], 32);
+      }
+      if (s < S && g < 2) {
+        const float t = w.t[s];
+        const float m[3] = {t * gx[0] + gd[0], t * gx[1] + gd[1], t * gx[2] + gd[2]};
+        // lane group 0 stores the torque, group 1 the force
+        float o0, o1, o2;
+        if (g == 0) {
+          o0 = d[1] * m[2] - d[2] * m[1];
+          o1 = d[2] * m[0] - d[0] * m[2];
+          o2 = d[0] * m[1] - d[1] * m[0];
+        } else {
+          o0 = gx[0];
+          o1 = gx[1];
+          o2 = gx[2];
         }
-        if (dir_grad && g < 3) w.gd[(int64_t)g * w.cap + s] = gd[g];
+        float* out = w.feat + (int64_t)(3 * g) * w.cap;  // feature rows are free by now
+        out[s] = o0;
+        out[w.cap + s] = o1;
+        out[2 * w.cap + s] = o2;
       }
     }
   }

@@ -14,6 +14,7 @@ constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column 
 constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile
 constexpr int kMaxGroups = 8;      // level groups of the encoding kernels (two levels each)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
+constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
 constexpr int kReduceBlocks = 2048;   // target blocks of the per-hypothesis reduction
 constexpr int kMaxReduceParts = 64;   // parts per hypothesis (K * parts <= max(K, 2048) * 7 floats)
 
@@ -43,9 +44,8 @@ struct DevField {
   uint32_t dense[kMaxLevels];   // 1: vertex index i + j n1 + k n1^2
   uint32_t n1[kMaxLevels];      // res + 1
   int32_t f16;                  // table stored as fp16
-  int32_t n_groups;             // level groups (L / 2) of the encoding kernels
+  int32_t n_groups;             // level groups (L / 2) of the encoding kernel
   int32_t grp_lv[kMaxGroups][2];   // the two levels of each group
-  int32_t part_row[kMaxGroups][3]; // feature rows reused for the group's d loss / d p
   const float* table32;         // [L][T][2]
   const __half* table16;        // [L][T][2]
   const float* wfwd;            // forward A-operand tiles (fp32)
@@ -82,9 +82,11 @@ struct DevWork {
   float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta;
   float *rex, *rey, *rez;       // direction correction: exact unit direction - (rdx, rdy, rdz)
   int32_t* count;               // kept samples per ray
-  int32_t* off;                 // [n_rays + 1] exclusive offsets
-  int32_t* blocksum;            // per 256-ray block
-  int32_t* total;               // device scalar: samples in this chunk
+  int32_t* off;                 // counted batch: offset inside each 256-ray block;
+                                // sample chunk: [n_rays + 1] exclusive offsets
+  int32_t* blocksum;            // per 256-ray block (exclusive, after the scan)
+  int32_t* hyp_total;           // [K] samples of every hypothesis of the counted batch
+  int32_t* total;               // device scalar: samples of the counted batch / the chunk
   float* ray_loss;              // [n_rays]
   float* partial;               // [K][parts][7] per-hypothesis partial sums
   // per sample
@@ -93,18 +95,19 @@ struct DevWork {
   float* sig;                   // sigma (forward) -> d loss / d h0 (after composite)
   float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
   uint32_t* masks;              // [tiles][6][64] ReLU masks
-  float* feat;                  // [2L][cap] features -> d loss / d feature -> d loss / d p partials
-  float* gd;                    // [3][cap] d loss / d direction through SH (view-direction path)
-  int64_t cap;                  // sample capacity (row stride of feat and gd)
+  float* feat;                  // [2L][cap] features; after the backward rows 0..5 = torque, force
+  float* jac;                   // [6L][cap] d feature / d p of every level
+  int64_t cap;                  // sample capacity (row stride of feat and jac)
 };
 
 // ---- launchers (all enqueue on `s`, no synchronisation)
-hipError_t launch_march(const DevField& f, const DevBatch& b, const DevWork& w,
-                        int32_t* lattice_j_out, hipStream_t s);
-hipError_t launch_encode_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                             hipStream_t s);
-hipError_t launch_encode_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                             hipStream_t s);
+hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w,
+                              hipStream_t s);
+hipError_t launch_march_write(const DevField& f, const DevBatch& b, const DevWork& wb,
+                              const DevWork& wc, int ray_base, int sample_base, int chunk_total,
+                              int32_t* lattice_j_out, hipStream_t s);
+hipError_t launch_encode(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                         int with_grad, hipStream_t s);
 hipError_t launch_mlp_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                           int with_grad, hipStream_t s);
 hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork& w, int with_grad,
@@ -115,7 +118,7 @@ hipError_t launch_reduce(const DevField& f, const DevBatch& b, const DevWork& w,
                          float* dpose, hipStream_t s);
 hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s);
 hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
-                               const int32_t* total, int64_t capacity, hipStream_t s);
+                               int64_t n, hipStream_t s);
 hipError_t launch_inspect(const DevField& f, const DevBatch& b, const DevWork& w, int what,
                           float* dst, int64_t n, hipStream_t s);
 hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base, hipStream_t s);
