@@ -68,8 +68,9 @@ struct pnerf_field {
   int device = 0;
   // owned device memory
   void* d_table = nullptr;
-  float* d_wfwd = nullptr;
-  float* d_wbwd = nullptr;
+  void* d_wfwd = nullptr;
+  void* d_wbwd = nullptr;
+  float* d_wc3 = nullptr;
   float* d_wd1 = nullptr;
   float* d_wd2 = nullptr;
   uint32_t* d_occ = nullptr;
@@ -98,11 +99,11 @@ struct pnerf_field {
 namespace {
 
 // ------------------------------------------------------------ weight tiles
-// A-operand tiles of v_mfma_f32_16x16x4_f32: unit u holds 64 floats, lane l
-// supplies A[row = l % 16][k = l / 16] of one (row tile, K step).  Rows are the
-// layer's outputs; the K order follows the C layout of the previous layer
-// (K step 4*m' + i, position g <-> input 16 m' + 4 g + i) so that accumulators
-// feed the next MFMA without data movement.
+// Weight units (see WeightUnit): unit u, lane l = 16 g + r, K position j holds
+// the weight of output row r of the unit's row tile and of the input that the
+// previous layer's accumulator layout puts at position j of lane group g of
+// the unit's K step: hidden unit 16 (2 s + j / 4) + 4 g + j % 4 of step s.
+// Each fp32 weight w is stored as bf16 hi = rn(w) and lo = rn(w - hi).
 struct Weights {
   int din;
   std::vector<float> d1, d2, c1, c2, c3;  // [in][out]
@@ -113,54 +114,85 @@ struct Weights {
   float C3(int i, int o) const { return c3[(size_t)i * 3 + o]; }
 };
 
-void build_fwd_tiles(const Weights& W, int lpg, std::vector<float>& t) {
-  t.assign(fwd_tile_floats(lpg), 0.0f);
-  auto put = [&](int unit, int lane, float v) { t[(size_t)unit * 64 + lane] = v; };
-  const int KD = 2 * lpg;
-  for (int lane = 0; lane < 64; ++lane) {
-    int g = lane / 16, c = lane % 16;
-    for (int m = 0; m < 4; ++m)
-      for (int ks = 0; ks < KD; ++ks) {
-        int level = 4 * (ks / 2) + g, feat = 2 * level + ks % 2;
-        put(fwd_off_d1(lpg) + m * KD + ks, lane, W.D1(feat, 16 * m + c));
-      }
-    for (int ks = 0; ks < 16; ++ks) {
-      int mp = ks / 4, i = ks % 4;
-      put(fwd_off_d2(lpg) + ks, lane, W.D2(16 * mp + 4 * g + i, c));
-      put(fwd_off_c3(lpg) + ks, lane, c < 3 ? W.C3(16 * mp + 4 * g + i, c) : 0.0f);
-      for (int m = 0; m < 4; ++m) put(fwd_off_c2(lpg) + m * 16 + ks, lane, W.C2(16 * mp + 4 * g + i, 16 * m + c));
-    }
-    for (int m = 0; m < 4; ++m)
-      for (int i = 0; i < 4; ++i) {
-        int hidx = 4 * g + i;  // h index; x_c index hidx - 1 (h_0 is not an input)
-        put(fwd_off_c1(lpg) + m * 8 + i, lane, hidx >= 1 ? W.C1(hidx - 1, 16 * m + c) : 0.0f);
-        put(fwd_off_c1(lpg) + m * 8 + 4 + i, lane, W.C1(15 + 4 * g + i, 16 * m + c));
-      }
-  }
+uint16_t bf16_rn(float x) {
+  uint32_t u;
+  std::memcpy(&u, &x, 4);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);  // NaN
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
 }
 
-void build_bwd_tiles(const Weights& W, int lpg, std::vector<float>& t) {
-  t.assign(bwd_tile_floats(lpg), 0.0f);
-  auto put = [&](int unit, int lane, float v) { t[(size_t)unit * 64 + lane] = v; };
-  const int MD = (lpg + 1) / 2;
+float bf16_value(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float x;
+  std::memcpy(&x, &u, 4);
+  return x;
+}
+
+struct Units {
+  std::vector<uint16_t> v;  // [unit][hi, lo][lane][8]
+  explicit Units(int n) : v((size_t)n * 2 * 64 * 8, 0) {}
+  void put(int unit, int lane, int j, float w) {
+    const uint16_t hi = bf16_rn(w);
+    const uint16_t lo = bf16_rn(w - bf16_value(hi));
+    v[(((size_t)unit * 2 + 0) * 64 + lane) * 8 + j] = hi;
+    v[(((size_t)unit * 2 + 1) * 64 + lane) * 8 + j] = lo;
+  }
+};
+
+// hidden unit at K position j of lane group g in K step s
+inline int kpos(int s, int g, int j) { return 16 * (2 * s + j / 4) + 4 * g + j % 4; }
+
+Units build_fwd_units(const Weights& W, int lpg) {
+  Units U(kFwdUnits);
   for (int lane = 0; lane < 64; ++lane) {
-    int g = lane / 16, c = lane % 16;
-    for (int m = 0; m < 4; ++m) put(bwd_off_c3(lpg) + m, lane, g < 3 ? W.C3(16 * m + c, g) : 0.0f);
-    for (int ks = 0; ks < 16; ++ks) {
-      int mp = ks / 4, i = ks % 4, kin = 16 * mp + 4 * g + i;
-      for (int m = 0; m < 4; ++m) put(bwd_off_c2(lpg) + m * 16 + ks, lane, W.C2(16 * m + c, kin));
-      put(bwd_off_c1(lpg) + ks, lane, c >= 1 ? W.C1(c - 1, kin) : 0.0f);
-      put(bwd_off_c1(lpg) + 16 + ks, lane, W.C1(15 + c, kin));
-      for (int m = 0; m < MD; ++m) {
-        int gp = c / 4, ip = c % 4, j = 2 * m + ip / 2;
-        float v = 0.0f;
-        if (j < lpg) v = W.D1(2 * (4 * j + gp) + ip % 2, kin);
-        put(bwd_off_d1(lpg) + m * 16 + ks, lane, v);
+    const int g = lane / 16, r = lane % 16;
+    for (int j = 0; j < 8; ++j) {
+      for (int m = 0; m < 4; ++m) {
+        // density 1: position j = feature j % 2 of level 4 (j / 2) + g
+        if (j < 2 * lpg) U.put(kFD1 + m, lane, j, W.D1(2 * (4 * (j / 2) + g) + j % 2, 16 * m + r));
+        // colour 1: positions 0..3 = h_{4g+j} (x_c index 4g+j-1; h_0 has no weight),
+        // positions 4..7 = SH_{4g+j-4} (x_c index 15 + 4g + j - 4)
+        const int hidx = 4 * g + j;
+        if (j < 4)
+          U.put(kFC1 + m, lane, j, hidx >= 1 ? W.C1(hidx - 1, 16 * m + r) : 0.0f);
+        else
+          U.put(kFC1 + m, lane, j, W.C1(15 + 4 * g + (j - 4), 16 * m + r));
+      }
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int u = kpos(s2, g, j);
+        U.put(kFD2 + s2, lane, j, W.D2(u, r));
+        U.put(kFC3 + s2, lane, j, r < 3 ? W.C3(u, r) : 0.0f);
+        for (int m = 0; m < 4; ++m) U.put(kFC2 + 2 * m + s2, lane, j, W.C2(u, 16 * m + r));
       }
     }
-    for (int m = 0; m < 4; ++m)
-      for (int i = 0; i < 4; ++i) put(bwd_off_d2(lpg) + m * 4 + i, lane, W.D2(16 * m + c, 4 * g + i));
   }
+  return U;
+}
+
+Units build_bwd_units(const Weights& W, int lpg) {
+  Units U(kBwdUnits);
+  const int MD = (lpg + 1) / 2;
+  for (int lane = 0; lane < 64; ++lane) {
+    const int g = lane / 16, r = lane % 16;
+    for (int j = 0; j < 8; ++j) {
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int o = kpos(s2, g, j);  // the layer's output unit (K of the transpose)
+        for (int m = 0; m < 4; ++m) U.put(kBC2 + 2 * m + s2, lane, j, W.C2(16 * m + r, o));
+        U.put(kBC1 + s2, lane, j, r >= 1 ? W.C1(r - 1, o) : 0.0f);  // h rows
+        U.put(kBC1 + 2 + s2, lane, j, W.C1(15 + r, o));              // SH rows
+        // density 1: row r = feature (r % 4) % 2 of level 4 (2 mm + (r % 4) / 2) + r / 4
+        for (int mm = 0; mm < MD; ++mm) {
+          const int jl = 2 * mm + (r % 4) / 2;
+          const float v = jl < lpg ? W.D1(2 * (4 * jl + r / 4) + (r % 4) % 2, o) : 0.0f;
+          U.put(kBD1 + 2 * mm + s2, lane, j, v);
+        }
+      }
+      // density 2: one K step, positions 0..3 = h_{4g+j}
+      for (int m = 0; m < 4; ++m) U.put(kBD2 + m, lane, j, j < 4 ? W.D2(16 * m + r, 4 * g + j) : 0.0f);
+    }
+  }
+  return U;
 }
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -633,9 +665,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   load(p->w_color1, 32 * 64, W.c1);
   load(p->w_color2, 64 * 64, W.c2);
   load(p->w_color3, 64 * 3, W.c3);
-  std::vector<float> tf, tb;
-  build_fwd_tiles(W, d.lpg, tf);
-  build_bwd_tiles(W, d.lpg, tb);
+  Units uf = build_fwd_units(W, d.lpg);
+  Units ub = build_bwd_units(W, d.lpg);
 
   size_t table_elems = (size_t)L * d.T * 2;
   size_t table_bytes = table_elems * (p->param_dtype == 0 ? 4 : 2);
@@ -649,18 +680,21 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   } while (0)
   CF_TRY(hipMalloc(&F->d_table, table_bytes));
   CF_TRY(hipMemcpyAsync(F->d_table, p->table, table_bytes, hipMemcpyHostToDevice, s));
-  CF_TRY(hipMalloc(&F->d_wfwd, tf.size() * 4));
-  CF_TRY(hipMemcpyAsync(F->d_wfwd, tf.data(), tf.size() * 4, hipMemcpyHostToDevice, s));
-  CF_TRY(hipMalloc(&F->d_wbwd, tb.size() * 4));
-  CF_TRY(hipMemcpyAsync(F->d_wbwd, tb.data(), tb.size() * 4, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wfwd, uf.v.size() * 2));
+  CF_TRY(hipMemcpyAsync(F->d_wfwd, uf.v.data(), uf.v.size() * 2, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wbwd, ub.v.size() * 2));
+  CF_TRY(hipMemcpyAsync(F->d_wbwd, ub.v.data(), ub.v.size() * 2, hipMemcpyHostToDevice, s));
+  CF_TRY(hipMalloc(&F->d_wc3, W.c3.size() * 4));
+  CF_TRY(hipMemcpyAsync(F->d_wc3, W.c3.data(), W.c3.size() * 4, hipMemcpyHostToDevice, s));
   CF_TRY(hipMalloc(&F->d_wd1, W.d1.size() * 4));
   CF_TRY(hipMemcpyAsync(F->d_wd1, W.d1.data(), W.d1.size() * 4, hipMemcpyHostToDevice, s));
   CF_TRY(hipMalloc(&F->d_wd2, W.d2.size() * 4));
   CF_TRY(hipMemcpyAsync(F->d_wd2, W.d2.data(), W.d2.size() * 4, hipMemcpyHostToDevice, s));
   d.table32 = p->param_dtype == 0 ? (const float*)F->d_table : nullptr;
   d.table16 = p->param_dtype == 1 ? (const __half*)F->d_table : nullptr;
-  d.wfwd = F->d_wfwd;
-  d.wbwd = F->d_wbwd;
+  d.wfwd = (const WeightUnit*)F->d_wfwd;
+  d.wbwd = (const WeightUnit*)F->d_wbwd;
+  d.wc3 = F->d_wc3;
   d.wd1 = F->d_wd1;
   d.wd2 = F->d_wd2;
   d.occ = nullptr;
@@ -697,6 +731,7 @@ void pnerf_destroy_field(pnerf_field* F) {
   (void)hipFree(F->d_table);
   (void)hipFree(F->d_wfwd);
   (void)hipFree(F->d_wbwd);
+  (void)hipFree(F->d_wc3);
   (void)hipFree(F->d_wd1);
   (void)hipFree(F->d_wd2);
   (void)hipFree(F->d_occ);

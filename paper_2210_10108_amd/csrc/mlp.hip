@@ -5,26 +5,107 @@
 // through the SH input to d loss / d direction), ending in each sample's force
 // and torque terms of Eq. 2 and Eq. 3.
 //
+// Arithmetic: every fp32 operand x is split into bf16 parts x = hi + lo + r
+// (|r| <= 2^-17 |x|), and each product is accumulated in fp32 as
+// hi*hi + hi*lo + lo*hi by v_mfma_f32_16x16x32_bf16 (the dropped lo*lo and r
+// terms are about 2^-16 of the product).  The weights are split once at field
+// creation; fp16-stored weights split exactly.
+//
 // Work unit: one wavefront takes a tile of 64 consecutive compacted samples,
-// as four 16-sample column tiles of v_mfma_f32_16x16x4_f32.  The batch (sample)
-// dimension is the MFMA N dimension, so every layer's output rows (C layout:
-// lane holds rows 4*(lane/16)+i of column lane%16) are directly the next
-// layer's B operand once the K order is permuted; the permutation is baked into
-// the weight tiles built at field creation, which each workgroup stages in LDS.
-// Lane group g = lane/16 reads the features of levels g, g+4, g+8, g+12 of its
-// column's sample (rows 2 LPG g .. of the SoA feature array), which is again
-// exactly the B layout of the first layer.
+// as four 16-sample column tiles.  The batch (sample) dimension is the MFMA N
+// dimension.  A layer's accumulators hold (C layout) rows 4*(lane/16)+i of
+// column lane%16 of each 16-row tile; two such tiles are exactly one 32-deep
+// K step of the next layer's B operand (lane group g holds K positions
+// 8g..8g+7), once the K order -- hidden unit 16(2s + j/4) + 4g + j%4 at
+// position j of step s -- is baked into the weight tiles built at field
+// creation, which each workgroup stages in LDS (hi and lo parts).
+// Lane group g reads the features of levels g, g+4, g+8, g+12 of its column's
+// sample (rows 2 LPG g .. of the SoA feature array): the first layer's B
+// operand.
 #include "pnerf_internal.h"
 
 namespace pnerf {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBlock = 256;  // 4 wavefronts
 
-__device__ __forceinline__ floatx4 mfma(float a, float b, floatx4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+struct Split {
+  bf16x8 hi, lo;
+};
+
+// x = hi + lo (+ a remainder below 2^-17 |x|), both parts rounded to nearest.
+__device__ __forceinline__ Split split8(const float v[8]) {
+  Split s;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const __bf16 h = (__bf16)v[i];
+    s.hi[i] = h;
+    s.lo[i] = (__bf16)(v[i] - (float)h);
+  }
+  return s;
+}
+
+// c += A B for split operands (small terms first).
+__device__ __forceinline__ floatx4 mfma3(const Split& a, const Split& b, floatx4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.lo, b.hi, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b.lo, c, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b.hi, c, 0, 0, 0);
+}
+
+// A operand of weight unit u (hi and lo parts, 16 bytes per lane each).
+__device__ __forceinline__ Split load_unit(const WeightUnit* lds, int u, int lane) {
+  Split s;
+  s.hi = __builtin_bit_cast(bf16x8, lds[u].hi[lane]);
+  s.lo = __builtin_bit_cast(bf16x8, lds[u].lo[lane]);
+  return s;
+}
+
+// B operand of one K step from two accumulator tiles (rows of tile t0 at
+// positions 0..3, of tile t1 at 4..7).
+__device__ __forceinline__ Split pack2(const floatx4& t0, const floatx4& t1) {
+  const float v[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+  return split8(v);
+}
+
+__device__ inline void stage(WeightUnit* lds, const WeightUnit* src, int n_units) {
+  const uint4* s = reinterpret_cast<const uint4*>(src);
+  uint4* d = reinterpret_cast<uint4*>(lds);
+  for (int i = threadIdx.x; i < n_units * 128; i += kBlock) d[i] = s[i];
+}
+
+// Unit ray direction of sample s.
+__device__ __forceinline__ void sample_dir(const DevWork& w, int s, float d[3]) {
+  int ray = w.sray[s];
+  d[0] = w.rdx[ray];
+  d[1] = w.rdy[ray];
+  d[2] = w.rdz[ray];
+}
+
+// ReLU on 4 accumulator tiles of one column tile; bit 4m+i of the mask = unit
+// 16m + 4g + i was active.
+__device__ __forceinline__ uint32_t relu_mask(floatx4 (&t)[4]) {
+  uint32_t mk = 0;
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = t[m][i];
+      const bool on = v > 0.0f;
+      t[m][i] = on ? v : 0.0f;
+      mk |= (on ? 1u : 0u) << (4 * m + i);
+    }
+  return mk;
+}
+
+__device__ __forceinline__ void apply_mask(floatx4 (&t)[4], uint32_t mk) {
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (!((mk >> (4 * m + i)) & 1u)) t[m][i] = 0.0f;
 }
 
 // Real SH of degree 0..3, the 4 functions 4g..4g+3 (no Condon-Shortley phase).
@@ -89,169 +170,113 @@ __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float
   for (int a = 0; a < 3; ++a) gd[a] = gs[0] * G[0][a] + gs[1] * G[1][a] + gs[2] * G[2][a] + gs[3] * G[3][a];
 }
 
-__device__ __forceinline__ float wA(const float* lds, int kstep_unit, int lane) {
-  return lds[kstep_unit * 64 + lane];
-}
-
-__device__ inline void stage(float* lds, const float* src, int n) {
-  for (int i = threadIdx.x; i < n; i += kBlock) lds[i] = src[i];
-  __syncthreads();
-}
-
-// Unit ray direction of sample s.
-__device__ __forceinline__ void sample_dir(const DevWork& w, int s, float d[3]) {
-  int ray = w.sray[s];
-  d[0] = w.rdx[ray];
-  d[1] = w.rdy[ray];
-  d[2] = w.rdz[ray];
-}
-
 // ------------------------------------------------------------------ forward
 // GRAD = false (forward rendering only) skips the ReLU masks the backward
 // pass needs; it is a separate kernel so that profiles keep the two apart.
 template <int LPG, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
-  constexpr int KD = 2 * LPG;  // density-layer K steps
-  __shared__ float lds[fwd_tile_floats(LPG)];
-  stage(lds, f.wfwd, fwd_tile_floats(LPG));
+  constexpr int KD = 2 * LPG;  // features per lane group
+  __shared__ WeightUnit lds[kFwdUnits];
+  stage(lds, f.wfwd, kFwdUnits);
+  __syncthreads();
 
   const int S = *w.total;
   const int n_tiles = (S + kTile - 1) / kTile;
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
-  const float* D1 = lds + 64 * fwd_off_d1(LPG);
-  const float* D2 = lds + 64 * fwd_off_d2(LPG);
-  const float* C1 = lds + 64 * fwd_off_c1(LPG);
-  const float* C2 = lds + 64 * fwd_off_c2(LPG);
-  const float* C3 = lds + 64 * fwd_off_c3(LPG);
+  const float* frow = w.feat + (int64_t)(g * KD) * w.cap;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
-    float feat[4][KD];
+    Split xf[4];
     float shv[4][4];
     int sidx[4];
-    const float* frow = w.feat + (int64_t)(g * KD) * w.cap;
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      int s = tile * kTile + nt * 16 + col;
+      const int s = tile * kTile + nt * 16 + col;
       sidx[nt] = s;
-      int sc = s < S ? s : S - 1;
+      const int sc = s < S ? s : S - 1;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = j < KD ? frow[(int64_t)j * w.cap + sc] : 0.0f;
+      xf[nt] = split8(v);
       float d[3];
       sample_dir(w, sc, d);
       sh4(d, g, shv[nt]);
-#pragma unroll
-      for (int ks = 0; ks < KD; ++ks) feat[nt][ks] = frow[(int64_t)ks * w.cap + sc];
     }
     // density layer 1: a = relu(W_d1^T feat), 4 row tiles of 16 hidden units
     floatx4 acc[4][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < 4; ++m) {
+      const Split a = load_unit(lds, kFD1 + m, lane);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < 4; ++nt) acc[nt][m] = mfma3(a, xf[nt], zero);
+    }
+    uint32_t mk_a[4], mk_b1[4], mk_b2[4];
 #pragma unroll
-    for (int ks = 0; ks < KD; ++ks)
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        float a = wA(D1, m * KD + ks, lane);
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[m][nt] = mfma(a, feat[nt][ks], acc[m][nt]);
-      }
-    uint32_t mk_a[4] = {0, 0, 0, 0}, mk_b1[4] = {0, 0, 0, 0}, mk_b2[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = acc[m][nt][i];
-          bool on = v > 0.0f;
-          acc[m][nt][i] = on ? v : 0.0f;
-          mk_a[nt] |= (on ? 1u : 0u) << (4 * m + i);
-        }
+    for (int nt = 0; nt < 4; ++nt) mk_a[nt] = relu_mask(acc[nt]);
     // density layer 2: h = W_d2^T a (16 outputs)
-    floatx4 h[4];
+    floatx4 h[4] = {zero, zero, zero, zero};
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) h[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = wA(D2, 4 * m + i, lane);
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) h[nt] = mfma(a, acc[m][nt][i], h[nt]);
-      }
-    // colour layer 1 on [h (h_0 row has zero weights), SH_16]
-    floatx4 b1[4][4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) b1[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        float a = wA(C1, m * 8 + i, lane);
-        float a2 = wA(C1, m * 8 + 4 + i, lane);
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          b1[m][nt] = mfma(a, h[nt][i], b1[m][nt]);
-          b1[m][nt] = mfma(a2, shv[nt][i], b1[m][nt]);
-        }
-      }
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const Split a = load_unit(lds, kFD2 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
+        h[nt] = mfma3(a, pack2(acc[nt][2 * s2], acc[nt][2 * s2 + 1]), h[nt]);
+    }
+    // colour layer 1 on [h (h_0 has zero weights), SH_16]
+    floatx4 b1[4][4];
+    {
+      Split xc[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = b1[m][nt][i];
-          bool on = v > 0.0f;
-          b1[m][nt][i] = on ? v : 0.0f;
-          mk_b1[nt] |= (on ? 1u : 0u) << (4 * m + i);
-        }
+      for (int nt = 0; nt < 4; ++nt) {
+        const float v[8] = {h[nt][0], h[nt][1], h[nt][2], h[nt][3],
+                            shv[nt][0], shv[nt][1], shv[nt][2], shv[nt][3]};
+        xc[nt] = split8(v);
+      }
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const Split a = load_unit(lds, kFC1 + m, lane);
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) b1[nt][m] = mfma3(a, xc[nt], zero);
+      }
+    }
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) mk_b1[nt] = relu_mask(b1[nt]);
     // colour layer 2
     floatx4 b2[4][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) b2[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int m = 0; m < 4; ++m) b2[nt][m] = zero;
 #pragma unroll
-    for (int mp = 0; mp < 4; ++mp)
+    for (int s2 = 0; s2 < 2; ++s2) {
+      Split x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(b1[nt][2 * s2], b1[nt][2 * s2 + 1]);
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          float a = wA(C2, m * 16 + 4 * mp + i, lane);
+      for (int m = 0; m < 4; ++m) {
+        const Split a = load_unit(lds, kFC2 + 2 * m + s2, lane);
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) b2[m][nt] = mfma(a, b1[mp][nt][i], b2[m][nt]);
-        }
+        for (int nt = 0; nt < 4; ++nt) b2[nt][m] = mfma3(a, x[nt], b2[nt][m]);
+      }
+    }
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int nt = 0; nt < 4; ++nt) mk_b2[nt] = relu_mask(b2[nt]);
+    // colour layer 3 (3 outputs in rows 0..2)
+    floatx4 z[4] = {zero, zero, zero, zero};
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const Split a = load_unit(lds, kFC3 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = b2[m][nt][i];
-          bool on = v > 0.0f;
-          b2[m][nt][i] = on ? v : 0.0f;
-          mk_b2[nt] |= (on ? 1u : 0u) << (4 * m + i);
-        }
-    // colour layer 3 (3 outputs in rows 0..2)
-    floatx4 z[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) z[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int mp = 0; mp < 4; ++mp)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = wA(C3, 4 * mp + i, lane);
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) z[nt] = mfma(a, b2[mp][nt][i], z[nt]);
-      }
+        z[nt] = mfma3(a, pack2(b2[nt][2 * s2], b2[nt][2 * s2 + 1]), z[nt]);
+    }
     // outputs: rows 0..3 live in lane group 0
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      int s = sidx[nt];
+      const int s = sidx[nt];
       if (g == 0 && s < S) {
         w.sig[s] = __expf(h[nt][0] + f.density_bias);
         w.cr[s] = 1.0f / (1.0f + __expf(-z[nt][0]));
@@ -272,146 +297,131 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
 // ----------------------------------------------------------------- backward
 template <int LPG>
 __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevWork w) {
-  constexpr int MD = (LPG + 1) / 2;  // row tiles of the first-layer input gradient
-  __shared__ float lds[bwd_tile_floats(LPG)];
-  stage(lds, f.wbwd, bwd_tile_floats(LPG));
+  constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
+  __shared__ WeightUnit lds[kBwdUnits];
+  __shared__ float s_c3[64 * 3];
+  stage(lds, f.wbwd, kBwdUnits);
+  for (int i = threadIdx.x; i < 64 * 3; i += kBlock) s_c3[i] = f.wc3[i];
+  __syncthreads();
 
   const int S = *w.total;
   const int n_tiles = (S + kTile - 1) / kTile;
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
-  const float* C3 = lds + 64 * bwd_off_c3(LPG);
-  const float* C2 = lds + 64 * bwd_off_c2(LPG);
-  const float* C1 = lds + 64 * bwd_off_c1(LPG);
-  const float* D2 = lds + 64 * bwd_off_d2(LPG);
-  const float* D1 = lds + 64 * bwd_off_d1(LPG);
   const bool dir_grad = f.sh_dir_grad != 0;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
-    uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
+    const uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
     uint32_t mk_a[4], mk_b1[4], mk_b2[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      uint32_t v = mw[nt * 64];
+      const uint32_t v = mw[nt * 64];
       mk_a[nt] = v & 0xFFFFu;
       mk_b1[nt] = v >> 16;
     }
     {
-      uint32_t v4 = mw[4 * 64], v5 = mw[5 * 64];
+      const uint32_t v4 = mw[4 * 64], v5 = mw[5 * 64];
       mk_b2[0] = v4 & 0xFFFFu;
       mk_b2[1] = v4 >> 16;
       mk_b2[2] = v5 & 0xFFFFu;
       mk_b2[3] = v5 >> 16;
     }
-    float gzv[4], gh0[4];
+    // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
+    // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
+    floatx4 gb2[4][4];
+    float gh0[4];
     int sidx[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
-      int s = tile * kTile + nt * 16 + col;
+      const int s = tile * kTile + nt * 16 + col;
       sidx[nt] = s;
-      int sc = s < S ? s : S - 1;
-      const float* src = g == 0 ? w.cr : (g == 1 ? w.cg : w.cb);
-      gzv[nt] = g < 3 && s < S ? src[sc] : 0.0f;
-      gh0[nt] = g == 0 && s < S ? w.sig[sc] : 0.0f;
-    }
-    // colour layer 3 transposed: gb2 = W_c3 gz (one K step: channels in lane groups)
-    floatx4 gb2[4][4];
+      const int sc = s < S ? s : S - 1;
+      const bool ok = s < S;
+      const float z0 = ok ? w.cr[sc] : 0.0f, z1 = ok ? w.cg[sc] : 0.0f, z2 = ok ? w.cb[sc] : 0.0f;
+      gh0[nt] = g == 0 && ok ? w.sig[sc] : 0.0f;
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      float a = wA(C3, m, lane);
+      for (int m = 0; m < 4; ++m)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        gb2[m][nt] = mfma(a, gzv[nt], floatx4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (!((mk_b2[nt] >> (4 * m + i)) & 1u)) gb2[m][nt][i] = 0.0f;
-      }
+        for (int i = 0; i < 4; ++i) {
+          const float* c3 = s_c3 + 3 * (16 * m + 4 * g + i);
+          gb2[nt][m][i] = c3[0] * z0 + c3[1] * z1 + c3[2] * z2;
+        }
+      apply_mask(gb2[nt], mk_b2[nt]);
     }
     // colour layer 2 transposed
     floatx4 gb1[4][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int nt = 0; nt < 4; ++nt)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) gb1[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int m = 0; m < 4; ++m) gb1[nt][m] = zero;
 #pragma unroll
-    for (int mp = 0; mp < 4; ++mp)
+    for (int s2 = 0; s2 < 2; ++s2) {
+      Split x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1]);
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          float a = wA(C2, m * 16 + 4 * mp + i, lane);
+      for (int m = 0; m < 4; ++m) {
+        const Split a = load_unit(lds, kBC2 + 2 * m + s2, lane);
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) gb1[m][nt] = mfma(a, gb2[mp][nt][i], gb1[m][nt]);
-        }
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (!((mk_b1[nt] >> (4 * m + i)) & 1u)) gb1[m][nt][i] = 0.0f;
-    // colour layer 1 transposed: rows = h index (row 0 has zero weights); optional SH rows
-    floatx4 gh[4], gsh[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      gh[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
-      gsh[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int nt = 0; nt < 4; ++nt) gb1[nt][m] = mfma3(a, x[nt], gb1[nt][m]);
+      }
     }
 #pragma unroll
-    for (int mp = 0; mp < 4; ++mp)
+    for (int nt = 0; nt < 4; ++nt) apply_mask(gb1[nt], mk_b1[nt]);
+    // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
+    floatx4 gh[4] = {zero, zero, zero, zero}, gsh[4] = {zero, zero, zero, zero};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = wA(C1, 4 * mp + i, lane);
+    for (int s2 = 0; s2 < 2; ++s2) {
+      Split x[4];
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) gh[nt] = mfma(a, gb1[mp][nt][i], gh[nt]);
+      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1]);
+      const Split a = load_unit(lds, kBC1 + s2, lane);
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
+      if (dir_grad) {
+        const Split a2 = load_unit(lds, kBC1 + 2 + s2, lane);
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) gsh[nt] = mfma3(a2, x[nt], gsh[nt]);
       }
-    if (dir_grad) {
-#pragma unroll
-      for (int mp = 0; mp < 4; ++mp)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float a = wA(C1, 16 + 4 * mp + i, lane);
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt) gsh[nt] = mfma(a, gb1[mp][nt][i], gsh[nt]);
-        }
     }
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) gh[nt][0] += gh0[nt];  // d loss / d h_0 (zero off group 0)
-    // density layer 2 transposed: ga = W_d2 gh, masked
+    // density layer 2 transposed: ga = W_d2 gh (one K step, upper half zero), masked
     floatx4 ga[4][4];
+    {
+      Split x[4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
+      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gh[nt], zero);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) ga[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int m = 0; m < 4; ++m) {
+        const Split a = load_unit(lds, kBD2 + m, lane);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float a = wA(D2, m * 4 + i, lane);
-#pragma unroll
-        for (int nt = 0; nt < 4; ++nt) ga[m][nt] = mfma(a, gh[nt][i], ga[m][nt]);
+        for (int nt = 0; nt < 4; ++nt) ga[nt][m] = mfma3(a, x[nt], zero);
       }
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (!((mk_a[nt] >> (4 * m + i)) & 1u)) ga[m][nt][i] = 0.0f;
     }
-    // density layer 1 transposed: gf rows permuted so lane group g gets its levels
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) apply_mask(ga[nt], mk_a[nt]);
+    // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
+    // level 4 (2 mm + i / 2) + g, so lane group g gets its own levels
     floatx4 gf[MD][4];
 #pragma unroll
-    for (int m = 0; m < MD; ++m)
+    for (int mm = 0; mm < MD; ++mm)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) gf[m][nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int nt = 0; nt < 4; ++nt) gf[mm][nt] = zero;
 #pragma unroll
-    for (int mp = 0; mp < 4; ++mp)
+    for (int s2 = 0; s2 < 2; ++s2) {
+      Split x[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1]);
 #pragma unroll
-        for (int m = 0; m < MD; ++m) {
-          float a = wA(D1, m * 16 + 4 * mp + i, lane);
+      for (int mm = 0; mm < MD; ++mm) {
+        const Split a = load_unit(lds, kBD1 + 2 * mm + s2, lane);
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) gf[m][nt] = mfma(a, ga[mp][nt][i], gf[m][nt]);
-        }
+        for (int nt = 0; nt < 4; ++nt) gf[mm][nt] = mfma3(a, x[nt], gf[mm][nt]);
+      }
+    }
     // d loss / d p = sum over the lane group's levels 4j + g of
     // d loss / d feature times the stored Jacobian, then over the 4 groups;
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)

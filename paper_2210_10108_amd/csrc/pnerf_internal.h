@@ -18,24 +18,19 @@ constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays pe
 constexpr int kReduceBlocks = 2048;   // target blocks of the per-hypothesis reduction
 constexpr int kMaxReduceParts = 64;   // parts per hypothesis (K * parts <= max(K, 2048) * 7 floats)
 
-// Sizes (in floats) of the MFMA A-operand weight tiles, see the layout built in api.hip.
-__host__ __device__ constexpr int fwd_tile_floats(int lpg) {
-  return (4 * 2 * lpg + 16 + 4 * 8 + 4 * 16 + 16) * 64;
-}
-__host__ __device__ constexpr int bwd_tile_floats(int lpg) {
-  return (4 * 1 + 4 * 16 + 2 * 16 + 4 * 4 + ((lpg + 1) / 2) * 16) * 64;
-}
-// offsets (in 64-float K-step units) of each layer inside the tile blocks
-__host__ __device__ constexpr int fwd_off_d1(int) { return 0; }
-__host__ __device__ constexpr int fwd_off_d2(int lpg) { return 4 * 2 * lpg; }
-__host__ __device__ constexpr int fwd_off_c1(int lpg) { return fwd_off_d2(lpg) + 16; }
-__host__ __device__ constexpr int fwd_off_c2(int lpg) { return fwd_off_c1(lpg) + 4 * 8; }
-__host__ __device__ constexpr int fwd_off_c3(int lpg) { return fwd_off_c2(lpg) + 4 * 16; }
-__host__ __device__ constexpr int bwd_off_c3(int) { return 0; }
-__host__ __device__ constexpr int bwd_off_c2(int) { return 4; }
-__host__ __device__ constexpr int bwd_off_c1(int) { return 4 + 64; }        // 2 M-tiles (h rows, SH rows)
-__host__ __device__ constexpr int bwd_off_d2(int) { return 4 + 64 + 32; }
-__host__ __device__ constexpr int bwd_off_d1(int) { return 4 + 64 + 32 + 16; }
+// A operand of one (row tile, K step) of v_mfma_f32_16x16x32_bf16: 8 bf16
+// values per lane, as a high part and the low part of the fp32 weight.  Lane
+// l = 16 g + r supplies row r and K positions 8g .. 8g+7.
+struct alignas(16) WeightUnit {
+  uint4 hi[64];
+  uint4 lo[64];
+};
+// unit indices of the forward tiles: density layer 1 (4 row tiles), layer 2
+// (2 K steps), colour layer 1 (4 row tiles), layer 2 (4 x 2), layer 3 (2 K steps)
+constexpr int kFD1 = 0, kFD2 = 4, kFC1 = 6, kFC2 = 10, kFC3 = 18, kFwdUnits = 20;
+// backward (transposed layers): colour 2 (4 x 2), colour 1 (h rows, SH rows) x 2
+// K steps, density 2 (4 row tiles), density 1 (up to 2 row tiles x 2 K steps)
+constexpr int kBC2 = 0, kBC1 = 8, kBD2 = 12, kBD1 = 16, kBwdUnits = 20;
 
 struct DevField {
   int32_t L, lpg;               // levels, levels per lane group (L / 4)
@@ -48,8 +43,9 @@ struct DevField {
   int32_t grp_lv[kMaxGroups][2];   // the two levels of each group
   const float* table32;         // [L][T][2]
   const __half* table16;        // [L][T][2]
-  const float* wfwd;            // forward A-operand tiles (fp32)
-  const float* wbwd;            // backward A-operand tiles (fp32)
+  const WeightUnit* wfwd;       // forward A-operand tiles [kFwdUnits]
+  const WeightUnit* wbwd;       // backward A-operand tiles [kBwdUnits]
+  const float* wc3;             // W_c3 [64][3] (fp32, transposed colour layer 3)
   const float* wd1;             // plain W_d1 [2L][64] and W_d2 [64][16] (occupancy build)
   const float* wd2;
   float density_bias;
