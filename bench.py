@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--overlap-chunks", type=int, default=0,
+                    help="field option: loss-gradient chunks pipelined over two streams "
+                         "(0 = library default, 1 = off)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (3 times), whose "
                          "FETCH_SIZE / WRITE_SIZE calibrate the profiler's byte counters")
@@ -114,7 +117,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     fa = synth.make_field(w, args.seed)
     spec = synth.field_spec(w, fa)        # occupancy (if any) built on the device
-    field = pnerf.Field(spec)
+    field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
     poses0 = synth.perturb_poses(gt, w.K, w.max_rot_deg, w.max_trans, args.seed)

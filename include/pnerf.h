@@ -123,8 +123,18 @@ typedef struct {
   int32_t sh_dir_grad;          /* 0 or 1 */
   int64_t max_workspace_bytes;  /* workspace budget; 0 = 96 GiB.  A batch whose
                                    samples need more is processed in chunks of
-                                   whole hypotheses (about 48 + 32 L bytes per
+                                   whole hypotheses (about 56 + 32 L bytes per
                                    sample). */
+  int32_t overlap_chunks;       /* render_loss_grad cuts a batch of 2^16 samples or
+                                   more into this many chunks of whole hypotheses
+                                   and runs the encoding of one chunk alongside
+                                   the networks of the previous, on two internal
+                                   streams (two sample buffers); 0 or 1 = off
+                                   (pnerf_field_inspect needs it off), at most
+                                   64.  Off by default: every kernel of the path
+                                   loads through the same L1 address path, and
+                                   on the 16 x 1024-ray workload the overlapped
+                                   chunks ran slower than one chunk. */
 } pnerf_field_params;
 
 /* Create a field: validates `params`, copies every array to the device (builds

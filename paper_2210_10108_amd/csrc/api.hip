@@ -78,10 +78,16 @@ struct pnerf_field {
   // workspace: per-ray arrays of one counted batch, per-sample arrays of one chunk
   void* d_rays = nullptr;
   size_t rays_bytes = 0;
-  int rays_cap = 0;
-  void* d_samp = nullptr;
+  int rays_cap = 0, rays_hyp = 0;
+  void* d_samp[2] = {nullptr, nullptr};  // two sample buffers (pipelined chunks alternate)
   size_t samp_bytes = 0;
   int64_t samp_cap = 0;
+  int n_slots = 0;              // sample buffers allocated (1 or 2)
+  int overlap_chunks = 0;       // chunks a loss-gradient batch is cut into for overlap
+  // internal streams of the pipelined loss gradient: encoding | networks
+  hipStream_t s_enc = nullptr, s_mlp = nullptr;
+  hipEvent_t ev_start = nullptr, ev_enc[2] = {nullptr, nullptr}, ev_mlp[2] = {nullptr, nullptr};
+  hipEvent_t ev_end_enc = nullptr, ev_end_mlp = nullptr;
   int32_t* d_totals = nullptr;  // [max_chunks] sample totals of the chunks, + 1 counted total
   int max_chunks = 0;
   int32_t* h_hyp = nullptr;     // pinned host copy of the per-hypothesis sample counts
@@ -89,7 +95,7 @@ struct pnerf_field {
   int last_chunks = 0;
   int64_t last_total = 0;
   int64_t budget = 0;
-  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0;
+  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0, enc_blocks_overlap = 0;
   // profiling
   bool profiling = false;
   std::vector<KernelStat> stats;
@@ -212,11 +218,12 @@ struct Carver {
 // sample chunks' own exclusive offsets.
 struct RayWs {
   float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta, *rex, *rey, *rez;
-  int32_t *count, *off, *offc, *blocksum, *hyp_total;
-  float *ray_loss, *partial;
+  int32_t *count, *off, *blocksum, *hyp_total;
+  int32_t* offc[2];             // per sample buffer: the chunk's own offsets,
+  float *ray_loss[2], *partial[2];  // per-ray losses and reduction partials
 };
 
-size_t carve_rays(int n_rays, RayWs* r, char* base) {
+size_t carve_rays(int n_rays, int n_hyp, RayWs* r, char* base) {
   Carver c{base};
   const size_t R = (size_t)n_rays;
   RayWs tmp{};
@@ -232,12 +239,13 @@ size_t carve_rays(int n_rays, RayWs* r, char* base) {
   x.rez = c.take<float>(R);
   x.count = c.take<int32_t>(R);
   x.off = c.take<int32_t>(R + 1);
-  x.offc = c.take<int32_t>(R + 1);
   x.blocksum = c.take<int32_t>((R + 255) / 256);
   x.hyp_total = c.take<int32_t>(R);
-  x.ray_loss = c.take<float>(R);
-  // K * parts <= max(K, kReduceBlocks + K) and K <= n_rays
-  x.partial = c.take<float>((R + kReduceBlocks) * 7);
+  for (int q = 0; q < 2; ++q) {
+    x.offc[q] = c.take<int32_t>(R + 1);
+    x.ray_loss[q] = c.take<float>(R);
+    x.partial[q] = c.take<float>((size_t)n_hyp * kReduceParts * 7);
+  }
   return c.off;
 }
 
@@ -264,7 +272,7 @@ size_t carve_samples(const DevField& f, int64_t cap, DevWork* w, char* base) {
 // sample chunk (per-ray arrays from the chunk's first ray, its own offsets).
 DevWork counted_work(pnerf_field* F) {
   RayWs r{};
-  carve_rays(F->rays_cap, &r, (char*)F->d_rays);
+  carve_rays(F->rays_cap, F->rays_hyp, &r, (char*)F->d_rays);
   DevWork w{};
   w.rdx = r.rdx; w.rdy = r.rdy; w.rdz = r.rdz;
   w.rtn = r.rtn; w.rtf = r.rtf; w.rdelta = r.rdelta;
@@ -273,26 +281,24 @@ DevWork counted_work(pnerf_field* F) {
   w.off = r.off;
   w.blocksum = r.blocksum;
   w.hyp_total = r.hyp_total;
-  w.ray_loss = r.ray_loss;
-  w.partial = r.partial;
   w.total = F->d_totals + F->max_chunks;
   return w;
 }
 
-DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id) {
+DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id, int slot) {
   RayWs r{};
-  carve_rays(F->rays_cap, &r, (char*)F->d_rays);
+  carve_rays(F->rays_cap, F->rays_hyp, &r, (char*)F->d_rays);
   DevWork w{};
-  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp);
+  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp[slot]);
   w.rdx = r.rdx + ray_base; w.rdy = r.rdy + ray_base; w.rdz = r.rdz + ray_base;
   w.rtn = r.rtn + ray_base; w.rtf = r.rtf + ray_base; w.rdelta = r.rdelta + ray_base;
   w.rex = r.rex + ray_base; w.rey = r.rey + ray_base; w.rez = r.rez + ray_base;
   w.count = r.count + ray_base;
-  w.off = r.offc;
+  w.off = r.offc[slot];
   w.blocksum = nullptr;
   w.hyp_total = nullptr;
-  w.ray_loss = r.ray_loss;
-  w.partial = r.partial;
+  w.ray_loss = r.ray_loss[slot];
+  w.partial = r.partial[slot];
   w.total = F->d_totals + chunk_id;
   return w;
 }
@@ -302,19 +308,23 @@ int64_t bytes_per_sample(const DevField& f) {
 }
 
 pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s) {
-  if (n_rays > F->rays_cap) {
+  if (n_rays > F->rays_cap || n_hyp > F->rays_hyp) {
+    n_rays = std::max(n_rays, F->rays_cap);
+    n_hyp = std::max(n_hyp, F->rays_hyp);
     if (F->d_rays) {
       HIP_TRY(hipStreamSynchronize(s));
       HIP_TRY(hipFree(F->d_rays));
       F->d_rays = nullptr;
       F->rays_cap = 0;
+      F->rays_hyp = 0;
     }
-    size_t bytes = carve_rays(n_rays, nullptr, nullptr);
+    size_t bytes = carve_rays(n_rays, n_hyp, nullptr, nullptr);
     hipError_t e = hipMalloc(&F->d_rays, bytes);
     if (e != hipSuccess)
       return fail(PNERF_ERR_OUT_OF_MEMORY, "ray workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
     F->rays_bytes = bytes;
     F->rays_cap = n_rays;
+    F->rays_hyp = n_hyp;
   }
   if (n_hyp > F->h_hyp_cap) {
     if (F->h_hyp) {
@@ -329,9 +339,10 @@ pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s) {
   return PNERF_OK;
 }
 
-// Grow the sample workspace to hold `need` samples (a quarter more than asked
-// when it grows, within `limit`), and the per-chunk totals to n_chunks.
-pnerf_status ensure_samples(pnerf_field* F, int64_t need, int64_t limit, int n_chunks,
+// Grow the sample workspace to `slots` buffers of `need` samples each (a
+// quarter more than asked when it grows, within `limit`), and the per-chunk
+// totals to n_chunks.
+pnerf_status ensure_samples(pnerf_field* F, int64_t need, int64_t limit, int n_chunks, int slots,
                             hipStream_t s) {
   if (n_chunks > F->max_chunks) {
     if (F->d_totals) {
@@ -344,21 +355,40 @@ pnerf_status ensure_samples(pnerf_field* F, int64_t need, int64_t limit, int n_c
     F->max_chunks = nc;
   }
   need = std::max<int64_t>(need, 1);
-  if (need <= F->samp_cap) return PNERF_OK;
-  int64_t cap = std::max(need, std::min(limit, F->samp_cap + F->samp_cap / 4));
+  if (need <= F->samp_cap && slots <= F->n_slots) return PNERF_OK;
+  int64_t cap = need <= F->samp_cap ? F->samp_cap
+                                     : std::max(need, std::min(limit, F->samp_cap + F->samp_cap / 4));
   cap = (cap + kTile - 1) / kTile * kTile;
-  if (F->d_samp) {
-    HIP_TRY(hipStreamSynchronize(s));
-    HIP_TRY(hipFree(F->d_samp));
-    F->d_samp = nullptr;
-    F->samp_cap = 0;
+  slots = std::max(slots, F->n_slots);
+  HIP_TRY(hipStreamSynchronize(s));
+  for (int q = 0; q < 2; ++q) {
+    if (F->d_samp[q]) HIP_TRY(hipFree(F->d_samp[q]));
+    F->d_samp[q] = nullptr;
   }
+  F->samp_cap = 0;
+  F->n_slots = 0;
   size_t bytes = carve_samples(F->dev, cap, nullptr, nullptr);
-  hipError_t e = hipMalloc(&F->d_samp, bytes);
-  if (e != hipSuccess)
-    return fail(PNERF_ERR_OUT_OF_MEMORY, "sample workspace of %zu bytes: %s", bytes, hipGetErrorString(e));
+  for (int q = 0; q < slots; ++q) {
+    hipError_t e = hipMalloc(&F->d_samp[q], bytes);
+    if (e != hipSuccess)
+      return fail(PNERF_ERR_OUT_OF_MEMORY, "sample workspace of %zu bytes: %s", bytes,
+                  hipGetErrorString(e));
+  }
   F->samp_bytes = bytes;
   F->samp_cap = cap;
+  F->n_slots = slots;
+  return PNERF_OK;
+}
+
+// Internal streams (default priority, non-blocking) and events of the
+// pipelined loss gradient, made on first use.
+pnerf_status ensure_pipeline(pnerf_field* F) {
+  if (F->s_enc) return PNERF_OK;
+  HIP_TRY(hipStreamCreateWithFlags(&F->s_enc, hipStreamNonBlocking));
+  HIP_TRY(hipStreamCreateWithFlags(&F->s_mlp, hipStreamNonBlocking));
+  hipEvent_t* evs[] = {&F->ev_start, &F->ev_enc[0], &F->ev_enc[1], &F->ev_mlp[0], &F->ev_mlp[1],
+                       &F->ev_end_enc, &F->ev_end_mlp};
+  for (hipEvent_t* e : evs) HIP_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
   return PNERF_OK;
 }
 
@@ -455,51 +485,75 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
     return fail(PNERF_ERR_CAPACITY, "march inspection needs K*P <= %lld rays", (long long)max_rays);
   pnerf_status st = ensure_rays(F, kr * P, kr, s);
   if (st != PNERF_OK) return st;
-  const int64_t per_sample = bytes_per_sample(F->dev);
+  const int64_t per_sample = bytes_per_sample(F->dev);  // per buffer
   const int64_t limit = std::min<int64_t>(
       std::max<int64_t>((F->budget - (int64_t)F->rays_bytes) / per_sample, kTile),
       ((int64_t)1 << 31) - 4 * kTile);
+  // loss gradient: several chunks, encoding of one overlapping the networks of
+  // the previous, on two internal streams with a sample buffer each
+  const int n_target = mode == kLossGrad ? std::max(1, F->overlap_chunks) : 1;
+  const bool pipe = n_target > 1;
+  if (pipe) {
+    st = ensure_pipeline(F);
+    if (st != PNERF_OK) return st;
+  }
+  const int64_t slot_limit = pipe ? std::max<int64_t>(limit / 2, kTile) : limit;
   int chunk_id = 0;
   int64_t grand = 0;
   for (int h0 = 0; h0 < K; h0 += kr) {
     const int hn = std::min(kr, K - h0);
     DevBatch bb = make_batch(hn, poses + (size_t)12 * h0, P, pix + (size_t)P * h0, obs, intr);
-    st = ensure_samples(F, 0, limit, chunk_id + 1, s);  // totals array for the counted batch
+    st = ensure_samples(F, 0, slot_limit, chunk_id + 1, 1, s);  // totals array for the counted batch
     if (st != PNERF_OK) return st;
     DevWork wb = counted_work(F);
     HIP_TRY(timed(F, "march", s, [&] { return launch_march_count(F->dev, bb, wb, s); }));
     HIP_TRY(hipMemcpyAsync(F->h_hyp, wb.hyp_total, sizeof(int32_t) * hn, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    // chunks of whole hypotheses
+    // chunks of whole hypotheses: about 1/n_target of the samples each (when
+    // pipelined) and never more than a buffer holds
+    int64_t counted = 0;
+    for (int k = 0; k < hn; ++k) counted += F->h_hyp[k];
+    const bool pipe_here = pipe && hn > 1 && counted >= (int64_t)kMinOverlapSamples;
+    const int64_t cap_c = pipe_here ? slot_limit : limit;
+    const int64_t goal = pipe_here ? (counted + n_target - 1) / n_target : cap_c;
     std::vector<int> cut{0};
     std::vector<int64_t> sums;
-    int64_t biggest = 0, counted = 0;
+    int64_t biggest = 0;
     for (int a = 0; a < hn;) {
       int64_t sum = 0;
       int b = a;
-      while (b < hn && sum + F->h_hyp[b] <= limit) sum += F->h_hyp[b++];
+      while (b < hn && sum + F->h_hyp[b] <= cap_c && (sum < goal || b == a)) sum += F->h_hyp[b++];
       if (b == a)
         return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace budget "
-                    "holds (%lld)", h0 + a, F->h_hyp[a], (long long)limit);
+                    "holds (%lld)", h0 + a, F->h_hyp[a], (long long)cap_c);
       cut.push_back(b);
       sums.push_back(sum);
       biggest = std::max(biggest, sum);
-      counted += sum;
       a = b;
     }
     const int n_chunks = (int)sums.size();
-    st = ensure_samples(F, biggest, limit, chunk_id + n_chunks, s);
+    const bool overlap = pipe_here && n_chunks > 1;
+    st = ensure_samples(F, biggest, cap_c, chunk_id + n_chunks, overlap ? 2 : 1, s);
     if (st != PNERF_OK) return st;
     wb = counted_work(F);
+    hipStream_t se = overlap ? F->s_enc : s, sm = overlap ? F->s_mlp : s;
+    if (overlap) {
+      HIP_TRY(hipEventRecord(F->ev_start, s));
+      HIP_TRY(hipStreamWaitEvent(se, F->ev_start, 0));
+      HIP_TRY(hipStreamWaitEvent(sm, F->ev_start, 0));
+    }
     int64_t base = 0;  // samples of the counted batch before this chunk
     for (int c = 0; c < n_chunks; ++c, ++chunk_id) {
       const int a = cut[c], kn = cut[c + 1] - cut[c], k0 = h0 + a;
+      const int slot = overlap ? c & 1 : 0;
       DevBatch b = make_batch(kn, poses + (size_t)12 * k0, P, pix + (size_t)P * k0, obs, intr);
-      DevWork w = chunk_work(F, a * P, chunk_id);
+      DevWork w = chunk_work(F, a * P, chunk_id, slot);
+      // the buffer is free once the networks of chunk c - 2 are done
+      if (overlap) HIP_TRY(hipStreamWaitEvent(se, F->ev_mlp[slot], 0));
       // inspection: lattice indices go to the (otherwise unused) blue-channel buffer
       int32_t* j_tmp = mode == kMarch ? reinterpret_cast<int32_t*>(w.cb) : nullptr;
-      HIP_TRY(timed(F, "march_write", s, [&] {
-        return launch_march_write(F->dev, b, wb, w, a * P, (int)base, (int)sums[c], j_tmp, s);
+      HIP_TRY(timed(F, "march_write", se, [&] {
+        return launch_march_write(F->dev, b, wb, w, a * P, (int)base, (int)sums[c], j_tmp, se);
       }));
       if (mode == kMarch) {
         const bool last = k0 + kn == K;
@@ -517,15 +571,28 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
           return launch_composite(F->dev, b, w, 0, rgb + (size_t)3 * P * k0, s);
         }));
       } else {
-        HIP_TRY(timed(F, "encode", s, [&] { return launch_encode(F->dev, b, w, F->enc_blocks, 1, s); }));
-        HIP_TRY(timed(F, "mlp_fwd", s, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, s); }));
-        HIP_TRY(timed(F, "composite", s, [&] { return launch_composite(F->dev, b, w, 1, nullptr, s); }));
-        HIP_TRY(timed(F, "mlp_bwd", s, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, s); }));
-        HIP_TRY(timed(F, "reduce", s, [&] {
-          return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, s);
+        const int eb = overlap ? F->enc_blocks_overlap : F->enc_blocks;
+        HIP_TRY(timed(F, "encode", se, [&] { return launch_encode(F->dev, b, w, eb, 1, se); }));
+        if (overlap) {
+          HIP_TRY(hipEventRecord(F->ev_enc[slot], se));
+          HIP_TRY(hipStreamWaitEvent(sm, F->ev_enc[slot], 0));
+        }
+        HIP_TRY(timed(F, "mlp_fwd", sm, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, sm); }));
+        HIP_TRY(timed(F, "composite", sm, [&] { return launch_composite(F->dev, b, w, 1, nullptr, sm); }));
+        HIP_TRY(timed(F, "mlp_bwd", sm, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, sm); }));
+        HIP_TRY(timed(F, "reduce", sm, [&] {
+          return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, sm);
         }));
+        if (overlap) HIP_TRY(hipEventRecord(F->ev_mlp[slot], sm));
       }
       base += sums[c];
+    }
+    if (overlap) {
+      // the caller's stream continues once both internal streams are done
+      HIP_TRY(hipEventRecord(F->ev_end_enc, se));
+      HIP_TRY(hipEventRecord(F->ev_end_mlp, sm));
+      HIP_TRY(hipStreamWaitEvent(s, F->ev_end_enc, 0));
+      HIP_TRY(hipStreamWaitEvent(s, F->ev_end_mlp, 0));
     }
     grand += counted;
   }
@@ -586,6 +653,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   if (!(p->loss_param > 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "loss_param must be > 0");
   if (p->sh_dir_grad != 0 && p->sh_dir_grad != 1) return fail(PNERF_ERR_INVALID_ARG, "sh_dir_grad");
   if (!(p->t_stop >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "t_stop must be >= 0");
+  if (p->overlap_chunks < 0 || p->overlap_chunks > 64)
+    return fail(PNERF_ERR_INVALID_ARG, "overlap_chunks=%d outside 0..64", p->overlap_chunks);
 
   pnerf_field* F = new pnerf_field();
   auto cleanup_fail = [&](pnerf_status st) {
@@ -713,7 +782,9 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   F->n_cu = prop.multiProcessorCount;
   F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
   F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg);
-  F->enc_blocks = encode_blocks(d, F->n_cu);
+  F->enc_blocks = encode_blocks(d, F->n_cu, 8);
+  F->enc_blocks_overlap = encode_blocks(d, F->n_cu, 4);  // leave room for the networks
+  F->overlap_chunks = p->overlap_chunks == 0 ? kDefaultOverlapChunks : p->overlap_chunks;
   CF_TRY(hipStreamSynchronize(s));
 #undef CF_TRY
   *out = F;
@@ -736,7 +807,14 @@ void pnerf_destroy_field(pnerf_field* F) {
   (void)hipFree(F->d_wd2);
   (void)hipFree(F->d_occ);
   (void)hipFree(F->d_rays);
-  (void)hipFree(F->d_samp);
+  (void)hipFree(F->d_samp[0]);
+  (void)hipFree(F->d_samp[1]);
+  if (F->s_enc) (void)hipStreamDestroy(F->s_enc);
+  if (F->s_mlp) (void)hipStreamDestroy(F->s_mlp);
+  hipEvent_t evs[] = {F->ev_start, F->ev_enc[0], F->ev_enc[1], F->ev_mlp[0], F->ev_mlp[1],
+                      F->ev_end_enc, F->ev_end_mlp};
+  for (hipEvent_t e : evs)
+    if (e) (void)hipEventDestroy(e);
   (void)hipFree(F->d_totals);
   if (F->h_hyp) (void)hipHostFree(F->h_hyp);
   delete F;
@@ -810,10 +888,10 @@ pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64
                                  void* stream) {
   if (!F || !dst) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
   if (what < 0 || what > 3) return fail(PNERF_ERR_INVALID_ARG, "what=%d", what);
-  if (!F->d_samp || n < 0 || n > F->samp_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
+  if (!F->d_samp[0] || n < 0 || n > F->samp_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
   if (F->last_chunks != 1) return fail(PNERF_ERR_INVALID_ARG, "last call used %d chunks", F->last_chunks);
   DevWork w{};
-  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp);
+  carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp[0]);
   w.total = F->d_totals;  // the single chunk of the last call
   HIP_TRY(launch_inspect(F->dev, DevBatch{}, w, what, dst, n, (hipStream_t)stream));
   return PNERF_OK;

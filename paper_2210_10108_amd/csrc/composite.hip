@@ -257,9 +257,11 @@ hipError_t launch_composite(const DevField& f, const DevBatch& b, const DevWork&
   return hipGetLastError();
 }
 
+// A fixed number of parts per hypothesis, so that a hypothesis's sums do not
+// depend on how a batch is cut into chunks.
 int reduce_parts(int K) {
-  int n = (kReduceBlocks + K - 1) / K;
-  return n < 1 ? 1 : (n > kMaxReduceParts ? kMaxReduceParts : n);
+  (void)K;
+  return kReduceParts;
 }
 
 hipError_t launch_reduce(const DevField& f, const DevBatch& b, const DevWork& w, float* loss,

@@ -173,35 +173,37 @@ __device__ __forceinline__ int jac_row(const DevField& f, int l, int q, int a) {
 }
 
 // ------------------------------------------------------------------ forward
-// Level-outer: a block first blends its group's first level for all its
-// samples, then the second, so that an XCD's L2 holds one level's table at a
-// time.  GRAD: also store the Jacobian rows.
+// One thread: both levels of its group for one sample (the position is
+// computed once).  Features and Jacobian rows are streamed out with
+// non-temporal stores so that they do not displace the level tables from L2.
+// GRAD: also store the Jacobian rows.
 template <bool F16, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWork w) {
   const int S = *w.total;
   const int grp = blockIdx.x % f.n_groups;
   const int stride = gridDim.x / f.n_groups;
   const int64_t cap = w.cap;
-  for (int li = 0; li < 2; ++li) {
-    const int l = f.grp_lv[grp][li];
-    float* r0 = w.feat + (int64_t)feat_row(f, l, 0) * cap;
-    float* r1 = w.feat + (int64_t)feat_row(f, l, 1) * cap;
-    float* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
-    for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
-      const int s = sb * kBlock + threadIdx.x;
-      if (s >= S) break;
-      Pos ps = sample_pos(f, b, w, s);
+  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
+    const int s = sb * kBlock + threadIdx.x;
+    if (s >= S) break;
+    Pos ps = sample_pos(f, b, w, s);
+#pragma unroll
+    for (int li = 0; li < 2; ++li) {
+      const int l = f.grp_lv[grp][li];
+      float* r0 = w.feat + (int64_t)feat_row(f, l, 0) * cap;
+      float* r1 = w.feat + (int64_t)feat_row(f, l, 1) * cap;
+      float* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
       float jac[6];
       float2 a = level_feature<F16>(f, l, ps.x, ps.dx, GRAD ? jac : nullptr);
-      r0[s] = a.x;
-      r1[s] = a.y;
+      __builtin_nontemporal_store(a.x, r0 + s);
+      __builtin_nontemporal_store(a.y, r1 + s);
       if (GRAD) {
 #pragma unroll
         for (int q = 0; q < 2; ++q)
 #pragma unroll
           for (int c = 0; c < 3; ++c) {
             float v = (ps.clamped >> c) & 1u ? 0.0f : jac[3 * q + c] * f.inv_ext[c];
-            jr[(int64_t)(3 * q + c) * cap + s] = v;
+            __builtin_nontemporal_store(v, jr + (int64_t)(3 * q + c) * cap + s);
           }
       }
     }
@@ -259,12 +261,12 @@ __global__ __launch_bounds__(kBlock) void k_occupancy(DevField f, uint32_t* bits
 
 }  // namespace
 
-int encode_blocks(const DevField& f, int n_cu) {
-  // 8 resident blocks of 256 threads per CU, rounded to a multiple of the
+int encode_blocks(const DevField& f, int n_cu, int per_cu) {
+  // per_cu resident blocks of 256 threads per CU, rounded to a multiple of the
   // group count and of 8 (XCDs) so that each block keeps its group's XCD
   int unit = 8;
   while (unit % f.n_groups) unit += 8;
-  int want = n_cu * 8;
+  int want = n_cu * per_cu;
   return ((want + unit - 1) / unit) * unit;
 }
 

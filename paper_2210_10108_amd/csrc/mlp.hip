@@ -11,8 +11,8 @@
 // terms are about 2^-16 of the product).  The weights are split once at field
 // creation; fp16-stored weights split exactly.
 //
-// Work unit: one wavefront takes a tile of 64 consecutive compacted samples,
-// as four 16-sample column tiles.  The batch (sample) dimension is the MFMA N
+// Work unit: one wavefront takes a tile of NT * 16 consecutive compacted
+// samples, as NT 16-sample column tiles.  The batch (sample) dimension is the MFMA N
 // dimension.  A layer's accumulators hold (C layout) rows 4*(lane/16)+i of
 // column lane%16 of each 16-row tile; two such tiles are exactly one 32-deep
 // K step of the next layer's B operand (lane group g holds K positions
@@ -31,6 +31,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBlock = 256;  // 4 wavefronts
+constexpr int kFwdNT = 2;    // 16-sample column tiles per wavefront, forward
+constexpr int kBwdNT = 2;    // and backward
 
 struct Split {
   bf16x8 hi, lo;
@@ -176,12 +178,13 @@ __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float
 template <int LPG, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
   constexpr int KD = 2 * LPG;  // features per lane group
+  constexpr int NT = kFwdNT, TS = 16 * NT;
   __shared__ WeightUnit lds[kFwdUnits];
   stage(lds, f.wfwd, kFwdUnits);
   __syncthreads();
 
   const int S = *w.total;
-  const int n_tiles = (S + kTile - 1) / kTile;
+  const int n_tiles = (S + TS - 1) / TS;
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
@@ -189,12 +192,12 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
-    Split xf[4];
-    float shv[4][4];
-    int sidx[4];
+    Split xf[NT];
+    float shv[NT][4];
+    int sidx[NT];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const int s = tile * kTile + nt * 16 + col;
+    for (int nt = 0; nt < NT; ++nt) {
+      const int s = tile * TS + nt * 16 + col;
       sidx[nt] = s;
       const int sc = s < S ? s : S - 1;
       float v[8];
@@ -206,31 +209,33 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
       sh4(d, g, shv[nt]);
     }
     // density layer 1: a = relu(W_d1^T feat), 4 row tiles of 16 hidden units
-    floatx4 acc[4][4];
+    floatx4 acc[NT][4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const Split a = load_unit(lds, kFD1 + m, lane);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[nt][m] = mfma3(a, xf[nt], zero);
+      for (int nt = 0; nt < NT; ++nt) acc[nt][m] = mfma3(a, xf[nt], zero);
     }
-    uint32_t mk_a[4], mk_b1[4], mk_b2[4];
+    uint32_t mk_a[NT], mk_b1[NT], mk_b2[NT];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) mk_a[nt] = relu_mask(acc[nt]);
+    for (int nt = 0; nt < NT; ++nt) mk_a[nt] = relu_mask(acc[nt]);
     // density layer 2: h = W_d2^T a (16 outputs)
-    floatx4 h[4] = {zero, zero, zero, zero};
+    floatx4 h[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) h[nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       const Split a = load_unit(lds, kFD2 + s2, lane);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
         h[nt] = mfma3(a, pack2(acc[nt][2 * s2], acc[nt][2 * s2 + 1]), h[nt]);
     }
     // colour layer 1 on [h (h_0 has zero weights), SH_16]
-    floatx4 b1[4][4];
+    floatx4 b1[NT][4];
     {
-      Split xc[4];
+      Split xc[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
+      for (int nt = 0; nt < NT; ++nt) {
         const float v[8] = {h[nt][0], h[nt][1], h[nt][2], h[nt][3],
                             shv[nt][0], shv[nt][1], shv[nt][2], shv[nt][3]};
         xc[nt] = split8(v);
@@ -239,43 +244,45 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kFC1 + m, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) b1[nt][m] = mfma3(a, xc[nt], zero);
+        for (int nt = 0; nt < NT; ++nt) b1[nt][m] = mfma3(a, xc[nt], zero);
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) mk_b1[nt] = relu_mask(b1[nt]);
+    for (int nt = 0; nt < NT; ++nt) mk_b1[nt] = relu_mask(b1[nt]);
     // colour layer 2
-    floatx4 b2[4][4];
+    floatx4 b2[NT][4];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int m = 0; m < 4; ++m) b2[nt][m] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[4];
+      Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(b1[nt][2 * s2], b1[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(b1[nt][2 * s2], b1[nt][2 * s2 + 1]);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kFC2 + 2 * m + s2, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) b2[nt][m] = mfma3(a, x[nt], b2[nt][m]);
+        for (int nt = 0; nt < NT; ++nt) b2[nt][m] = mfma3(a, x[nt], b2[nt][m]);
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) mk_b2[nt] = relu_mask(b2[nt]);
+    for (int nt = 0; nt < NT; ++nt) mk_b2[nt] = relu_mask(b2[nt]);
     // colour layer 3 (3 outputs in rows 0..2)
-    floatx4 z[4] = {zero, zero, zero, zero};
+    floatx4 z[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) z[nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
       const Split a = load_unit(lds, kFC3 + s2, lane);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt)
+      for (int nt = 0; nt < NT; ++nt)
         z[nt] = mfma3(a, pack2(b2[nt][2 * s2], b2[nt][2 * s2 + 1]), z[nt]);
     }
     // outputs: rows 0..3 live in lane group 0
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
+    for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       if (g == 0 && s < S) {
         w.sig[s] = __expf(h[nt][0] + f.density_bias);
@@ -285,11 +292,13 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
       }
     }
     if (GRAD) {
-      uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
+      // two words per lane per 16-sample column tile
+      uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) mw[nt * 64] = mk_a[nt] | (mk_b1[nt] << 16);
-      mw[4 * 64] = mk_b2[0] | (mk_b2[1] << 16);
-      mw[5 * 64] = mk_b2[2] | (mk_b2[3] << 16);
+      for (int nt = 0; nt < NT; ++nt) {
+        mw[(2 * nt) * 64] = mk_a[nt] | (mk_b1[nt] << 16);
+        mw[(2 * nt + 1) * 64] = mk_b2[nt];
+      }
     }
   }
 }
@@ -298,6 +307,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevW
 template <int LPG>
 __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevWork w) {
   constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
+  constexpr int NT = kBwdNT, TS = 16 * NT;
   __shared__ WeightUnit lds[kBwdUnits];
   __shared__ float s_c3[64 * 3];
   stage(lds, f.wbwd, kBwdUnits);
@@ -305,7 +315,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   __syncthreads();
 
   const int S = *w.total;
-  const int n_tiles = (S + kTile - 1) / kTile;
+  const int n_tiles = (S + TS - 1) / TS;
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
@@ -313,29 +323,23 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
-    const uint32_t* mw = w.masks + (size_t)tile * kMaskWords * 64 + lane;
-    uint32_t mk_a[4], mk_b1[4], mk_b2[4];
+    const uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
+    uint32_t mk_a[NT], mk_b1[NT], mk_b2[NT];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const uint32_t v = mw[nt * 64];
+    for (int nt = 0; nt < NT; ++nt) {
+      const uint32_t v = mw[(2 * nt) * 64];
       mk_a[nt] = v & 0xFFFFu;
       mk_b1[nt] = v >> 16;
-    }
-    {
-      const uint32_t v4 = mw[4 * 64], v5 = mw[5 * 64];
-      mk_b2[0] = v4 & 0xFFFFu;
-      mk_b2[1] = v4 >> 16;
-      mk_b2[2] = v5 & 0xFFFFu;
-      mk_b2[3] = v5 >> 16;
+      mk_b2[nt] = mw[(2 * nt + 1) * 64];
     }
     // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
     // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
-    floatx4 gb2[4][4];
-    float gh0[4];
-    int sidx[4];
+    floatx4 gb2[NT][4];
+    float gh0[NT];
+    int sidx[NT];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const int s = tile * kTile + nt * 16 + col;
+    for (int nt = 0; nt < NT; ++nt) {
+      const int s = tile * TS + nt * 16 + col;
       sidx[nt] = s;
       const int sc = s < S ? s : S - 1;
       const bool ok = s < S;
@@ -351,75 +355,77 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       apply_mask(gb2[nt], mk_b2[nt]);
     }
     // colour layer 2 transposed
-    floatx4 gb1[4][4];
+    floatx4 gb1[NT][4];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int m = 0; m < 4; ++m) gb1[nt][m] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[4];
+      Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1]);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kBC2 + 2 * m + s2, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) gb1[nt][m] = mfma3(a, x[nt], gb1[nt][m]);
+        for (int nt = 0; nt < NT; ++nt) gb1[nt][m] = mfma3(a, x[nt], gb1[nt][m]);
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) apply_mask(gb1[nt], mk_b1[nt]);
+    for (int nt = 0; nt < NT; ++nt) apply_mask(gb1[nt], mk_b1[nt]);
     // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
-    floatx4 gh[4] = {zero, zero, zero, zero}, gsh[4] = {zero, zero, zero, zero};
+    floatx4 gh[NT], gsh[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) gh[nt] = gsh[nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[4];
+      Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1]);
       const Split a = load_unit(lds, kBC1 + s2, lane);
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
+      for (int nt = 0; nt < NT; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
       if (dir_grad) {
         const Split a2 = load_unit(lds, kBC1 + 2 + s2, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) gsh[nt] = mfma3(a2, x[nt], gsh[nt]);
+        for (int nt = 0; nt < NT; ++nt) gsh[nt] = mfma3(a2, x[nt], gsh[nt]);
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) gh[nt][0] += gh0[nt];  // d loss / d h_0 (zero off group 0)
+    for (int nt = 0; nt < NT; ++nt) gh[nt][0] += gh0[nt];  // d loss / d h_0 (zero off group 0)
     // density layer 2 transposed: ga = W_d2 gh (one K step, upper half zero), masked
-    floatx4 ga[4][4];
+    floatx4 ga[NT][4];
     {
-      Split x[4];
+      Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(gh[nt], zero);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gh[nt], zero);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kBD2 + m, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) ga[nt][m] = mfma3(a, x[nt], zero);
+        for (int nt = 0; nt < NT; ++nt) ga[nt][m] = mfma3(a, x[nt], zero);
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) apply_mask(ga[nt], mk_a[nt]);
+    for (int nt = 0; nt < NT; ++nt) apply_mask(ga[nt], mk_a[nt]);
     // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
     // level 4 (2 mm + i / 2) + g, so lane group g gets its own levels
-    floatx4 gf[MD][4];
+    floatx4 gf[MD][NT];
 #pragma unroll
     for (int mm = 0; mm < MD; ++mm)
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) gf[mm][nt] = zero;
+      for (int nt = 0; nt < NT; ++nt) gf[mm][nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[4];
+      Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1]);
 #pragma unroll
       for (int mm = 0; mm < MD; ++mm) {
         const Split a = load_unit(lds, kBD1 + 2 * mm + s2, lane);
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) gf[mm][nt] = mfma3(a, x[nt], gf[mm][nt]);
+        for (int nt = 0; nt < NT; ++nt) gf[mm][nt] = mfma3(a, x[nt], gf[mm][nt]);
       }
     }
     // d loss / d p = sum over the lane group's levels 4j + g of
@@ -427,7 +433,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
     const float* jrow = w.jac + (int64_t)(g * 6 * LPG) * w.cap;
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
+    for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       const int sc = s < S ? s : S - 1;
       float gx[3] = {0.f, 0.f, 0.f};

@@ -11,12 +11,13 @@ namespace pnerf {
 constexpr int kMaxLevels = 16;
 constexpr int kHidden = 64;
 constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
-constexpr int kMaskWords = 6;      // ReLU-mask words per lane per tile
+constexpr int kMaskWords = 8;      // ReLU-mask words per lane per 64 samples (2 per 16-sample column)
 constexpr int kMaxGroups = 8;      // level groups of the encoding kernels (two levels each)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
 constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
-constexpr int kReduceBlocks = 2048;   // target blocks of the per-hypothesis reduction
-constexpr int kMaxReduceParts = 64;   // parts per hypothesis (K * parts <= max(K, 2048) * 7 floats)
+constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
+constexpr int kMinOverlapSamples = 1 << 16;  // smaller batches run as one chunk
+constexpr int kReduceParts = 64;      // parts per hypothesis of the reduction (lanes of one wave)
 
 // A operand of one (row tile, K step) of v_mfma_f32_16x16x32_bf16: 8 bf16
 // values per lane, as a high part and the low part of the fp32 weight.  Lane
@@ -90,7 +91,7 @@ struct DevWork {
   int32_t* sray;                // ray of each sample
   float* sig;                   // sigma (forward) -> d loss / d h0 (after composite)
   float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
-  uint32_t* masks;              // [tiles][6][64] ReLU masks
+  uint32_t* masks;              // [column tiles of 16][2][64] ReLU masks
   float* feat;                  // [2L][cap] features; after the backward rows 0..5 = torque, force
   float* jac;                   // [6L][cap] d feature / d p of every level
   int64_t cap;                  // sample capacity (row stride of feat and jac)
@@ -127,6 +128,6 @@ hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, i
 int reduce_parts(int K);
 int mlp_fwd_blocks_per_cu(int lpg);
 int mlp_bwd_blocks_per_cu(int lpg);
-int encode_blocks(const DevField& f, int n_cu);
+int encode_blocks(const DevField& f, int n_cu, int per_cu);
 
 }  // namespace pnerf

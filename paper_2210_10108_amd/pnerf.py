@@ -41,7 +41,8 @@ class FieldParams(C.Structure):
                 ("t_stop", C.c_float), ("occ_res", C.c_int32), ("occ_bits", C.c_void_p),
                 ("occ_threshold", C.c_float), ("background", C.c_float * 3),
                 ("loss_type", C.c_int32), ("loss_param", C.c_float),
-                ("sh_dir_grad", C.c_int32), ("max_workspace_bytes", C.c_int64)]
+                ("sh_dir_grad", C.c_int32), ("max_workspace_bytes", C.c_int64),
+                ("overlap_chunks", C.c_int32)]
 
 
 _lib = None
@@ -125,7 +126,7 @@ def intrinsics(d) -> Intrinsics:
 class Field:
     """A frozen field on the current device (wraps pnerf_create_field)."""
 
-    def __init__(self, spec, stream=None, max_workspace_bytes: int = 0):
+    def __init__(self, spec, stream=None, max_workspace_bytes: int = 0, overlap_chunks: int = 0):
         self._h = C.c_void_p()
         f16 = spec.param_dtype == "f16"
         npdt = np.float16 if f16 else np.float32
@@ -158,6 +159,7 @@ class Field:
         p.background = (C.c_float * 3)(*spec.background)
         p.loss_type, p.loss_param, p.sh_dir_grad = spec.loss_type, spec.loss_param, spec.sh_dir_grad
         p.max_workspace_bytes = int(max_workspace_bytes)
+        p.overlap_chunks = int(overlap_chunks)
         self.spec = spec
         self.occ_res = spec.occ_res
         _check(lib().pnerf_create_field(C.byref(p), _stream(stream), C.byref(self._h)))

@@ -115,7 +115,7 @@ def run_loss_grad(pn, case, obs, max_ws=0, per_sample=False):
     """GPU loss and gradient; with per_sample also each sample's (torque, force)
     share and each hypothesis's sample range (from the GPU's own ray offsets)."""
     import torch
-    f = pn.Field(case.spec, max_workspace_bytes=max_ws)
+    f = pn.Field(case.spec, max_workspace_bytes=max_ws, overlap_chunks=1 if per_sample else 0)
     poses, pix = G.to_dev(case.poses), G.to_dev(case.pix)
     loss, dpose = f.render_loss_grad(poses, pix, G.to_dev(obs), case.intr)
     torch.cuda.synchronize()
@@ -242,6 +242,29 @@ def test_loss_grad_chunked_matches_single_chunk(pn):
     l1, g1, _ = run_loss_grad(pn, case, obs)
     l2, g2, _ = run_loss_grad(pn, case, obs, max_ws=1_000_000)  # forces one hypothesis per chunk
     assert np.allclose(l1, l2, rtol=1e-5) and np.allclose(g1, g2, rtol=1e-4, atol=1e-9)
+
+
+@pytest.mark.parametrize("chunks", [2, 4, 7])
+def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks):
+    # the pipelined loss gradient (encoding of one chunk alongside the networks
+    # of the previous, two streams and sample buffers) gives the same bits as
+    # one chunk on the caller's stream: per-sample work does not depend on the
+    # chunking and every hypothesis is reduced in the same fixed order
+    import torch
+    case = G.make_case("ngp800_uniform", K=16, P=1024)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    out = []
+    for oc in (1, chunks):
+        f = pn.Field(case.spec, overlap_chunks=oc)
+        loss, dpose = f.render_loss_grad(G.to_dev(case.poses), G.to_dev(case.pix), G.to_dev(obs),
+                                         case.intr)
+        torch.cuda.synchronize()
+        n = f.last_sample_count()
+        out.append((loss.cpu().numpy(), dpose.cpu().numpy(), n))
+        f.close()
+    assert out[0][2] == out[1][2] > 65536
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
 
 
 def test_loss_grad_deterministic(pn):
