@@ -123,7 +123,7 @@ typedef struct {
   int32_t sh_dir_grad;          /* 0 or 1 */
   int64_t max_workspace_bytes;  /* workspace budget; 0 = 96 GiB.  A batch whose
                                    samples need more is processed in chunks of
-                                   whole hypotheses (about 56 + 32 L bytes per
+                                   whole hypotheses (about 56 + 20 L bytes per
                                    sample). */
   int32_t overlap_chunks;       /* render_loss_grad cuts a batch of 2^16 samples or
                                    more into this many chunks of whole hypotheses

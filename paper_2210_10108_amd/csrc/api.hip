@@ -263,7 +263,7 @@ size_t carve_samples(const DevField& f, int64_t cap, DevWork* w, char* base) {
   x.cb = c.take<float>(n);
   x.masks = c.take<uint32_t>(n / kTile * kMaskWords * 64);
   x.feat = c.take<float>((size_t)std::max(2 * f.L, 6) * n);
-  x.jac = c.take<float>((size_t)6 * f.L * n);
+  x.jac = c.take<__half>((size_t)6 * f.L * n);
   x.cap = cap;
   return c.off;
 }

@@ -14,10 +14,12 @@
 //
 // Features are stored SoA, row p = (l % 4) * 2 LPG + (l / 4) * 2 + q for
 // feature q of level l (the order in which the MLP kernels feed them to MFMA),
-// row stride = the workspace sample capacity.  The Jacobian d feature / d p
-// (world units, zero along clamped components) is stored SoA too, row
-// ((l % 4) LPG + l / 4) * 6 + 3 q + a, so that lane group l % 4 of the MLP
-// backward kernel reads one contiguous block of rows.
+// row stride = the workspace sample capacity.  The Jacobian d feature /
+// d pos of every level (pos = x N_l: bounded by the table's value
+// differences, zero along clamped components) is stored SoA in fp16 (rounding
+// below 2^-11 of each entry), row ((l % 4) LPG + l / 4) * 6 + 3 q + a, so that
+// lane group l % 4 of the MLP backward kernel reads one contiguous block of
+// rows; that kernel applies N_l and 1 / extent in fp32.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -129,8 +131,8 @@ __device__ __forceinline__ float2 vertex(const DevField& f, uint32_t idx) {
 }
 
 // Feature (2 values) of level l at position x -- blend of the 8 vertices --
-// and, when jac != nullptr, its derivative with respect to x (jac[3 q + a] =
-// N d feature_q / d pos_a, pos = x N).
+// and, when jac != nullptr, its derivative with respect to the level's grid
+// coordinate (jac[3 q + a] = d feature_q / d pos_a, pos = x N).
 template <bool F16>
 __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const float x[3],
                                                 const float dx[3], float* jac) {
@@ -147,18 +149,17 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
   r.y = uz * (uy * (ux * v[0].y + wx * v[1].y) + wy * (ux * v[2].y + wx * v[3].y)) +
         wz * (uy * (ux * v[4].y + wx * v[5].y) + wy * (ux * v[6].y + wx * v[7].y));
   if (jac) {
-    const float N = (float)f.res[l];
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       float t[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) t[k] = q ? v[k].y : v[k].x;
-      jac[3 * q + 0] = N * (uy * uz * (t[1] - t[0]) + wy * uz * (t[3] - t[2]) +
-                            uy * wz * (t[5] - t[4]) + wy * wz * (t[7] - t[6]));
-      jac[3 * q + 1] = N * (ux * uz * (t[2] - t[0]) + wx * uz * (t[3] - t[1]) +
-                            ux * wz * (t[6] - t[4]) + wx * wz * (t[7] - t[5]));
-      jac[3 * q + 2] = N * (ux * uy * (t[4] - t[0]) + wx * uy * (t[5] - t[1]) +
-                            ux * wy * (t[6] - t[2]) + wx * wy * (t[7] - t[3]));
+      jac[3 * q + 0] = uy * uz * (t[1] - t[0]) + wy * uz * (t[3] - t[2]) +
+                       uy * wz * (t[5] - t[4]) + wy * wz * (t[7] - t[6]);
+      jac[3 * q + 1] = ux * uz * (t[2] - t[0]) + wx * uz * (t[3] - t[1]) +
+                       ux * wz * (t[6] - t[4]) + wx * wz * (t[7] - t[5]);
+      jac[3 * q + 2] = ux * uy * (t[4] - t[0]) + wx * uy * (t[5] - t[1]) +
+                       ux * wy * (t[6] - t[2]) + wx * wy * (t[7] - t[3]);
     }
   }
   return r;
@@ -192,7 +193,7 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
       const int l = f.grp_lv[grp][li];
       float* r0 = w.feat + (int64_t)feat_row(f, l, 0) * cap;
       float* r1 = w.feat + (int64_t)feat_row(f, l, 1) * cap;
-      float* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
+      __half* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
       float jac[6];
       float2 a = level_feature<F16>(f, l, ps.x, ps.dx, GRAD ? jac : nullptr);
       __builtin_nontemporal_store(a.x, r0 + s);
@@ -202,8 +203,10 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
         for (int q = 0; q < 2; ++q)
 #pragma unroll
           for (int c = 0; c < 3; ++c) {
-            float v = (ps.clamped >> c) & 1u ? 0.0f : jac[3 * q + c] * f.inv_ext[c];
-            __builtin_nontemporal_store(v, jr + (int64_t)(3 * q + c) * cap + s);
+            const float v = (ps.clamped >> c) & 1u ? 0.0f : jac[3 * q + c];
+            __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)),
+                                        reinterpret_cast<unsigned short*>(jr) +
+                                            (int64_t)(3 * q + c) * cap + s);
           }
       }
     }

@@ -431,20 +431,27 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     // d loss / d p = sum over the lane group's levels 4j + g of
     // d loss / d feature times the stored Jacobian, then over the 4 groups;
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
-    const float* jrow = w.jac + (int64_t)(g * 6 * LPG) * w.cap;
+    const __half* jrow = w.jac + (int64_t)(g * 6 * LPG) * w.cap;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       const int sc = s < S ? s : S - 1;
       float gx[3] = {0.f, 0.f, 0.f};
 #pragma unroll
-      for (int j = 0; j < LPG; ++j)
+      for (int j = 0; j < LPG; ++j) {
+        // level 4j + g: d loss / d pos_l = sum_q gf * J, then times N_l
+        float gl[3] = {0.f, 0.f, 0.f};
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const float gq = gf[j / 2][nt][2 * (j % 2) + q];
 #pragma unroll
-          for (int a = 0; a < 3; ++a) gx[a] += gq * jrow[(int64_t)(6 * j + 3 * q + a) * w.cap + sc];
+          for (int a = 0; a < 3; ++a)
+            gl[a] += gq * __half2float(jrow[(int64_t)(6 * j + 3 * q + a) * w.cap + sc]);
         }
+        const float N = (float)f.res[4 * j + g];
+#pragma unroll
+        for (int a = 0; a < 3; ++a) gx[a] += N * gl[a];
+      }
       float gd[3] = {0.f, 0.f, 0.f};
       float d[3];
       sample_dir(w, sc, d);
@@ -456,6 +463,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       for (int a = 0; a < 3; ++a) {
         gx[a] += __shfl_xor(gx[a], 16);
         gx[a] += __shfl_xor(gx[a], 32);
+        gx[a] *= f.inv_ext[a];  // d pos / d p = N_l / extent (N_l applied above)
         gd[a] += __shfl_xor(gd[a], 16);
         gd[a] += __shfl_xor(gd[a], 32);
       }

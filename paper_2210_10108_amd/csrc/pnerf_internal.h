@@ -93,7 +93,7 @@ struct DevWork {
   float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
   uint32_t* masks;              // [column tiles of 16][2][64] ReLU masks
   float* feat;                  // [2L][cap] features; after the backward rows 0..5 = torque, force
-  float* jac;                   // [6L][cap] d feature / d p of every level
+  __half* jac;                  // [6L][cap] d feature / d pos of every level (fp16)
   int64_t cap;                  // sample capacity (row stride of feat and jac)
 };
 
