@@ -323,6 +323,9 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
+    // the weight units are re-read from LDS every tile: hoisted out of the
+    // loop they would pin ~150 registers and cap occupancy at 1 wave/SIMD
+    asm volatile("" ::: "memory");
     const uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
     uint32_t mk_a[NT], mk_b1[NT], mk_b2[NT];
 #pragma unroll
