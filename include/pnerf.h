@@ -90,8 +90,15 @@ typedef struct {
  * colour `background`; when t_stop > 0 a ray stops after the first sample whose
  * outgoing transmittance is below t_stop.
  *
- * Loss (Sec. IV-C): loss_type 0 = Huber with threshold loss_param on each
- * channel residual, averaged over the P pixels and 3 channels of a hypothesis.
+ * Loss (Sec. IV-C, the pixel-based RGB losses): a function of each channel's
+ * residual r = C - y (rendered C, observed y), averaged over the P pixels and 3
+ * channels of a hypothesis; p = loss_param:
+ *   0 Huber        0.5 r^2 if |r| <= p, else p (|r| - p/2)
+ *   1 L1           |r|                     2 L2     r^2
+ *   3 Log L1       log(1 + |r|)            4 Relative L2  r^2 / (y^2 + p)
+ *   5 MAPE         |r| / (|y| + p)         6 sMAPE  2 |r| / (|C| + |y| + p)
+ *   7 Smooth L1    0.5 r^2 / p if |r| < p, else |r| - p/2
+ * (the derivative of |r| at r = 0 is taken as 0).
  * sh_dir_grad 0 gives the torque of Eq. 3 alone; 1 also carries the gradient
  * through the view-direction input of the colour network. */
 typedef struct {
@@ -118,8 +125,8 @@ typedef struct {
   const uint32_t* occ_bits;     /* ceil(R^3/32) words, or NULL (build on device) */
   float occ_threshold;
   float background[3];
-  int32_t loss_type;            /* 0 = Huber */
-  float loss_param;             /* Huber threshold > 0 */
+  int32_t loss_type;            /* 0..7, see above */
+  float loss_param;             /* > 0: Huber / Smooth L1 threshold, or epsilon */
   int32_t sh_dir_grad;          /* 0 or 1 */
   int64_t max_workspace_bytes;  /* workspace budget; 0 = 96 GiB.  A batch whose
                                    samples need more is processed in chunks of

@@ -72,6 +72,8 @@ def lib():
         L.orc_composite.argtypes = [i32, vp, vp, f64, vp, f64, vp, vp, vp, vp]
         L.orc_composite_grad.argtypes = [i32, vp, vp, f64, vp, f64, vp, vp, vp]
         L.orc_exp_so3.argtypes = [vp, vp]
+        L.orc_pixel_loss.restype = f64
+        L.orc_pixel_loss.argtypes = [i32, f64, f64, f64, vp, vp]
         L.orc_step_momentum.argtypes = [i32, vp, vp, vp, f32, f32]
         L.orc_resample.argtypes = [i32, vp, vp, vp, f32, f32, f32, u64, u32, vp]
         L.orc_splitmix64_next.restype = u64
@@ -272,6 +274,14 @@ def composite_grad(sigma, rgb, delta, gC, bg=(0, 0, 0), t_stop=0.0):
     gr = np.zeros((n, 3))
     lib().orc_composite_grad(n, _p(sigma), _p(rgb), delta, _p(bg), t_stop, _p(gC), _p(gs), _p(gr))
     return gs, gr
+
+
+def pixel_loss(loss_type, C, y, p):
+    """(loss, d loss / d C, kink distance) of one channel."""
+    g = np.zeros(1)
+    k = np.zeros(1)
+    v = lib().orc_pixel_loss(int(loss_type), float(C), float(y), float(p), _p(g), _p(k))
+    return v, float(g[0]), float(k[0])
 
 
 def exp_so3(w):

@@ -364,18 +364,83 @@ void orc_composite_grad(int32_t n, const double* sigma, const double* rgb, doubl
 }
 
 /* ------------------------------------------------------------------ loss */
-/* Robust per-pixel RGB loss (Sec. IV-C).  Huber with threshold delta:
- * 0.5 r^2 for |r| <= delta, else delta (|r| - delta/2). */
-static double huber(double r, double dl, double* grad, int* branch) {
-  double ar = fabs(r);
-  if (ar <= dl) {
-    *grad = r;
-    *branch = 0;
-    return 0.5 * r * r;
+/* Pixel-based RGB losses of one channel (Sec. IV-C), residual r = C - y of the
+ * rendered value C against the observed y.  p is the loss parameter: the
+ * threshold of Huber (0) and Smooth L1 (7), the epsilon of the relative losses
+ * (4, 5, 6); unused by L1 (1), L2 (2) and Log L1 (3).  Returns the loss and
+ * writes d loss / d C, a code of the branch taken (signature of the discrete
+ * decision), and the distance of r (or C) from the nearest point where the
+ * derivative jumps (INFINITY when there is none).
+ *   0 Huber       0.5 r^2 (|r| <= p), p (|r| - p / 2)
+ *   1 L1          |r|
+ *   2 L2          r^2
+ *   3 Log L1      log(1 + |r|)
+ *   4 Relative L2 r^2 / (y^2 + p)
+ *   5 MAPE        |r| / (|y| + p)
+ *   6 sMAPE       2 |r| / (|C| + |y| + p)
+ *   7 Smooth L1   0.5 r^2 / p (|r| < p), |r| - p / 2 */
+static double pixel_loss(int type, double C, double y, double p, double* grad, int* branch,
+                         double* kink) {
+  const double r = C - y, ar = fabs(r), sr = r > 0.0 ? 1.0 : (r < 0.0 ? -1.0 : 0.0);
+  *branch = r > 0.0 ? 1 : (r < 0.0 ? 2 : 0);
+  *kink = INFINITY;
+  switch (type) {
+    case 0:
+      if (ar <= p) {
+        *grad = r;
+        *branch = 0;
+        return 0.5 * r * r;
+      }
+      *grad = p * sr;
+      return p * (ar - 0.5 * p);
+    case 1:
+      *grad = sr;
+      *kink = ar;
+      return ar;
+    case 2:
+      *grad = 2.0 * r;
+      *branch = 0;
+      return r * r;
+    case 3:
+      *grad = sr / (1.0 + ar);
+      *kink = ar;
+      return log1p(ar);
+    case 4: {
+      const double den = y * y + p;
+      *grad = 2.0 * r / den;
+      *branch = 0;
+      return r * r / den;
+    }
+    case 5: {
+      const double den = fabs(y) + p;
+      *grad = sr / den;
+      *kink = ar;
+      return ar / den;
+    }
+    case 6: {
+      const double den = fabs(C) + fabs(y) + p;
+      const double sc = C > 0.0 ? 1.0 : (C < 0.0 ? -1.0 : 0.0);
+      *grad = 2.0 * sr / den - 2.0 * ar * sc / (den * den);
+      *branch = 3 * *branch + (C > 0.0 ? 1 : (C < 0.0 ? 2 : 0));
+      *kink = ar < fabs(C) ? ar : fabs(C);
+      return 2.0 * ar / den;
+    }
+    default:  /* 7 */
+      if (ar < p) {
+        *grad = r / p;
+        *branch = 0;
+        return 0.5 * r * r / p;
+      }
+      *grad = sr;
+      *kink = fabs(ar - p);
+      return ar - 0.5 * p;
   }
-  *grad = r > 0.0 ? dl : -dl;
-  *branch = r > 0.0 ? 1 : 2;
-  return dl * (ar - 0.5 * dl);
+}
+
+/* One channel's loss for testing: value, derivative and kink distance. */
+double orc_pixel_loss(int32_t type, double C, double y, double p, double* grad, double* kink) {
+  int br;
+  return pixel_loss(type, C, y, p, grad, &br, kink);
 }
 
 /* ------------------------------------------------------------- signature */
@@ -500,12 +565,11 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
   double gC[3], L = 0.0, norm = 1.0 / (3.0 * (double)P);
   double kink = INFINITY;
   for (int c = 0; c < 3; ++c) {
-    double g;
+    double g, km;
     int br;
-    L += huber(C[c] - (double)I[c], f->loss_param, &g, &br) * norm;
+    L += pixel_loss(f->loss_type, C[c], (double)I[c], f->loss_param, &g, &br, &km) * norm;
     gC[c] = g * norm;
     h = fnv(h, br);
-    double km = fabs(fabs(C[c] - (double)I[c]) - f->loss_param);
     if (km < kink) kink = km;
   }
   *loss_out = L;
@@ -616,7 +680,8 @@ int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
                   const double* sh_dirs, double* loss, double* dpose, double* rgb,
                   int32_t* ray_stop, uint64_t* signature, double* sample_out,
                   int32_t n_threads) {
-  if (f->F != 2 || f->din != f->L * f->F || f->din > CIN || f->loss_type != 0) return 1;
+  if (f->F != 2 || f->din != f->L * f->F || f->din > CIN || f->loss_type < 0 || f->loss_type > 7)
+    return 1;
   int64_t n_rays = (int64_t)K * P;
   double* rl = (double*)malloc(sizeof(double) * (size_t)(n_rays + 1));
   double* rg = (double*)malloc(sizeof(double) * 6 * (size_t)(n_rays + 1));

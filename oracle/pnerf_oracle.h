@@ -45,8 +45,9 @@ typedef struct {
   int32_t occ_res;              /* 0: no occupancy grid */
   const uint32_t* occ_bits;     /* R^3 bits, index x + R(y + Rz), LSB first */
   double bg[3];                 /* background colour */
-  int32_t loss_type;            /* 0 Huber(delta=loss_param) */
-  double loss_param;
+  int32_t loss_type;            /* 0 Huber, 1 L1, 2 L2, 3 Log L1, 4 Relative L2, 5 MAPE,
+                                   6 sMAPE, 7 Smooth L1 (see orc_pixel_loss) */
+  double loss_param;            /* Huber / Smooth L1 threshold, relative losses' epsilon */
   int32_t sh_dir_grad;          /* 1: add the view-direction path to the torque */
 } orc_field;
 
@@ -70,7 +71,7 @@ int32_t orc_march(const orc_field* f, int32_t K, const float* poses, int32_t P,
  * every discrete decision), sample_out[S][16] = per sample (sigma, rgb[3],
  * dL/dh0, dL/dz[3], dL/dp[3] -- zeros past a ray's stop -- the smallest
  * relative margin of its ReLU and stop decisions, its ray's distance from the
- * Huber kink, and its share of the torque [3]).  sh_dirs: NULL, or [K*P][3] fixed directions fed to the SH
+ * nearest jump of the loss derivative, and its share of the torque [3]).  sh_dirs: NULL, or [K*P][3] fixed directions fed to the SH
  * encoding instead of the ray direction (used to freeze that path). */
 int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
                   const int32_t* pix, const float* obs, const orc_intr* in,
@@ -92,6 +93,9 @@ void orc_composite_grad(int32_t n, const double* sigma, const double* rgb, doubl
                         const double bg[3], double t_stop, const double gC[3],
                         double* g_sigma, double* g_rgb);
 void orc_exp_so3(const double w[3], double R[9]);
+/* One channel of a pixel loss: value, d loss / d C, distance from the nearest
+ * derivative jump (INFINITY if none). */
+double orc_pixel_loss(int32_t type, double C, double y, double p, double* grad, double* kink);
 
 /* Heavy-ball momentum step on SO(3) x T(3), in place. */
 void orc_step_momentum(int32_t K, float* poses, float* momentum, const float* dpose,

@@ -649,8 +649,10 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     return fail(PNERF_ERR_INVALID_ARG, "march_mode=%d", p->march_mode);
   }
   if (p->occ_res < 0 || p->occ_res > 1024) return fail(PNERF_ERR_INVALID_ARG, "occ_res=%d", p->occ_res);
-  if (p->loss_type != 0) return fail(PNERF_ERR_NOT_SUPPORTED, "loss_type=%d (supported: 0 Huber)", p->loss_type);
-  if (!(p->loss_param > 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "loss_param must be > 0");
+  if (p->loss_type < 0 || p->loss_type > 7)
+    return fail(PNERF_ERR_INVALID_ARG, "loss_type=%d outside 0..7", p->loss_type);
+  if (!(p->loss_param > 0.0f) || !std::isfinite(p->loss_param))
+    return fail(PNERF_ERR_INVALID_ARG, "loss_param must be finite and > 0");
   if (p->sh_dir_grad != 0 && p->sh_dir_grad != 1) return fail(PNERF_ERR_INVALID_ARG, "sh_dir_grad");
   if (!(p->t_stop >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "t_stop must be >= 0");
   if (p->overlap_chunks < 0 || p->overlap_chunks > 64)

@@ -28,15 +28,55 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Huber with threshold dl; returns the loss, writes its derivative.
-__device__ __forceinline__ float huber(float r, float dl, float& grad) {
-  float ar = fabsf(r);
-  if (ar <= dl) {
-    grad = r;
-    return 0.5f * r * r;
+// Pixel-based RGB loss of one channel (Sec. IV-C): r = C - y; returns the
+// loss and writes d loss / d C.  p: threshold of Huber (0) and Smooth L1 (7),
+// epsilon of Relative L2 (4), MAPE (5) and sMAPE (6).
+//   0 Huber 0.5 r^2 (|r| <= p) or p (|r| - p/2)   1 L1 |r|        2 L2 r^2
+//   3 Log L1 log(1 + |r|)   4 Relative L2 r^2 / (y^2 + p)   5 MAPE |r| / (|y| + p)
+//   6 sMAPE 2|r| / (|C| + |y| + p)   7 Smooth L1 0.5 r^2 / p (|r| < p) or |r| - p/2
+__device__ __forceinline__ float pixel_loss(int type, float C, float y, float p, float& grad) {
+  const float r = C - y, ar = fabsf(r), sr = r > 0.0f ? 1.0f : (r < 0.0f ? -1.0f : 0.0f);
+  switch (type) {
+    case 0:
+      if (ar <= p) {
+        grad = r;
+        return 0.5f * r * r;
+      }
+      grad = p * sr;
+      return p * (ar - 0.5f * p);
+    case 1:
+      grad = sr;
+      return ar;
+    case 2:
+      grad = 2.0f * r;
+      return r * r;
+    case 3:
+      grad = sr / (1.0f + ar);
+      return log1pf(ar);
+    case 4: {
+      const float den = y * y + p;
+      grad = 2.0f * r / den;
+      return r * r / den;
+    }
+    case 5: {
+      const float den = fabsf(y) + p;
+      grad = sr / den;
+      return ar / den;
+    }
+    case 6: {
+      const float den = fabsf(C) + fabsf(y) + p;
+      const float sc = C > 0.0f ? 1.0f : (C < 0.0f ? -1.0f : 0.0f);
+      grad = 2.0f * sr / den - 2.0f * ar * sc / (den * den);
+      return 2.0f * ar / den;
+    }
+    default:
+      if (ar < p) {
+        grad = r / p;
+        return 0.5f * r * r / p;
+      }
+      grad = sr;
+      return ar - 0.5f * p;
   }
-  grad = r > 0.0f ? dl : -dl;
-  return dl * (ar - 0.5f * dl);
 }
 
 struct Chunk {
@@ -113,7 +153,7 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   float gC[3], L = 0.0f;
   for (int q = 0; q < 3; ++q) {
     float gq;
-    L += huber(C[q] - I[q], f.loss_param, gq);
+    L += pixel_loss(f.loss_type, C[q], I[q], f.loss_param, gq);
     gC[q] = gq * norm;
   }
   if (lane == 0) w.ray_loss[ray] = L * norm;

@@ -167,6 +167,19 @@ def test_loss_grad_tiny(pn, overrides):
     assert np.abs(ex["gz"][ok] - so[ok, 5:8]).max() <= 1e-3 * np.abs(so[:, 5:8]).max()
 
 
+@pytest.mark.parametrize("loss_type,param", [(1, 0.1), (2, 0.1), (3, 0.1), (4, 0.01), (5, 0.01),
+                                             (6, 0.01), (7, 0.1)])
+def test_loss_grad_pixel_losses(pn, loss_type, param):
+    # every pixel-based RGB loss of Sec. IV-C: loss, gradient and per-sample
+    # terms against the oracle
+    case = G.make_case("tiny32", loss_type=loss_type, loss_param=param)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, _ = check_full(pn, case, obs, ref)
+    assert stats["samples"] == int(ref["march"][0][-1])
+
+
 def test_loss_grad_early_stop_and_occupancy(pn):
     R = 16
     case = G.make_case("tiny32", K=3, P=200, march_mode=1, step=math.sqrt(3) / 96,

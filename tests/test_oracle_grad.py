@@ -165,3 +165,15 @@ def test_hypotheses_are_independent_and_thread_count_invariant(oracle_lib):
         assert a["loss"][k] == b["loss"][k]
         assert np.array_equal(a["dpose"][k], b["dpose"][k])
     assert a["loss"][1] != b["loss"][1]
+
+
+@pytest.mark.parametrize("loss_type,param", [(1, 0.1), (2, 0.1), (3, 0.1), (4, 0.01), (5, 0.01),
+                                             (6, 0.01), (7, 0.1)])
+def test_gradient_fd_pixel_losses(oracle_lib, loss_type, param):
+    # the pose gradient of every pixel loss of Sec. IV-C against central
+    # differences of the loss (view direction frozen, literal Eq. 3)
+    w, spec, gt, intr, pix, poses = setup_case(dict(loss_type=loss_type, loss_param=param), seed=1)
+    of = oracle_lib.OracleField(spec)
+    obs = observe(of, gt, pix, intr)
+    dirs = ray_dirs64(poses.astype(np.float64), pix, intr)
+    fd_check(of, poses, pix, obs, intr, sh_dirs=dirs)

@@ -488,3 +488,51 @@ def test_occupancy_build(oracle_lib):
     thr = float(np.median(sig))
     bits = synth.unpack_bits(of.build_occupancy(R, thr), R)
     assert np.array_equal(bits, sig > thr)
+
+
+# ------------------------------------------------------------ pixel losses
+# Loss types of the pixel-based RGB losses (paper Sec. IV-C): 0 Huber, 1 L1,
+# 2 L2, 3 Log L1, 4 Relative L2, 5 MAPE, 6 sMAPE, 7 Smooth L1.
+LOSSES = range(8)
+
+
+def test_pixel_losses_identities(oracle_lib):
+    O = oracle_lib
+    rng = np.random.default_rng(7)
+    for C, y in rng.uniform(-0.2, 1.2, size=(200, 2)):
+        r = C - y
+        eps, th = 0.01, 0.1
+        v = {t: O.pixel_loss(t, C, y, th if t in (0, 7) else eps)[0] for t in LOSSES}
+        l1, l2 = O.pixel_loss(1, C, y, 1.0)[0], O.pixel_loss(2, C, y, 1.0)[0]
+        # definitions tied to each other rather than restated
+        assert math.isclose(l1, abs(C - y), rel_tol=0, abs_tol=1e-15)
+        assert math.isclose(l2, l1 * l1, rel_tol=1e-13)
+        assert math.isclose(v[7], v[0] / th, rel_tol=1e-13)          # Smooth L1_b = Huber_b / b
+        assert math.isclose(v[3], math.log1p(l1), rel_tol=1e-13)      # log of (1 + L1)
+        assert math.isclose(v[4] * (y * y + eps), l2, rel_tol=1e-13)  # L2 relative to the target
+        assert math.isclose(v[5] * (abs(y) + eps), l1, rel_tol=1e-13) # L1 relative to the target
+        # sMAPE: symmetric in (prediction, target), bounded by 2
+        assert math.isclose(v[6], O.pixel_loss(6, y, C, eps)[0], rel_tol=1e-13)
+        assert 0.0 <= v[6] <= 2.0
+        if abs(r) <= th:   # Huber is half of L2 inside its threshold
+            assert math.isclose(v[0], 0.5 * l2, rel_tol=1e-13)
+        assert all(x >= 0.0 for x in v.values())
+    for t in LOSSES:       # no loss at a perfect match
+        assert O.pixel_loss(t, 0.37, 0.37, 0.05)[0] == 0.0
+
+
+@pytest.mark.parametrize("loss_type", LOSSES)
+def test_pixel_loss_derivative_fd(oracle_lib, loss_type):
+    O = oracle_lib
+    rng = np.random.default_rng(loss_type)
+    p = 0.1 if loss_type in (0, 7) else 0.01
+    n = 0
+    for C, y in rng.uniform(0.0, 1.0, size=(200, 2)):
+        v, g, kink = O.pixel_loss(loss_type, C, y, p)
+        if kink < 1e-3 or (loss_type in (0, 7) and abs(abs(C - y) - p) < 1e-3):
+            continue
+        h = 1e-7
+        fd = (O.pixel_loss(loss_type, C + h, y, p)[0] - O.pixel_loss(loss_type, C - h, y, p)[0]) / (2 * h)
+        assert abs(fd - g) <= 1e-6 * max(1.0, abs(g)), (C, y, fd, g)
+        n += 1
+    assert n > 150
