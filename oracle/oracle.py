@@ -75,7 +75,8 @@ def lib():
         L.orc_pixel_loss.restype = f64
         L.orc_pixel_loss.argtypes = [i32, f64, f64, f64, vp, vp]
         L.orc_step_momentum.argtypes = [i32, vp, vp, vp, f32, f32]
-        L.orc_resample.argtypes = [i32, vp, vp, vp, f32, f32, f32, u64, u32, vp]
+        L.orc_step_adam.argtypes = [i32, vp, vp, vp, i32, vp]
+        L.orc_resample.argtypes = [i32, vp, vp, i32, vp, f32, f32, f32, u64, u32, vp]
         L.orc_splitmix64_next.restype = u64
         L.orc_splitmix64_next.argtypes = [vp]
         L.orc_normals6.argtypes = [u64, u32, u32, vp]
@@ -300,15 +301,43 @@ def step_momentum(poses, momentum, dpose, lr, beta):
     return poses, momentum
 
 
-def resample(poses, momentum, loss, keep_frac, sigma_rot, sigma_trans, seed, round_idx):
+ADAM_STATE = 16  # floats per hypothesis: m[6], v[6], step count, 3 zeros
+
+
+class _Adam(C.Structure):
+    _fields_ = [("lr_rot", C.c_float), ("lr_trans", C.c_float), ("beta1", C.c_float),
+                ("beta2", C.c_float), ("eps", C.c_float), ("decay_base", C.c_float),
+                ("decay_steps", C.c_int32), ("staircase", C.c_int32),
+                ("second_moment", C.c_int32)]
+
+
+def step_adam(poses, state, dpose, step, lr_rot, lr_trans, beta1=0.9, beta2=0.999, eps=1e-8,
+              decay_base=1.0, decay_steps=0, staircase=0, second_moment=0):
+    """Adam on SO(3) x T(3) (Sec. IV-A, IV-C); returns new (poses, state)."""
     poses = np.array(poses, dtype=np.float32, copy=True)
-    momentum = np.array(momentum, dtype=np.float32, copy=True)
-    loss = np.ascontiguousarray(loss, dtype=np.float32)
+    state = np.array(state, dtype=np.float32, copy=True)
+    dpose = np.ascontiguousarray(dpose, dtype=np.float32)
     K = poses.shape[0]
+    assert state.shape == (K, ADAM_STATE) and dpose.shape == (K, 6)
+    a = _Adam(lr_rot, lr_trans, beta1, beta2, eps, decay_base, decay_steps, staircase,
+              second_moment)
+    lib().orc_step_adam(K, _p(poses), _p(state), _p(dpose), step, C.byref(a))
+    return poses, state
+
+
+def resample(poses, state, loss, keep_frac, sigma_rot, sigma_trans, seed, round_idx):
+    """Monte Carlo resampling (Sec. IV-B); state is [K][state_dim] (or None);
+    returns new (poses, state, rank)."""
+    poses = np.array(poses, dtype=np.float32, copy=True)
+    K = poses.shape[0]
+    if state is None:
+        state = np.zeros((K, 0), np.float32)
+    state = np.array(state, dtype=np.float32, copy=True).reshape(K, -1)
+    loss = np.ascontiguousarray(loss, dtype=np.float32)
     rank = np.zeros(K, np.int32)
-    lib().orc_resample(K, _p(poses), _p(momentum), _p(loss), keep_frac, sigma_rot, sigma_trans,
-                       seed, round_idx, _p(rank))
-    return poses, momentum, rank
+    lib().orc_resample(K, _p(poses), _p(state), state.shape[1], _p(loss), keep_frac, sigma_rot,
+                       sigma_trans, seed, round_idx, _p(rank))
+    return poses, state, rank
 
 
 def splitmix64_stream(seed: int, n: int):

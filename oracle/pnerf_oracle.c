@@ -780,6 +780,55 @@ void orc_step_momentum(int32_t K, float* poses, float* momentum, const float* dp
   }
 }
 
+/* Learning rate at global step `step` under the exponential decay of Sec. IV-C
+ * (base `decay_base` per `decay_steps` steps; continuous or stepwise). */
+static double decayed_lr(double lr0, const orc_adam* a, int32_t step) {
+  if (a->decay_steps <= 0) return lr0;
+  double e = (double)step / (double)a->decay_steps;
+  if (a->staircase) e = floor(e);
+  return lr0 * pow((double)a->decay_base, e);
+}
+
+/* Adam (Kingma and Ba, ICLR 2015, Algorithm 1) applied independently on the two
+ * subspaces SO(3) and T(3) (Sec. IV-A, "Momentum-Based Optimization"): the
+ * first moments are vectors (the rotational one built from the torque), and the
+ * bias-corrected step is applied as a rotation Exp(u_w) of the orientation and
+ * a shift u_t of the camera centre.  The second moment is kept per component,
+ * or (second_moment = 1) as one squared norm per subspace.  State row per
+ * hypothesis: m[6], v[6], its own step count t, three zeros. */
+void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, int32_t step,
+                   const orc_adam* a) {
+  const double b1 = (double)a->beta1, b2 = (double)a->beta2, eps = (double)a->eps;
+  const double alpha[2] = {decayed_lr((double)a->lr_rot, a, step),
+                           decayed_lr((double)a->lr_trans, a, step)};
+  for (int32_t k = 0; k < K; ++k) {
+    float* st = state + 16 * k;
+    double t = (double)st[12] + 1.0; /* t <- t + 1 */
+    double u[6];
+    for (int sub = 0; sub < 2; ++sub) {
+      const float* g = dpose + 6 * k + 3 * sub;
+      double m[3], v[3], sq = 0.0;
+      for (int i = 0; i < 3; ++i) sq += (double)g[i] * (double)g[i];
+      for (int i = 0; i < 3; ++i) {
+        m[i] = b1 * (double)st[3 * sub + i] + (1.0 - b1) * (double)g[i];
+        if (a->second_moment)
+          v[i] = b2 * (double)st[6 + 3 * sub] + (1.0 - b2) * sq;
+        else
+          v[i] = b2 * (double)st[6 + 3 * sub + i] + (1.0 - b2) * (double)g[i] * (double)g[i];
+      }
+      for (int i = 0; i < 3; ++i) {
+        double m_hat = m[i] / (1.0 - pow(b1, t));
+        double v_hat = v[i] / (1.0 - pow(b2, t));
+        u[3 * sub + i] = -alpha[sub] * m_hat / (sqrt(v_hat) + eps);
+        st[3 * sub + i] = (float)m[i];
+        st[6 + 3 * sub + i] = (float)v[i];
+      }
+    }
+    st[12] = (float)t;
+    apply_update(poses + 12 * k, u, u + 3);
+  }
+}
+
 /* ------------------------------------------------------------- resampling */
 /* SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): state += golden gamma, then
  * the output mix. */
@@ -819,10 +868,11 @@ static int loss_before(float a, int32_t ia, float b, int32_t ib) {
 
 /* Parallel Monte Carlo resampling (Sec. IV-B): rank hypotheses by loss, keep
  * the lowest-loss fraction, redraw every other one around a kept hypothesis
- * with a small random rotation and translation; redrawn momentum restarts at 0.
+ * with a small random rotation and translation; a redrawn slot's optimiser
+ * state (state_dim floats) restarts at 0.
  * The i-th redrawn slot (ascending index) takes the kept hypothesis of rank
  * i mod n_keep as its parent. */
-void orc_resample(int32_t K, float* poses, float* momentum, const float* loss,
+void orc_resample(int32_t K, float* poses, float* state, int32_t state_dim, const float* loss,
                   float keep_frac, float sigma_rot, float sigma_trans, uint64_t seed,
                   uint32_t round_idx, int32_t* rank_out) {
   int32_t n_keep = (int32_t)floor((double)K * (double)keep_frac);
@@ -851,7 +901,7 @@ void orc_resample(int32_t K, float* poses, float* momentum, const float* loss,
     }
     memcpy(poses + 12 * i, poses + 12 * parent, 12 * sizeof(float));
     apply_update(poses + 12 * i, w, v);
-    for (int q = 0; q < 6; ++q) momentum[6 * i + q] = 0.0f;
+    for (int32_t q = 0; q < state_dim; ++q) state[(size_t)state_dim * i + q] = 0.0f;
   }
   free(rank);
   free(by_rank);

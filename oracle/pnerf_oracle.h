@@ -101,8 +101,20 @@ double orc_pixel_loss(int32_t type, double C, double y, double p, double* grad, 
 void orc_step_momentum(int32_t K, float* poses, float* momentum, const float* dpose,
                        float lr, float beta);
 
-/* Keep the lowest-loss hypotheses, redraw the rest around them, in place. */
-void orc_resample(int32_t K, float* poses, float* momentum, const float* loss,
+/* Adam on SO(3) x T(3), separate moments per subspace, in place.
+ * state [K][16] = m[6], v[6], per-hypothesis step count, 3 zeros. */
+typedef struct {
+  float lr_rot, lr_trans, beta1, beta2, eps, decay_base;
+  int32_t decay_steps;   /* 0: no decay */
+  int32_t staircase;     /* 1: exponent floor(step / decay_steps) */
+  int32_t second_moment; /* 0: per component; 1: squared norm per subspace */
+} orc_adam;
+void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, int32_t step,
+                   const orc_adam* a);
+
+/* Keep the lowest-loss hypotheses, redraw the rest around them, in place;
+ * redrawn rows of the optimiser state ([K][state_dim]) restart at 0. */
+void orc_resample(int32_t K, float* poses, float* state, int32_t state_dim, const float* loss,
                   float keep_frac, float sigma_rot, float sigma_trans, uint64_t seed,
                   uint32_t round_idx, int32_t* rank_out /* [K] or NULL */);
 uint64_t orc_splitmix64_next(uint64_t* state);

@@ -427,6 +427,162 @@ def test_momentum_keeps_rotation_orthonormal(oracle_lib):
         assert np.abs(R.T @ R - np.eye(3)).max() < 1e-5
 
 
+# ------------------------------------------------------------------- Adam
+def _torch_adam_increments(grads, lr, beta1, beta2, eps, decay_base, decay_steps, staircase):
+    """Per-step updates of torch.optim.Adam (float64) on a parameter that starts
+    at 0, with torch's own schedulers for the two readings of the decay."""
+    import torch
+    theta = torch.zeros(grads.shape[1], dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([theta], lr=lr, betas=(beta1, beta2), eps=eps)
+    if decay_steps == 0:
+        sched = None
+    elif staircase:
+        sched = torch.optim.lr_scheduler.StepLR(opt, step_size=decay_steps, gamma=decay_base)
+    else:
+        sched = torch.optim.lr_scheduler.ExponentialLR(opt, gamma=decay_base ** (1.0 / decay_steps))
+    out = []
+    for g in grads:
+        before = theta.detach().clone()
+        theta.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        if sched is not None:
+            sched.step()
+        out.append((theta.detach() - before).numpy())
+    return np.array(out)
+
+
+def _adam_run(oracle_lib, pose0, grads, **kw):
+    pose, st = pose0.copy(), np.zeros((pose0.shape[0], oracle_lib.ADAM_STATE), np.float32)
+    for t, g in enumerate(grads):
+        pose, st = oracle_lib.step_adam(pose, st, g, t, **kw)
+    return pose, st
+
+
+@pytest.mark.parametrize("decay_steps,staircase", [(0, 0), (64, 0), (64, 1)])
+def test_adam_per_component_matches_torch_adam(oracle_lib, decay_steps, staircase):
+    """Sec. IV-A/IV-C Adam with per-component second moments: the translation
+    follows torch's Adam on the camera centre, and the orientation is the
+    product of the rotations given by torch's Adam steps on a rotation vector."""
+    w, _ = tiny_spec()
+    pose0 = synth.ground_truth_pose(w, 0)[None]
+    rng = np.random.default_rng(5)
+    n = 150
+    scales = np.array([1e-3, 0.3, 4.0, 2e-2, 1.0, 0.1])
+    grads = (rng.normal(size=(n, 1, 6)) * scales).astype(np.float32)
+    grads[rng.uniform(size=grads.shape) < 0.05] = 0.0
+    hp = dict(lr_rot=5e-3, lr_trans=3e-3, beta1=0.9, beta2=0.999, eps=1e-8, decay_base=0.33,
+              decay_steps=decay_steps, staircase=staircase)
+    pose, st = _adam_run(oracle_lib, pose0, grads, **hp)
+    g64 = grads[:, 0].astype(np.float64)
+    common = dict(beta1=0.9, beta2=0.999, eps=1e-8, decay_base=0.33, decay_steps=decay_steps,
+                  staircase=staircase)
+    du = _torch_adam_increments(g64[:, 3:], 3e-3, **common)
+    dw = _torch_adam_increments(g64[:, :3], 5e-3, **common)
+    tol = n * 2.0 ** -23  # float32 pose storage after each of the n steps
+    assert np.allclose(pose[0, :, 3], pose0[0, :, 3] + du.sum(0), atol=tol, rtol=0)
+    R = pose0[0, :, :3].astype(np.float64)
+    for inc in dw:
+        R = Rotation.from_rotvec(inc).as_matrix() @ R
+    assert np.allclose(pose[0, :, :3], R, atol=tol, rtol=0)
+    assert st[0, 12] == n and np.all(st[0, 13:] == 0)
+    # the moments are Adam's exponential averages of g and g^2; float storage
+    # each step bounds their relative error by 2^-24 / (1 - beta)
+    b = 0.9 ** np.arange(n)[::-1]
+    assert np.allclose(st[0, :6], 0.1 * (b[:, None] * g64).sum(0), rtol=1e-5, atol=1e-12)
+    b2 = 0.999 ** np.arange(n)[::-1]
+    assert np.allclose(st[0, 6:12], 1e-3 * (b2[:, None] * g64 ** 2).sum(0), rtol=1e-4,
+                       atol=1e-15)
+
+
+def test_adam_restarts_bias_correction_after_reset(oracle_lib):
+    """A hypothesis whose state was cleared at global step s0 (a redrawn slot)
+    continues as a fresh Adam run -- its bias correction counts its own steps --
+    while the learning rate keeps decaying with the global step."""
+    w, _ = tiny_spec()
+    pose0 = synth.ground_truth_pose(w, 0)[None]
+    rng = np.random.default_rng(6)
+    s0, n, D = 40, 30, 64
+    grads = (rng.normal(size=(s0 + n, 1, 6)) * [0.3, 1, 0.02, 1, 0.1, 2]).astype(np.float32)
+    hp = dict(lr_rot=5e-3, lr_trans=3e-3, decay_base=0.33, decay_steps=D)
+    pose, st = pose0.copy(), np.zeros((1, oracle_lib.ADAM_STATE), np.float32)
+    for t in range(s0):
+        pose, st = oracle_lib.step_adam(pose, st, grads[t], t, **hp)
+    mid = pose.copy()
+    st[:] = 0.0
+    for t in range(s0, s0 + n):
+        pose, st = oracle_lib.step_adam(pose, st, grads[t], t, **hp)
+    g64 = grads[s0:, 0].astype(np.float64)
+    f0 = 0.33 ** (s0 / D)
+    common = dict(beta1=0.9, beta2=0.999, eps=1e-8, decay_base=0.33, decay_steps=D, staircase=0)
+    du = _torch_adam_increments(g64[:, 3:], 3e-3 * f0, **common)
+    dw = _torch_adam_increments(g64[:, :3], 5e-3 * f0, **common)
+    tol = n * 2.0 ** -23
+    assert np.allclose(pose[0, :, 3], mid[0, :, 3] + du.sum(0), atol=tol, rtol=0)
+    R = mid[0, :, :3].astype(np.float64)
+    for inc in dw:
+        R = Rotation.from_rotvec(inc).as_matrix() @ R
+    assert np.allclose(pose[0, :, :3], R, atol=tol, rtol=0)
+    assert st[0, 12] == n
+
+
+@pytest.mark.parametrize("staircase", [0, 1])
+def test_adam_per_subspace_constant_gradient_closed_form(oracle_lib, staircase):
+    """A constant gradient makes the bias-corrected moments exactly g and |g|^2,
+    so every step moves lr(t) |g| / (|g| + eps) against g; the rotations share
+    one axis and compose to a single Exp."""
+    w, _ = tiny_spec()
+    pose0 = synth.ground_truth_pose(w, 1)[None]
+    g = np.array([[0.02, -0.05, 0.01, 0.3, 0.0, -0.4]], np.float32)
+    n, D, base, eps = 300, 64, 0.33, 1e-8
+    pose, _ = _adam_run(oracle_lib, pose0, [g] * n, lr_rot=5e-3, lr_trans=3e-3, decay_base=base,
+                        decay_steps=D, staircase=staircase, second_moment=1, eps=eps)
+    t = np.arange(n)
+    f = base ** (np.floor(t / D) if staircase else t / D)
+    g64 = g[0].astype(np.float64)
+    gw, gt = g64[:3], g64[3:]
+    shift = -3e-3 * f.sum() * gt / (np.linalg.norm(gt) + eps)
+    turn = -5e-3 * f.sum() * gw / (np.linalg.norm(gw) + eps)
+    # the pose is stored in float32 after each step: with a constant increment
+    # the rounding can be systematic, n half-ulps of a unit-sized value at most
+    tol = n * 2.0 ** -23
+    assert np.allclose(pose[0, :, 3], pose0[0, :, 3] + shift, atol=tol, rtol=0)
+    R = Rotation.from_rotvec(turn).as_matrix() @ pose0[0, :, :3].astype(np.float64)
+    assert np.allclose(pose[0, :, :3], R, atol=tol, rtol=0)
+
+
+def test_adam_per_subspace_is_rotation_invariant(oracle_lib):
+    """Rotating the world by Q (pose -> Q pose, torque and force -> Q g) rotates
+    the per-subspace Adam trajectory by Q; per-component second moments are tied
+    to the world axes and do not have this symmetry."""
+    w, _ = tiny_spec()
+    pose0 = synth.perturb_poses(synth.ground_truth_pose(w, 2), 3, 20, 0.1, 3)
+    rng = np.random.default_rng(11)
+    grads = rng.normal(size=(60, 3, 6)).astype(np.float64) * [0.1, 0.1, 0.1, 1, 1, 1]
+    Q = Rotation.from_rotvec([0.7, -0.4, 1.1]).as_matrix()
+    qpose0 = np.einsum("ij,kjl->kil", Q, pose0.astype(np.float64)).astype(np.float32)
+    qgrads = np.concatenate([grads[..., :3] @ Q.T, grads[..., 3:] @ Q.T], axis=-1)
+    errs = []
+    for mode in (1, 0):
+        a, _ = _adam_run(oracle_lib, pose0, grads.astype(np.float32), lr_rot=2e-2,
+                         lr_trans=2e-2, second_moment=mode)
+        b, _ = _adam_run(oracle_lib, qpose0, qgrads.astype(np.float32), lr_rot=2e-2,
+                         lr_trans=2e-2, second_moment=mode)
+        errs.append(np.abs(np.einsum("ij,kjl->kil", Q, a.astype(np.float64)) - b).max())
+    assert errs[0] < 1e-5
+    assert errs[1] > 1e-3
+
+
+def test_adam_keeps_rotation_orthonormal(oracle_lib):
+    w, _ = tiny_spec()
+    pose = synth.perturb_poses(synth.ground_truth_pose(w, 0), 4, 30, 0.2, 0)
+    rng = np.random.default_rng(12)
+    pose, _ = _adam_run(oracle_lib, pose, rng.normal(size=(1000, 4, 6)).astype(np.float32),
+                        lr_rot=5e-3, lr_trans=3e-3, decay_base=0.33, decay_steps=256)
+    for k in range(4):
+        R = pose[k, :, :3].astype(np.float64)
+        assert np.abs(R.T @ R - np.eye(3)).max() < 1e-5
+
+
 # --------------------------------------------------------------- resampling
 def test_splitmix64_published_vectors(oracle_lib):
     # reference outputs of SplitMix64 started at state 0
@@ -464,6 +620,24 @@ def test_resample_keeps_argsort_and_redraws_rest(oracle_lib):
         assert np.all(out_m[i] == 0)
     for i in kept:
         assert np.array_equal(out_p[i], poses[i]) and np.array_equal(out_m[i], mom[i])
+
+
+def test_resample_clears_adam_state_rows(oracle_lib):
+    w, _ = tiny_spec()
+    K = 16
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 0), K, 30, 0.2, 1)
+    st = np.random.default_rng(2).normal(size=(K, oracle_lib.ADAM_STATE)).astype(np.float32)
+    loss = np.random.default_rng(3).uniform(0, 1, K).astype(np.float32)
+    out_p, out_s, rank = oracle_lib.resample(poses, st, loss, 0.25, 0.05, 0.03, 5, 1)
+    for i in range(K):
+        if rank[i] < 4:
+            assert np.array_equal(out_s[i], st[i]) and np.array_equal(out_p[i], poses[i])
+        else:
+            assert np.all(out_s[i] == 0)
+    # the state width does not change which slots are kept or where they go
+    p6, _, rank6 = oracle_lib.resample(poses, st[:, :6], loss, 0.25, 0.05, 0.03, 5, 1)
+    p0, _, _ = oracle_lib.resample(poses, None, loss, 0.25, 0.05, 0.03, 5, 1)
+    assert np.array_equal(rank6, rank) and np.array_equal(p6, out_p) and np.array_equal(p0, out_p)
 
 
 # --------------------------------------------------------------- occupancy
