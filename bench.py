@@ -1,8 +1,9 @@
 """Throughput of the pose-inversion hot path on one MI355X.
 
 A step is one pass of the whole hot path over one batch: render -> Huber loss
--> pose gradient for K hypotheses (pnerf_render_loss_grad), the momentum update
-(pnerf_step_momentum) and, at the workload's resampling interval, Monte Carlo
+-> pose gradient for K hypotheses (pnerf_render_loss_grad), the pose update
+(pnerf_step_momentum, or pnerf_step_adam at the setting of Sec. IV-C with
+--optimizer adam) and, at the workload's resampling interval, Monte Carlo
 resampling (pnerf_resample_hypotheses).  Inputs (field, observation, pixel
 batches, poses) are resident in HBM before timing starts.
 
@@ -37,6 +38,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="ngp800_uniform", choices=synth.ORDER)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--optimizer", default="momentum", choices=("momentum", "adam"),
+                    help="pose update: the workload's momentum SGD, or Adam with the "
+                         "learning rates and decay of Sec. IV-C")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--overlap-chunks", type=int, default=0,
@@ -159,15 +163,21 @@ def main():
             field.render_loss_grad(poses, pix[i % n_batches], obs, intr, loss, dpose)
             if count:
                 counts.append(field.last_sample_count())
-            pnerf.step_momentum(poses, mom, dpose, w.lr, w.beta)
+            if adam is None:
+                pnerf.step_momentum(poses, mom, dpose, w.lr, w.beta)
+            else:
+                pnerf.step_adam(poses, mom, dpose, i, adam)
             if w.resample_every and (i + 1) % w.resample_every == 0:
                 pnerf.resample_hypotheses(poses, mom, loss, w.keep_frac, sr,
                                           w.resample_sigma_trans, args.seed,
                                           (i + 1) // w.resample_every)
 
+    adam = pnerf.AdamParams() if args.optimizer == "adam" else None
+    state_dim = 6 if adam is None else pnerf.ADAM_STATE
+
     def fresh():
         return (torch.from_numpy(poses0.copy()).to(dev),
-                torch.zeros(K, 6, dtype=torch.float32, device=dev))
+                torch.zeros(K, state_dim, dtype=torch.float32, device=dev))
 
     W, S = args.warmup, args.steps
     # sample counts of the timed steps (deterministic replay, synchronising per step)
@@ -261,7 +271,7 @@ def main():
         "config": {"workload": w.name, "K": K, "P": w.P, "levels": w.n_levels,
                    "table": f"2^{w.log2_table}", "image": f"{w.width}x{w.height}",
                    "sampling": "uniform" if w.march_mode == 0 else "lattice+occupancy",
-                   "parallelism": "single-gpu"},
+                   "optimizer": args.optimizer, "parallelism": "single-gpu"},
         "hypothesis_iters_per_sec": K * S / elapsed,
         "samples_per_step": samples_per_step,
         "mean_samples_per_ray": samples_per_step / w.n_rays,

@@ -8,8 +8,8 @@
  * minimise a photometric loss between the field's rendering and the observed
  * image.  This library evaluates, for K pose hypotheses at once (Sec. IV-B),
  * the loss and its gradient split into a rotation part (the torque of Eq. 3)
- * and a translation part (the force of Eq. 2), applies the momentum update on
- * SO(3) x T(3) (Sec. IV-A), and resamples hypotheses (Sec. IV-B).
+ * and a translation part (the force of Eq. 2), applies a momentum or Adam update
+ * on SO(3) x T(3) (Sec. IV-A, IV-C), and resamples hypotheses (Sec. IV-B).
  *
  * Conventions shared by every entry point
  *  - Poses are camera-to-world float32 [K][3][4] = [R | o], row major: o is the
@@ -21,12 +21,13 @@
  *  - Array arguments marked (device) are device pointers owned by the caller;
  *    they must stay valid until the work queued on `stream` has finished.
  *    Arguments marked (host) are read before the call returns.
- *  - `stream` is a hipStream_t (NULL = the default stream).  pnerf_step_momentum
- *    and pnerf_resample_hypotheses only enqueue work and return.  The calls that
- *    render (pnerf_render_loss_grad, pnerf_render, pnerf_march) synchronise the
- *    stream once per 2^21 rays: after counting every ray's samples they read the
- *    per-hypothesis sample counts back, size the workspace to them and cut the
- *    batch into chunks of whole hypotheses, then enqueue the rest and return.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  pnerf_step_momentum,
+ *    pnerf_step_adam and pnerf_resample_hypotheses only enqueue work and
+ *    return.  The calls that render (pnerf_render_loss_grad, pnerf_render,
+ *    pnerf_march) synchronise the stream once per 2^21 rays: after counting
+ *    every ray's samples they read the per-hypothesis sample counts back, size
+ *    the workspace to them and cut the batch into chunks of whole hypotheses,
+ *    then enqueue the rest and return.
  *    pnerf_create_field and pnerf_field_occupancy synchronise the stream.
  *  - Arguments are validated on the host before anything is enqueued; a
  *    failed validation returns PNERF_ERR_INVALID_ARG (or NOT_SUPPORTED) and
@@ -176,17 +177,55 @@ pnerf_status pnerf_render_loss_grad(pnerf_field* field, int32_t K, const float* 
 pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum,
                                  const float* dpose, float lr, float beta, void* stream);
 
+/* Adam on SO(3) x T(3) (Sec. IV-A, "Momentum-Based Optimization": Adam's first
+ * and second moments kept separately for the rotation and the translation, the
+ * rotational moments as vectors, the orientation updated by the rotation they
+ * induce; Kingma and Ba's Algorithm 1 within each subspace).  For each k, with
+ * g = dpose[k] and n the hypothesis's own step count (state[k][12] + 1):
+ *   m <- beta1 m + (1 - beta1) g
+ *   v <- beta2 v + (1 - beta2) g^2        (second_moment = 0: per component)
+ *   v_s <- beta2 v_s + (1 - beta2) |g_s|^2 (second_moment = 1: one value per
+ *                                          subspace s, stored in its 3 slots)
+ *   u = -lr_s(step) (m / (1 - beta1^n)) / (sqrt(v / (1 - beta2^n)) + eps)
+ *   R <- Exp(u_w) R,  o <- o + u_t
+ * with the learning rates of Sec. IV-C decaying exponentially in the global
+ * step index `step` (0 for the first step of a run):
+ *   lr_s(step) = lr_s * decay_base^(step / decay_steps)       (staircase = 0)
+ *   lr_s(step) = lr_s * decay_base^floor(step / decay_steps)  (staircase = 1)
+ * and no decay when decay_steps = 0.  The paper's setting is lr_rot 5e-3,
+ * lr_trans 3e-3, decay_base 0.33, decay_steps 256.
+ * state (device) float32 [K][PNERF_ADAM_STATE] = (m_w[3], m_t[3], v_w[3],
+ * v_t[3], n, 0, 0, 0): all zero before a hypothesis's first step (also what
+ * pnerf_resample_hypotheses leaves in a redrawn slot given state_dim =
+ * PNERF_ADAM_STATE); n is exact up to 2^24 steps.  poses (device) [K][3][4],
+ * dpose (device) [K][6], params (host).  Requires K >= 1, step >= 0, finite
+ * lr >= 0, 0 <= beta < 1, eps > 0, decay_base > 0, decay_steps >= 0. */
+#define PNERF_ADAM_STATE 16
+typedef struct {
+  float lr_rot, lr_trans;  /* learning rates at step 0 */
+  float beta1, beta2, eps; /* Adam's moment decays and epsilon (0.9, 0.999, 1e-8) */
+  float decay_base;        /* learning-rate factor per decay_steps steps */
+  int32_t decay_steps;     /* 0: constant learning rates */
+  int32_t staircase;       /* 0: continuous decay; 1: stepwise */
+  int32_t second_moment;   /* 0: per component; 1: per subspace (rotation invariant) */
+} pnerf_adam_params;
+
+pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float* dpose,
+                             int32_t step, const pnerf_adam_params* params, void* stream);
+
 /* Monte Carlo resampling (Sec. IV-B): rank hypotheses by loss (ascending, ties
  * by index, NaN last), keep n_keep = max(1, floor(K keep_frac)), and redraw
  * each other slot -- the i-th one in ascending slot order takes the kept
  * hypothesis of rank i mod n_keep as parent -- as R = Exp(w) R_parent,
  * o = o_parent + v with w ~ N(0, sigma_rot^2 I), v ~ N(0, sigma_trans^2 I);
- * redrawn momenta restart at 0.  The normals of slot s come from the SplitMix64
- * stream started at seed ^ mix(round << 32 | s) (mix = SplitMix64's output
- * function), uniforms ((u >> 11) + 1/2) 2^-53, Box-Muller on pairs, in the
- * order w_x, w_y, w_z, v_x, v_y, v_z.  In place; 1 <= K <= 65535. */
-pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
-                                       const float* loss, float keep_frac,
+ * a redrawn slot's optimiser state (its row of opt_state, state_dim floats:
+ * 6 for momentum, PNERF_ADAM_STATE for Adam) restarts at 0.  The normals of
+ * slot s come from the SplitMix64 stream started at seed ^ mix(round << 32 | s)
+ * (mix = SplitMix64's output function), uniforms ((u >> 11) + 1/2) 2^-53,
+ * Box-Muller on pairs, in the order w_x, w_y, w_z, v_x, v_y, v_z.  In place;
+ * 1 <= K <= 65535, 0 <= state_dim <= 64 (opt_state may be NULL when 0). */
+pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* opt_state,
+                                       int32_t state_dim, const float* loss, float keep_frac,
                                        float sigma_rot, float sigma_trans, uint64_t seed,
                                        uint32_t round_idx, void* stream);
 

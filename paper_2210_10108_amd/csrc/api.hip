@@ -865,12 +865,44 @@ pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum, const
   return PNERF_OK;
 }
 
-pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
-                                       const float* loss, float keep_frac, float sigma_rot,
-                                       float sigma_trans, uint64_t seed, uint32_t round_idx,
-                                       void* stream) {
+pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float* dpose,
+                             int32_t step, const pnerf_adam_params* p, void* stream) {
+  static_assert(PNERF_ADAM_STATE == kAdamState, "Adam state width");
+  if (K < 1) return fail(PNERF_ERR_INVALID_ARG, "K=%d", K);
+  if (!p) return fail(PNERF_ERR_INVALID_ARG, "NULL params");
+  if (step < 0) return fail(PNERF_ERR_INVALID_ARG, "step=%d", step);
+  if (!(std::isfinite(p->lr_rot) && p->lr_rot >= 0.0f && std::isfinite(p->lr_trans) &&
+        p->lr_trans >= 0.0f))
+    return fail(PNERF_ERR_INVALID_ARG, "learning rates must be finite and >= 0");
+  if (!(p->beta1 >= 0.0f && p->beta1 < 1.0f && p->beta2 >= 0.0f && p->beta2 < 1.0f))
+    return fail(PNERF_ERR_INVALID_ARG, "beta1/beta2 outside [0, 1)");
+  if (!(std::isfinite(p->eps) && p->eps > 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "eps");
+  if (!(std::isfinite(p->decay_base) && p->decay_base > 0.0f) || p->decay_steps < 0)
+    return fail(PNERF_ERR_INVALID_ARG, "decay_base/decay_steps");
+  if ((p->staircase != 0 && p->staircase != 1) || (p->second_moment != 0 && p->second_moment != 1))
+    return fail(PNERF_ERR_INVALID_ARG, "staircase/second_moment must be 0 or 1");
+  if (!poses || !state || !dpose) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  // Learning-rate decay of Sec. IV-C, evaluated once per call in double.
+  double scale = 1.0;
+  if (p->decay_steps > 0) {
+    double e = p->staircase ? std::floor((double)step / (double)p->decay_steps)
+                            : (double)step / (double)p->decay_steps;
+    scale = std::pow((double)p->decay_base, e);
+  }
+  HIP_TRY(launch_step_adam(K, poses, state, dpose, (double)p->lr_rot * scale,
+                           (double)p->lr_trans * scale, p->beta1, p->beta2, p->eps,
+                           p->second_moment, (hipStream_t)stream));
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* opt_state,
+                                       int32_t state_dim, const float* loss, float keep_frac,
+                                       float sigma_rot, float sigma_trans, uint64_t seed,
+                                       uint32_t round_idx, void* stream) {
   if (K < 1 || K > 65535) return fail(PNERF_ERR_INVALID_ARG, "K=%d outside 1..65535", K);
-  if (!poses || !momentum || !loss) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (state_dim < 0 || state_dim > 64) return fail(PNERF_ERR_INVALID_ARG, "state_dim=%d", state_dim);
+  if (!poses || !loss || (state_dim > 0 && !opt_state))
+    return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
   if (!(keep_frac >= 0.0f && keep_frac <= 1.0f)) return fail(PNERF_ERR_INVALID_ARG, "keep_frac");
   if (!(sigma_rot >= 0.0f) || !(sigma_trans >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "sigma");
   int n_keep = (int)std::floor((double)K * (double)keep_frac);
@@ -878,8 +910,8 @@ pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* momentum,
   hipStream_t s = (hipStream_t)stream;
   int32_t* scratch = nullptr;
   HIP_TRY(hipMallocAsync((void**)&scratch, sizeof(int32_t) * 2 * (size_t)K, s));
-  hipError_t e = launch_resample(K, poses, momentum, loss, n_keep, sigma_rot, sigma_trans, seed,
-                                 round_idx, scratch, s);
+  hipError_t e = launch_resample(K, poses, opt_state, state_dim, loss, n_keep, sigma_rot,
+                                 sigma_trans, seed, round_idx, scratch, s);
   hipError_t e2 = hipFreeAsync(scratch, s);
   if (e != hipSuccess) return fail(PNERF_ERR_DEVICE, "resample launch: %s", hipGetErrorString(e));
   HIP_TRY(e2);

@@ -18,6 +18,7 @@ constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays pe
 constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
 constexpr int kMinOverlapSamples = 1 << 16;  // smaller batches run as one chunk
 constexpr int kReduceParts = 64;      // parts per hypothesis of the reduction (lanes of one wave)
+constexpr int kAdamState = 16;        // Adam state floats per hypothesis: m[6], v[6], n, 3 pads
 
 // A operand of one (row tile, K step) of v_mfma_f32_16x16x32_bf16: 8 bf16
 // values per lane, as a high part and the low part of the fp32 weight.  Lane
@@ -121,9 +122,12 @@ hipError_t launch_inspect(const DevField& f, const DevBatch& b, const DevWork& w
 hipError_t launch_offsets_i64(const int32_t* off, int64_t* out, int n, int64_t base, hipStream_t s);
 hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dpose, float lr,
                                 float beta, hipStream_t s);
-hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, int n_keep,
-                           float sr, float st, uint64_t seed, uint32_t round, int32_t* scratch,
-                           hipStream_t s);
+hipError_t launch_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
+                            double lr_t, double b1, double b2, double eps, int per_subspace,
+                            hipStream_t s);
+hipError_t launch_resample(int K, float* poses, float* state, int state_dim, const float* loss,
+                           int n_keep, float sr, float st, uint64_t seed, uint32_t round,
+                           int32_t* scratch, hipStream_t s);
 
 int reduce_parts(int K);
 int mlp_fwd_blocks_per_cu(int lpg);

@@ -1,6 +1,7 @@
-// Pose update on SO(3) x T(3) with heavy-ball momentum, and Monte Carlo
-// hypothesis resampling.  Both are tiny (one thread per hypothesis) and run in
-// double precision; results are stored as float.
+// Pose updates on SO(3) x T(3) (heavy-ball momentum; Adam with separate moments
+// per subspace) and Monte Carlo hypothesis resampling.  All are tiny (one
+// thread per hypothesis) and run in double precision; results are stored as
+// float.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -58,6 +59,41 @@ __global__ void k_step_momentum(int K, float* poses, float* mom, const float* dp
   for (int q = 0; q < 12; ++q) poses[12 * k + q] = pose[q];
 }
 
+// Adam (Kingma and Ba, Algorithm 1) run separately on the rotation and the
+// translation subspace.  State row: m[6], v[6], step count, 3 zero pads.
+__global__ void k_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
+                            double lr_t, double b1, double b2, double eps, int per_subspace) {
+  int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= K) return;
+  float* st = state + (size_t)kAdamState * k;
+  double n = (double)st[12] + 1.0;
+  double c1 = 1.0 - pow(b1, n), c2 = 1.0 - pow(b2, n);
+  double u[6];
+  for (int sub = 0; sub < 2; ++sub) {
+    double g[3], m[3], v[3];
+    for (int a = 0; a < 3; ++a) g[a] = (double)dpose[6 * k + 3 * sub + a];
+    for (int a = 0; a < 3; ++a) m[a] = b1 * (double)st[3 * sub + a] + (1.0 - b1) * g[a];
+    if (per_subspace) {
+      double gg = g[0] * g[0] + g[1] * g[1] + g[2] * g[2];
+      double vs = b2 * (double)st[6 + 3 * sub] + (1.0 - b2) * gg;
+      v[0] = v[1] = v[2] = vs;
+    } else {
+      for (int a = 0; a < 3; ++a) v[a] = b2 * (double)st[6 + 3 * sub + a] + (1.0 - b2) * g[a] * g[a];
+    }
+    double lr = sub == 0 ? lr_r : lr_t;
+    for (int a = 0; a < 3; ++a) {
+      u[3 * sub + a] = -lr * (m[a] / c1) / (sqrt(v[a] / c2) + eps);
+      st[3 * sub + a] = (float)m[a];
+      st[6 + 3 * sub + a] = (float)v[a];
+    }
+  }
+  st[12] = (float)n;
+  float pose[12];
+  for (int q = 0; q < 12; ++q) pose[q] = poses[12 * k + q];
+  apply(pose, u, u + 3);
+  for (int q = 0; q < 12; ++q) poses[12 * k + q] = pose[q];
+}
+
 // ---------------------------------------------------------------- resample
 // SplitMix64 output function and stream step (Steele, Lea, Flood 2014).
 __device__ inline uint64_t mix64(uint64_t z) {
@@ -99,8 +135,8 @@ __global__ __launch_bounds__(kRankBlock) void k_rank(int K, const float* loss, i
 
 // Each discarded slot counts the discarded slots before it, picks its parent
 // by rank, and redraws itself around the parent.
-__global__ __launch_bounds__(kRankBlock) void k_redraw(int K, float* poses, float* mom,
-                                                       const int32_t* rank,
+__global__ __launch_bounds__(kRankBlock) void k_redraw(int K, float* poses, float* opt,
+                                                       int state_dim, const int32_t* rank,
                                                        const int32_t* by_rank, int n_keep,
                                                        float sr, float st, uint64_t seed,
                                                        uint32_t round) {
@@ -138,7 +174,7 @@ __global__ __launch_bounds__(kRankBlock) void k_redraw(int K, float* poses, floa
   for (int q = 0; q < 12; ++q) pose[q] = poses[12 * parent + q];
   apply(pose, w, v);
   for (int q = 0; q < 12; ++q) poses[12 * i + q] = pose[q];
-  for (int q = 0; q < 6; ++q) mom[6 * i + q] = 0.0f;
+  for (int q = 0; q < state_dim; ++q) opt[(size_t)state_dim * i + q] = 0.0f;
 }
 
 }  // namespace
@@ -150,15 +186,23 @@ hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dp
   return hipGetLastError();
 }
 
-hipError_t launch_resample(int K, float* poses, float* mom, const float* loss, int n_keep,
-                           float sr, float st, uint64_t seed, uint32_t round, int32_t* scratch,
-                           hipStream_t s) {
+hipError_t launch_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
+                            double lr_t, double b1, double b2, double eps, int per_subspace,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(k_step_adam, dim3((K + 63) / 64), dim3(64), 0, s, K, poses, state, dpose,
+                     lr_r, lr_t, b1, b2, eps, per_subspace);
+  return hipGetLastError();
+}
+
+hipError_t launch_resample(int K, float* poses, float* state, int state_dim, const float* loss,
+                           int n_keep, float sr, float st, uint64_t seed, uint32_t round,
+                           int32_t* scratch, hipStream_t s) {
   int nb = (K + kRankBlock - 1) / kRankBlock;
   int32_t* rank = scratch;
   int32_t* by_rank = scratch + K;
   hipLaunchKernelGGL(k_rank, dim3(nb), dim3(kRankBlock), 0, s, K, loss, rank, by_rank);
-  hipLaunchKernelGGL(k_redraw, dim3(nb), dim3(kRankBlock), 0, s, K, poses, mom, rank, by_rank,
-                     n_keep, sr, st, seed, round);
+  hipLaunchKernelGGL(k_redraw, dim3(nb), dim3(kRankBlock), 0, s, K, poses, state, state_dim,
+                     rank, by_rank, n_keep, sr, st, seed, round);
   return hipGetLastError();
 }
 

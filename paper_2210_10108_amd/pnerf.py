@@ -56,9 +56,11 @@ _SIGS = {
                                          C.c_void_p]),
     "pnerf_step_momentum": (C.c_int, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_float,
                                       C.c_float, C.c_void_p]),
-    "pnerf_resample_hypotheses": (C.c_int, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
-                                            C.c_float, C.c_float, C.c_float, C.c_uint64,
-                                            C.c_uint32, C.c_void_p]),
+    "pnerf_step_adam": (C.c_int, [C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                  C.c_void_p, C.c_void_p]),
+    "pnerf_resample_hypotheses": (C.c_int, [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
+                                            C.c_void_p, C.c_float, C.c_float, C.c_float,
+                                            C.c_uint64, C.c_uint32, C.c_void_p]),
     "pnerf_render": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_void_p]),
     "pnerf_march": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p,
@@ -271,12 +273,40 @@ def step_momentum(poses, momentum, dpose, lr: float, beta: float, stream=None):
         _dev(dpose, torch.float32, (K, 6), "dpose"), lr, beta, _stream(stream)))
 
 
-def resample_hypotheses(poses, momentum, loss, keep_frac: float, sigma_rot: float,
-                        sigma_trans: float, seed: int, round_idx: int, stream=None):
+ADAM_STATE = 16  # floats of Adam state per hypothesis (PNERF_ADAM_STATE)
+
+
+class AdamParams(C.Structure):
+    """pnerf_adam_params; the defaults are the setting of Sec. IV-C."""
+    _fields_ = [("lr_rot", C.c_float), ("lr_trans", C.c_float), ("beta1", C.c_float),
+                ("beta2", C.c_float), ("eps", C.c_float), ("decay_base", C.c_float),
+                ("decay_steps", C.c_int32), ("staircase", C.c_int32),
+                ("second_moment", C.c_int32)]
+
+    def __init__(self, lr_rot=5e-3, lr_trans=3e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                 decay_base=0.33, decay_steps=256, staircase=0, second_moment=0):
+        super().__init__(lr_rot, lr_trans, beta1, beta2, eps, decay_base, decay_steps,
+                         staircase, second_moment)
+
+
+def step_adam(poses, state, dpose, step: int, params: AdamParams, stream=None):
     import torch
     K = poses.shape[0]
+    _check(lib().pnerf_step_adam(
+        K, _dev(poses, torch.float32, (K, 3, 4), "poses"),
+        _dev(state, torch.float32, (K, ADAM_STATE), "state"),
+        _dev(dpose, torch.float32, (K, 6), "dpose"), step, C.byref(params), _stream(stream)))
+
+
+def resample_hypotheses(poses, state, loss, keep_frac: float, sigma_rot: float,
+                        sigma_trans: float, seed: int, round_idx: int, stream=None):
+    """state: the optimiser state [K][D] (momentum D = 6, Adam D = ADAM_STATE)
+    or None; redrawn rows restart at 0."""
+    import torch
+    K = poses.shape[0]
+    dim = 0 if state is None else int(state.shape[1])
     _check(lib().pnerf_resample_hypotheses(
         K, _dev(poses, torch.float32, (K, 3, 4), "poses"),
-        _dev(momentum, torch.float32, (K, 6), "momentum"),
+        None if state is None else _dev(state, torch.float32, (K, dim), "state"), dim,
         _dev(loss, torch.float32, (K,), "loss"), keep_frac, sigma_rot, sigma_trans,
         seed & 0xFFFFFFFFFFFFFFFF, round_idx, _stream(stream)))

@@ -50,6 +50,10 @@ def test_struct_layouts_match_header(pn, tmp_path):
 int main(void) {{
   printf("size %zu\\n", sizeof(pnerf_field_params));
   printf("isize %zu\\n", sizeof(pnerf_intrinsics));
+  printf("asize %zu\\n", sizeof(pnerf_adam_params));
+  printf("astate %d\\n", PNERF_ADAM_STATE);
+  printf("a.decay_base %zu\\n", offsetof(pnerf_adam_params, decay_base));
+  printf("a.second_moment %zu\\n", offsetof(pnerf_adam_params, second_moment));
   O(n_levels); O(level_res); O(table); O(w_color3); O(density_bias); O(aabb_max);
   O(march_mode); O(step); O(t_stop); O(occ_bits); O(occ_threshold); O(background);
   O(loss_type); O(loss_param); O(sh_dir_grad); O(max_workspace_bytes); O(overlap_chunks);
@@ -61,8 +65,13 @@ int main(void) {{
                                                  check=True).stdout.splitlines())
     assert int(got["size"]) == C.sizeof(pn.FieldParams)
     assert int(got["isize"]) == C.sizeof(pn.Intrinsics)
+    assert int(got["asize"]) == C.sizeof(pn.AdamParams)
+    assert int(got["astate"]) == pn.ADAM_STATE
     for k, v in got.items():
-        if k in ("size", "isize"):
+        if k in ("size", "isize", "asize", "astate"):
+            continue
+        if k.startswith("a."):
+            assert getattr(pn.AdamParams, k[2:]).offset == int(v), k
             continue
         assert getattr(pn.FieldParams, k).offset == int(v), k
 
@@ -71,8 +80,30 @@ def test_host_validation_rejects_bad_arguments(pn):
     L = pn.lib()
     assert L.pnerf_step_momentum(0, None, None, None, 0.1, 0.9, None) == pn.ERR_INVALID_ARG
     assert b"K=0" in L.pnerf_last_error()
-    assert L.pnerf_resample_hypotheses(70000, None, None, None, 0.5, 0.1, 0.1, 1, 0,
+    assert L.pnerf_resample_hypotheses(70000, None, None, 6, None, 0.5, 0.1, 0.1, 1, 0,
                                        None) == pn.ERR_INVALID_ARG
+    # scalar arguments are checked before pointers, so NULL pointers isolate them
+    assert L.pnerf_resample_hypotheses(4, None, None, 65, None, 0.5, 0.1, 0.1, 1, 0,
+                                       None) == pn.ERR_INVALID_ARG
+    assert b"state_dim" in L.pnerf_last_error()
+    assert L.pnerf_resample_hypotheses(4, None, None, 6, None, 0.5, 0.1, 0.1, 1, 0,
+                                       None) == pn.ERR_INVALID_ARG
+    assert b"NULL" in L.pnerf_last_error()
+    assert L.pnerf_step_adam(4, None, None, None, -1, C.byref(pn.AdamParams()),
+                             None) == pn.ERR_INVALID_ARG
+    assert b"step" in L.pnerf_last_error()
+    for field, bad in [("beta1", 1.0), ("beta2", -0.1), ("eps", 0.0), ("lr_rot", -1e-3),
+                       ("lr_trans", float("nan")), ("decay_base", 0.0), ("decay_steps", -1),
+                       ("staircase", 2), ("second_moment", 3)]:
+        p = pn.AdamParams()
+        setattr(p, field, bad)
+        assert L.pnerf_step_adam(4, None, None, None, 0, C.byref(p), None) == \
+            pn.ERR_INVALID_ARG, field
+        assert b"NULL" not in L.pnerf_last_error(), field
+    assert L.pnerf_step_adam(4, None, None, None, 0, C.byref(pn.AdamParams()),
+                             None) == pn.ERR_INVALID_ARG
+    assert b"NULL pointer" in L.pnerf_last_error()
+    assert L.pnerf_step_adam(4, None, None, None, 0, None, None) == pn.ERR_INVALID_ARG
     assert L.pnerf_render_loss_grad(None, 4, None, 8, None, None, None, None, None,
                                     None) == pn.ERR_INVALID_ARG
     assert L.pnerf_create_field(None, None, None) == pn.ERR_INVALID_ARG

@@ -1,0 +1,243 @@
+"""Parity of the pose optimisers and of whole optimisation runs with the CPU
+oracle: the Adam step on SO(3) x T(3) (Sec. IV-A, IV-C), resampling with Adam
+state (Sec. IV-B), and short runs of render -> loss -> gradient -> update ->
+resample on both sides from the same seeded start."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2210_10108_amd import synth
+from tests import gpu_common as G
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def announce(request):
+    sys.stderr.write(f"\n[gpu] {request.node.nodeid}\n")
+    sys.stderr.flush()
+    yield
+
+
+@pytest.fixture(scope="module")
+def pn():
+    from paper_2210_10108_amd import pnerf
+    pnerf.lib()
+    return pnerf
+
+
+def adam_state(rng, K, per_subspace):
+    """A valid mid-run Adam state: some rows fresh, the others with moments
+    and a step count."""
+    st = np.zeros((K, O.ADAM_STATE), np.float32)
+    n = rng.integers(0, 40, K)
+    for k in range(K):
+        if n[k] == 0:
+            continue
+        st[k, :6] = rng.normal(size=6) * 0.1
+        v = rng.uniform(1e-4, 1.0, 6)
+        if per_subspace:
+            v[:3], v[3:] = v[0], v[3]
+        st[k, 6:12] = v
+        st[k, 12] = n[k]
+    return st
+
+
+@pytest.mark.parametrize("second_moment,staircase", [(0, 0), (1, 0), (0, 1), (1, 1)])
+def test_step_adam_matches_oracle(pn, second_moment, staircase):
+    import torch
+    rng = np.random.default_rng(10 + 2 * second_moment + staircase)
+    K, n_steps, step0 = 37, 120, 200           # crosses the decay boundary at 256
+    w = synth.WORKLOADS["tiny32"]
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 0), K, 40, 0.3, 0)
+    st = adam_state(rng, K, second_moment)
+    grads = (rng.normal(size=(n_steps, K, 6)) * rng.uniform(0.01, 3, (1, K, 6))).astype(np.float32)
+    grads[:, 5] = 0.0                          # a fresh hypothesis with no gradient at all
+    st[5] = 0.0
+    hp = dict(lr_rot=5e-3, lr_trans=3e-3, beta1=0.9, beta2=0.999, eps=1e-8, decay_base=0.33,
+              decay_steps=256, staircase=staircase, second_moment=second_moment)
+    prm = pn.AdamParams(**hp)
+    p_ref, s_ref = poses, st
+    p_d, s_d, g_d = G.to_dev(poses), G.to_dev(st), G.to_dev(grads)
+    for i in range(n_steps):
+        p_ref, s_ref = O.step_adam(p_ref, s_ref, grads[i], step0 + i, **hp)
+        pn.step_adam(p_d, s_d, g_d[i], step0 + i, prm)
+    torch.cuda.synchronize()
+    p_g, s_g = p_d.cpu().numpy(), s_d.cpu().numpy()
+    # both sides run in double and store float32: rounding-order differences
+    # reach the last float bit now and then, n_steps ulps at most
+    assert np.allclose(p_g, p_ref, atol=n_steps * 2.0 ** -23, rtol=0)
+    assert np.allclose(s_g, s_ref, rtol=1e-5, atol=1e-12)
+    assert np.array_equal(s_g[:, 12], s_ref[:, 12])
+    assert np.array_equal(p_g[5], poses[5])    # zero gradient, fresh state: no motion
+
+
+def test_step_adam_paper_setting_single_step(pn):
+    """One step at the paper's setting from a fresh state moves every component
+    by its learning rate against the sign of its gradient."""
+    import torch
+    K = 64
+    w = synth.WORKLOADS["tiny32"]
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 1), K, 20, 0.1, 1)
+    g = np.random.default_rng(3).normal(size=(K, 6)).astype(np.float32)
+    p_d = G.to_dev(poses)
+    s_d = G.to_dev(np.zeros((K, O.ADAM_STATE), np.float32))
+    pn.step_adam(p_d, s_d, G.to_dev(g), 0, pn.AdamParams())
+    torch.cuda.synchronize()
+    p_ref, _ = O.step_adam(poses, np.zeros((K, O.ADAM_STATE), np.float32), g, 0, 5e-3, 3e-3,
+                           decay_base=0.33, decay_steps=256)
+    assert np.allclose(p_d.cpu().numpy(), p_ref, atol=2.0 ** -22, rtol=0)
+    assert np.allclose(p_d.cpu().numpy()[:, :, 3] - poses[:, :, 3], -3e-3 * np.sign(g[:, 3:]),
+                       atol=1e-6)
+
+
+@pytest.mark.parametrize("K,keep", [(64, 0.25), (300, 0.1)])
+def test_resample_with_adam_state_matches_oracle(pn, K, keep):
+    import torch
+    w = synth.WORKLOADS["tiny32"]
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 0), K, 40, 0.3, 2)
+    rng = np.random.default_rng(K)
+    st = adam_state(rng, K, 0)
+    loss = rng.uniform(0, 1, K).astype(np.float32)
+    sr, stt = math.radians(3), 0.02
+    p_ref, s_ref, _ = O.resample(poses, st, loss, keep, sr, stt, 99, 2)
+    p_d, s_d = G.to_dev(poses), G.to_dev(st)
+    pn.resample_hypotheses(p_d, s_d, G.to_dev(loss), keep, sr, stt, 99, 2)
+    torch.cuda.synchronize()
+    assert np.allclose(p_d.cpu().numpy(), p_ref, atol=1e-6, rtol=0)
+    assert np.array_equal(s_d.cpu().numpy(), s_ref)
+
+
+def test_resample_without_state_matches_oracle(pn):
+    import torch
+    K = 50
+    w = synth.WORKLOADS["tiny32"]
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 0), K, 40, 0.3, 4)
+    loss = np.random.default_rng(4).uniform(0, 1, K).astype(np.float32)
+    p_ref, _, _ = O.resample(poses, None, loss, 0.2, 0.05, 0.02, 5, 1)
+    p_d = G.to_dev(poses)
+    pn.resample_hypotheses(p_d, None, G.to_dev(loss), 0.2, 0.05, 0.02, 5, 1)
+    torch.cuda.synchronize()
+    assert np.allclose(p_d.cpu().numpy(), p_ref, atol=1e-6, rtol=0)
+
+
+# ------------------------------------------------------- whole optimisation runs
+def full_observation(of, gt, intr):
+    pix = np.arange(intr["width"] * intr["height"], dtype=np.int32)[None]
+    return of.render(gt[None], pix, intr)[0].reshape(intr["height"], intr["width"], 3).astype(
+        np.float32)
+
+
+def oracle_run(of, poses, obs, intr, pixels, n_steps, update, resample_at):
+    """The optimisation loop on the oracle: its own render, loss and gradient
+    each step, its own update, and resampling after the steps listed in
+    resample_at ({steps done: (keep_frac, round)})."""
+    losses, grads = [], []
+    state = None
+    for it in range(n_steps):
+        out = of.render_loss_grad(poses, pixels(it), obs, intr)
+        loss = out["loss"].astype(np.float32)
+        dpose = out["dpose"].astype(np.float32)
+        losses.append(loss)
+        grads.append(dpose)
+        poses, state = update(poses, state, dpose, it)
+        if it + 1 in resample_at:
+            keep, rnd = resample_at[it + 1]
+            poses, state, _ = O.resample(poses, state, loss, keep, 0.05, 0.02, 7, rnd)
+    return poses, np.array(losses), np.array(grads)
+
+
+def test_momentum_run_matches_oracle_tiny(pn):
+    """The small configuration's run: K = 4 hypotheses, 256 pixels each, Huber
+    loss, 10 steps of momentum SGD (lr 1e-2, beta 0.9)."""
+    import torch
+    case = G.make_case("tiny32")
+    w = case.w
+    of = O.OracleField(case.spec)
+    obs = full_observation(of, case.gt, case.intr)
+    K, P, n = 4, 256, 10
+    pixels = lambda it: synth.pixel_batch(0, it, K, P, w.width, w.height)  # noqa: E731
+
+    def upd(p, m, g, it):
+        return O.step_momentum(p, np.zeros((K, 6), np.float32) if m is None else m, g, 1e-2, 0.9)
+
+    p_ref, l_ref, g_ref = oracle_run(of, case.poses[:K], obs, case.intr, pixels, n, upd, {})
+    f = pn.Field(case.spec)
+    p_d = G.to_dev(case.poses[:K])
+    m_d = G.to_dev(np.zeros((K, 6), np.float32))
+    obs_d = G.to_dev(obs)
+    losses = []
+    for it in range(n):
+        loss, dpose = f.render_loss_grad(p_d, G.to_dev(pixels(it)), obs_d, case.intr)
+        losses.append(loss.cpu().numpy())
+        pn.step_momentum(p_d, m_d, dpose, 1e-2, 0.9)
+    torch.cuda.synchronize()
+    p_g = p_d.cpu().numpy()
+    f.close()
+    losses = np.array(losses)
+    assert np.allclose(losses, l_ref, rtol=G.LOSS_RTOL, atol=0)
+    # a gradient error of GRAD_RTOL moves each step by at most lr |m| GRAD_RTOL,
+    # and each side rounds the pose to float32 after every step
+    bound = sum(1e-2 * np.abs(g_ref[: i + 1]).max() * (1 / (1 - 0.9)) * G.GRAD_RTOL
+                for i in range(n)) + n * 2.0 ** -21
+    assert np.abs(p_g - p_ref).max() <= bound
+
+
+def test_adam_mc_schedule_run_matches_oracle(pn):
+    """A scaled-down run of the Monte Carlo schedule with Adam: 8 hypotheses,
+    6 free steps, then 2 rounds of resampling (keep 1/2, then 1/4) each
+    followed by 4 steps, learning rates decaying every 8 steps.
+
+    The step lengths are 1/1000 of the paper's.  On the seeded random field
+    the pose gradient is rough at the paper's step length: a pose change of
+    5e-6 rad moves tens of samples across hash-grid cell faces, where the
+    encoding's slope jumps, and changes the gradient by 10-20 %.  Adam's
+    normalised steps would then turn the last-bit differences of the two
+    sides into independent trajectories within two steps.  The paper's
+    learning rates are checked step by step above."""
+    import torch
+    from paper_2210_10108_amd import driver
+    case = G.make_case("tiny32", K=8)
+    w = case.w
+    of = O.OracleField(case.spec)
+    obs = full_observation(of, case.gt, case.intr)
+    K, P = 8, 128
+    sched = driver.MCSchedule(n_hypotheses=K, s1=6, s2=4, rounds=2, keep_frac=0.5)
+    n = sched.total_steps
+    assert n == 14
+    hp = dict(lr_rot=5e-6, lr_trans=3e-6, decay_base=0.33, decay_steps=8, second_moment=1)
+    pixels = lambda it: synth.pixel_batch(1, it, K, P, w.width, w.height)  # noqa: E731
+
+    def upd(p, s, g, it):
+        s = np.zeros((K, O.ADAM_STATE), np.float32) if s is None else s
+        return O.step_adam(p, s, g, it, **hp)
+
+    # the schedule written out from Sec. IV-B: resample after 6 and 10 steps
+    p_ref, l_ref, _ = oracle_run(of, case.poses, obs, case.intr, pixels, n, upd,
+                                 {6: (0.5, 1), 10: (0.25, 2)})
+    # resampling ranks by loss: the case must not hold near-ties
+    for s in (5, 9):
+        srt = np.sort(l_ref[s])
+        assert np.min(np.diff(srt) / srt[1:]) > 20 * G.LOSS_RTOL
+    f = pn.Field(case.spec)
+    p_d = G.to_dev(case.poses)
+    obs_d = G.to_dev(obs)
+    losses = []
+    pix_d = [G.to_dev(pixels(it)) for it in range(n)]
+    loss, state = driver.invert(f, p_d, obs_d, case.intr, lambda it: pix_d[it], sched,
+                                pn.AdamParams(**hp), sigma_rot=0.05, sigma_trans=0.02, seed=7,
+                                on_step=lambda it, l: losses.append(l.cpu().numpy()))
+    torch.cuda.synchronize()
+    p_g = p_d.cpu().numpy()
+    f.close()
+    losses = np.array(losses)
+    assert np.allclose(losses, l_ref, rtol=G.LOSS_RTOL, atol=0)
+    # per-subspace Adam moves each step by lr |m_hat| / sqrt(v_hat), whose
+    # relative change is bounded by that of the gradient; both sides round the
+    # pose to float32 after every step
+    bound = n * (5e-6 * math.sqrt(3) * G.GRAD_RTOL + 2.0 ** -21)
+    assert np.abs(p_g - p_ref).max() <= bound
+    assert np.array_equal(state.cpu().numpy()[:, 12] > 0, np.ones(K, bool))
