@@ -8,9 +8,19 @@
 // Work split: the levels are partitioned into NG groups of two levels each,
 // and block b works on group b % NG.  Workgroups are dispatched round-robin
 // over the XCDs, so every XCD (own 4 MB L2) serves the same one or two level
-// groups for the whole launch and its L2 holds only those levels' tables.  One
-// thread handles one sample of its group; blocks are persistent and stride
-// over the compacted sample array.
+// groups for the whole launch and its L2 holds only those levels' tables.
+// Each sample takes both levels of its group in turn (one position, twice the
+// independent gathers in flight).
+//
+// Two adjacent lanes handle one sample: lane side 0 gathers the four vertices
+// at the cell's lower x, side 1 the four at x + 1.  The two x neighbours of a
+// vertex nearly always share a cache line: a dense level stores them side by
+// side, and the spatial hash (x ^ y' ^ z') of x and x + 1 differs only in the
+// bits that the carry of x + 1 flips, the lowest bit for even x.  Each gather
+// instruction so touches about half as many lines as with one lane per sample,
+// and the gather's cost follows the lines, not the instructions.  Each lane
+// blends its half; one lane-pair exchange completes the sums.  Blocks are
+// persistent and stride over the compacted sample array.
 //
 // Features are stored SoA, row p = (l % 4) * 2 LPG + (l / 4) * 2 + q for
 // feature q of level l (the order in which the MLP kernels feed them to MFMA),
@@ -81,10 +91,11 @@ __device__ inline Pos sample_pos(const DevField& f, const DevBatch& b, const Dev
   return ps;
 }
 
-// Cell of one level and the 8 corner table indices (in vertex units).
+// Cell of one level: lower corner, interpolation weights, and the table index
+// of corner k (bit 0: x + 1, bit 1: y + 1, bit 2: z + 1).
 struct Cell {
   float w[3];
-  uint32_t idx[8];
+  uint32_t i0[3];
 };
 
 // The cell comes from the float product x N (as a reference implementation in
@@ -93,32 +104,27 @@ struct Cell {
 __device__ __forceinline__ void make_cell(const DevField& f, int l, const float x[3],
                                           const float dx[3], Cell& c) {
   const int N = f.res[l];
-  const uint32_t n1 = f.n1[l];
-  const bool dense = f.dense[l] != 0;
-  uint32_t i0[3];
   const float Nf = (float)N;
 #pragma unroll
   for (int a = 0; a < 3; ++a) {
     float pos = __fmul_rn(x[a], Nf);
     int ci = (int)pos;
     ci = ci < N - 1 ? ci : N - 1;
-    i0[a] = (uint32_t)ci;
+    c.i0[a] = (uint32_t)ci;
     c.w[a] = (__fsub_rn(pos, (float)ci) + fmaf(x[a], Nf, -pos)) + Nf * dx[a];
   }
-  const uint32_t mask = f.T - 1u;
+}
+
+__device__ __forceinline__ uint32_t corner_index(const DevField& f, int l, const Cell& c, int k) {
+  const bool dense = f.dense[l] != 0;
+  const uint32_t n1 = f.n1[l];
   const uint32_t sy = dense ? n1 : kPrime1;
   const uint32_t sz = dense ? n1 * n1 : kPrime2;
-  const uint32_t y0 = i0[1] * sy, y1 = y0 + sy;
-  const uint32_t z0 = i0[2] * sz, z1 = z0 + sz;
-  const uint32_t base = (uint32_t)l * f.T;
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    uint32_t xi = i0[0] + (k & 1);
-    uint32_t yi = (k & 2) ? y1 : y0;
-    uint32_t zi = (k & 4) ? z1 : z0;
-    uint32_t h = dense ? (xi + yi + zi) : ((xi ^ yi ^ zi) & mask);
-    c.idx[k] = base + h;
-  }
+  const uint32_t xi = c.i0[0] + (k & 1);
+  const uint32_t yi = (c.i0[1] + ((k >> 1) & 1)) * sy;
+  const uint32_t zi = (c.i0[2] + ((k >> 2) & 1)) * sz;
+  const uint32_t h = dense ? (xi + yi + zi) : ((xi ^ yi ^ zi) & (f.T - 1u));
+  return (uint32_t)l * f.T + h;
 }
 
 template <bool F16>
@@ -140,7 +146,7 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
   make_cell(f, l, x, dx, c);
   float2 v[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, c.idx[k]);
+  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, corner_index(f, l, c, k));
   const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
   const float ux = 1.0f - wx, uy = 1.0f - wy, uz = 1.0f - wz;
   float2 r;
@@ -165,6 +171,38 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
   return r;
 }
 
+// One lane's half of level l: the four corners with x offset `side`, blended
+// with that side's x weight.  p = (feature_0, feature_1, then when GRAD the
+// half of d feature_q / d pos_a at 2 + 3 q + a).  The halves of the two lanes
+// of a pair add up to the whole cell's values.
+template <bool F16, bool GRAD>
+__device__ __forceinline__ void half_cell(const DevField& f, int l, const float x[3],
+                                          const float dx[3], int side, float p[8]) {
+  Cell c;
+  make_cell(f, l, x, dx, c);
+  float2 v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = vertex<F16>(f, corner_index(f, l, c, 2 * j + side));
+  const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
+  const float ux = 1.0f - wx, uy = 1.0f - wy, uz = 1.0f - wz;
+  const float sx = side ? wx : ux;       // this side's x weight
+  const float sgn = side ? 1.0f : -1.0f; // its derivative along x
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    float t[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t[j] = q ? v[j].y : v[j].x;
+    // corners j: bit 0 = y + 1, bit 1 = z + 1
+    const float ty0 = uz * t[0] + wz * t[2], ty1 = uz * t[1] + wz * t[3];
+    p[q] = sx * (uy * ty0 + wy * ty1);
+    if (GRAD) {
+      p[2 + 3 * q + 0] = sgn * (uy * ty0 + wy * ty1);
+      p[2 + 3 * q + 1] = sx * (ty1 - ty0);
+      p[2 + 3 * q + 2] = sx * (uy * (t[2] - t[0]) + wy * (t[3] - t[1]));
+    }
+  }
+}
+
 __device__ __forceinline__ int feat_row(const DevField& f, int l, int q) {
   return (l & 3) * 2 * f.lpg + (l >> 2) * 2 + q;
 }
@@ -174,40 +212,44 @@ __device__ __forceinline__ int jac_row(const DevField& f, int l, int q, int a) {
 }
 
 // ------------------------------------------------------------------ forward
-// One thread: both levels of its group for one sample (the position is
-// computed once).  Features and Jacobian rows are streamed out with
-// non-temporal stores so that they do not displace the level tables from L2.
-// GRAD: also store the Jacobian rows.
+// A lane pair: both levels of its group for one sample (the position is
+// computed by both lanes).  Lane side q keeps feature q and its Jacobian row:
+// it adds the partner's half of those to its own, and hands over its half of
+// the other feature.  Outputs are streamed out with non-temporal stores so that
+// they do not displace the level tables from L2.  GRAD: also the Jacobian.
 template <bool F16, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWork w) {
+  constexpr int kSamples = kBlock / 2;
   const int S = *w.total;
   const int grp = blockIdx.x % f.n_groups;
   const int stride = gridDim.x / f.n_groups;
   const int64_t cap = w.cap;
-  for (int sb = blockIdx.x / f.n_groups; sb * kBlock < S; sb += stride) {
-    const int s = sb * kBlock + threadIdx.x;
-    if (s >= S) break;
+  const int side = threadIdx.x & 1;
+  for (int sb = blockIdx.x / f.n_groups; sb * kSamples < S; sb += stride) {
+    const int s = sb * kSamples + (threadIdx.x >> 1);
+    if (s >= S) break;  // the two lanes of a pair leave together
     Pos ps = sample_pos(f, b, w, s);
 #pragma unroll
     for (int li = 0; li < 2; ++li) {
       const int l = f.grp_lv[grp][li];
-      float* r0 = w.feat + (int64_t)feat_row(f, l, 0) * cap;
-      float* r1 = w.feat + (int64_t)feat_row(f, l, 1) * cap;
-      __half* jr = w.jac + (int64_t)jac_row(f, l, 0, 0) * cap;
-      float jac[6];
-      float2 a = level_feature<F16>(f, l, ps.x, ps.dx, GRAD ? jac : nullptr);
-      __builtin_nontemporal_store(a.x, r0 + s);
-      __builtin_nontemporal_store(a.y, r1 + s);
+      float p[8];
+      half_cell<F16, GRAD>(f, l, ps.x, ps.dx, side, p);
+      const float keep = side ? p[1] : p[0];
+      const float give = side ? p[0] : p[1];
+      __builtin_nontemporal_store(keep + __shfl_xor(give, 1),
+                                  w.feat + (int64_t)feat_row(f, l, side) * cap + s);
       if (GRAD) {
+        unsigned short* jr =
+            reinterpret_cast<unsigned short*>(w.jac + (int64_t)jac_row(f, l, side, 0) * cap);
 #pragma unroll
-        for (int q = 0; q < 2; ++q)
-#pragma unroll
-          for (int c = 0; c < 3; ++c) {
-            const float v = (ps.clamped >> c) & 1u ? 0.0f : jac[3 * q + c];
-            __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)),
-                                        reinterpret_cast<unsigned short*>(jr) +
-                                            (int64_t)(3 * q + c) * cap + s);
-          }
+        for (int a = 0; a < 3; ++a) {
+          const float jk = side ? p[5 + a] : p[2 + a];
+          const float jg = side ? p[2 + a] : p[5 + a];
+          float v = jk + __shfl_xor(jg, 1);
+          v = (ps.clamped >> a) & 1u ? 0.0f : v;
+          __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)),
+                                      jr + (int64_t)a * cap + s);
+        }
       }
     }
   }
