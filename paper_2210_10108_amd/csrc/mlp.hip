@@ -87,17 +87,19 @@ __device__ __forceinline__ void sample_dir(const DevWork& w, int s, float d[3]) 
 }
 
 // ReLU on 4 accumulator tiles of one column tile; bit 4m+i of the mask = unit
-// 16m + 4g + i was active.
+// 16m + 4g + i was active.  Integer arithmetic on the bit patterns keeps it in
+// three vector instructions per value: max(bits, 0) as a signed integer is the
+// ReLU (every non-positive float, -0 included, has a bit pattern <= 0), and
+// min(bits, 1) of the result is its mask bit.
 __device__ __forceinline__ uint32_t relu_mask(floatx4 (&t)[4]) {
   uint32_t mk = 0;
 #pragma unroll
   for (int m = 0; m < 4; ++m)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float v = t[m][i];
-      const bool on = v > 0.0f;
-      t[m][i] = on ? v : 0.0f;
-      mk |= (on ? 1u : 0u) << (4 * m + i);
+      const int r = max(__float_as_int(t[m][i]), 0);
+      t[m][i] = __int_as_float(r);
+      mk |= min((uint32_t)r, 1u) << (4 * m + i);
     }
   return mk;
 }
@@ -176,7 +178,7 @@ __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float
 // GRAD = false (forward rendering only) skips the ReLU masks the backward
 // pass needs; it is a separate kernel so that profiles keep the two apart.
 template <int LPG, bool GRAD>
-__global__ __launch_bounds__(kBlock) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
   constexpr int KD = 2 * LPG;  // features per lane group
   constexpr int NT = kFwdNT, TS = 16 * NT;
   __shared__ WeightUnit lds[kFwdUnits];
