@@ -135,87 +135,155 @@ __device__ inline int march_wave(const DevField& f, const RayGeom& g, int lane, 
   return kept;
 }
 
+// Exclusive scan of one value per thread over a block of kScanBlock threads
+// (shuffles within each wavefront, the wavefront totals in LDS, fixed order);
+// returns the thread's exclusive prefix and sets *block_total.
+__device__ inline int block_exclusive_scan(int c, int* s_wave, int* block_total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int inc = c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int x = __shfl_up(inc, d);
+    if (lane >= d) inc += x;
+  }
+  if (lane == 63) s_wave[wv] = inc;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int v = 0; v < kScanBlock / 64; ++v) {
+    const int x = s_wave[v];
+    before += v < wv ? x : 0;
+    total += x;
+  }
+  *block_total = total;
+  return before + inc - c;
+}
+
+// One thread per ray: ray generation and box clip, stored for the kernels
+// that follow (their float values decide the samples, so they are computed
+// once).  Without an occupancy grid a uniform-mode ray keeps all its
+// candidates, so its count is known here; SCAN then also takes the first
+// level of the offset scan (as k_scan_local does).
+template <bool SCAN>
+__global__ __launch_bounds__(kRayBlock) void k_ray_setup(DevField f, DevBatch b, DevWork w) {
+  static_assert(!SCAN || kRayBlock == kScanBlock, "one scan block per workgroup");
+  const int ray = blockIdx.x * kRayBlock + threadIdx.x;
+  int c = 0;
+  if (ray < b.n_rays) {
+    const RayGeom g = make_ray(f, b, ray);
+    w.rdx[ray] = g.d[0];
+    w.rdy[ray] = g.d[1];
+    w.rdz[ray] = g.d[2];
+    w.rex[ray] = g.de[0];
+    w.rey[ray] = g.de[1];
+    w.rez[ray] = g.de[2];
+    w.rtn[ray] = g.tn;
+    w.rtf[ray] = g.tf;
+    w.rdelta[ray] = g.delta;
+    if (SCAN) {
+      c = g.hit ? (f.n_uniform < f.max_per_ray ? f.n_uniform : f.max_per_ray) : 0;
+      w.count[ray] = c;
+    }
+  }
+  if (SCAN) {
+    __shared__ int s_wave[kScanBlock / 64];
+    int total;
+    const int e = block_exclusive_scan(c, s_wave, &total);
+    if (ray < b.n_rays) w.off[ray] = e;
+    if (threadIdx.x == 0) w.blocksum[blockIdx.x] = total;
+  }
+}
+
+// The stored geometry of a ray (hit = the clip left an interval).
+__device__ inline RayGeom stored_ray(const DevBatch& b, const DevWork& w, int ray) {
+  RayGeom g;
+  const float* pose = b.poses + 12 * (ray / b.P);
+  g.o[0] = pose[3];
+  g.o[1] = pose[7];
+  g.o[2] = pose[11];
+  g.d[0] = w.rdx[ray];
+  g.d[1] = w.rdy[ray];
+  g.d[2] = w.rdz[ray];
+  g.tn = w.rtn[ray];
+  g.tf = w.rtf[ray];
+  g.delta = w.rdelta[ray];
+  g.hit = g.tf > g.tn;
+  return g;
+}
+
 // Rays of one wavefront: kRaysPerWave consecutive rays, marched one after the
-// other with all 64 lanes testing candidates; lane 0 stores the ray's count and
-// geometry.
+// other with all 64 lanes testing candidates; lane 0 stores the ray's count.
+// (Not launched when k_ray_setup already knows the counts.)
 __global__ __launch_bounds__(kRayBlock) void k_ray_count(DevField f, DevBatch b, DevWork w) {
   int lane = threadIdx.x & 63;
   int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
   for (int q = 0; q < kRaysPerWave; ++q) {
     int ray = wave * kRaysPerWave + q;
     if (ray >= b.n_rays) break;
-    RayGeom g = make_ray(f, b, ray);
+    const RayGeom g = stored_ray(b, w, ray);
     int n = march_wave<false>(f, g, lane, f.max_per_ray, nullptr, nullptr, nullptr, ray);
-    if (lane == 0) {
-      w.count[ray] = n;
-      w.rdx[ray] = g.d[0];
-      w.rdy[ray] = g.d[1];
-      w.rdz[ray] = g.d[2];
-      w.rex[ray] = g.de[0];
-      w.rey[ray] = g.de[1];
-      w.rez[ray] = g.de[2];
-      w.rtn[ray] = g.tn;
-      w.rtf[ray] = g.tf;
-      w.rdelta[ray] = g.delta;
-    }
+    if (lane == 0) w.count[ray] = n;
   }
 }
 
-// Exclusive scan of the counts of each block of kScanBlock rays (fixed-order
-// Hillis-Steele in LDS): off[ray] = offset inside the block, blocksum = total.
+// Exclusive scan of the counts of each block of kScanBlock rays: off[ray] =
+// offset inside the block, blocksum = the block's total.
 __global__ __launch_bounds__(kScanBlock) void k_scan_local(DevBatch b, DevWork w) {
-  __shared__ int s_off[kScanBlock];
-  int tid = threadIdx.x;
-  int ray = blockIdx.x * kScanBlock + tid;
-  int c = ray < b.n_rays ? w.count[ray] : 0;
-  s_off[tid] = c;
-  __syncthreads();
-  for (int off = 1; off < kScanBlock; off <<= 1) {
-    int x = tid >= off ? s_off[tid - off] : 0;
-    __syncthreads();
-    s_off[tid] += x;
-    __syncthreads();
-  }
-  if (ray < b.n_rays) w.off[ray] = s_off[tid] - c;
-  if (tid == kScanBlock - 1) w.blocksum[blockIdx.x] = s_off[tid];
+  __shared__ int s_wave[kScanBlock / 64];
+  const int ray = blockIdx.x * kScanBlock + threadIdx.x;
+  const int c = ray < b.n_rays ? w.count[ray] : 0;
+  int total;
+  const int e = block_exclusive_scan(c, s_wave, &total);
+  if (ray < b.n_rays) w.off[ray] = e;
+  if (threadIdx.x == 0) w.blocksum[blockIdx.x] = total;
 }
 
-// Exclusive scan of the block totals in one workgroup (n_blocks <= 8192); also
-// writes the batch's sample total.
-__global__ __launch_bounds__(1024) void k_scan_blocks(DevWork w, int n_blocks) {
-  __shared__ int s[1024];
-  constexpr int kPer = 8;
-  int tid = threadIdx.x;
+// Second level, in one workgroup: exclusive scan of the block totals
+// (n_blocks <= kMaxScanBlocks, kPer per thread; shuffles within wavefronts,
+// the wavefront totals in LDS), the batch's sample total, and the samples of
+// every hypothesis -- the difference of the exclusive offsets at its first
+// ray and past its last -- which the host reads to size and plan the chunks.
+__global__ __launch_bounds__(1024) void k_scan_finish(DevBatch b, DevWork w, int n_blocks) {
+  constexpr int kPer = kMaxScanBlocks / 1024;
+  __shared__ int s_wave[1024 / 64];
+  __shared__ int s_bs[kMaxScanBlocks];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   int v[kPer], acc = 0;
+#pragma unroll
   for (int q = 0; q < kPer; ++q) {
-    int i = tid * kPer + q;
+    const int i = tid * kPer + q;
     v[q] = i < n_blocks ? w.blocksum[i] : 0;
     acc += v[q];
   }
-  s[tid] = acc;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    int x = tid >= off ? s[tid - off] : 0;
-    __syncthreads();
-    s[tid] += x;
-    __syncthreads();
+  int inc = acc;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int x = __shfl_up(inc, d);
+    if (lane >= d) inc += x;
   }
-  int run = s[tid] - acc;  // exclusive prefix of this thread's chunk
+  if (lane == 63) s_wave[wv] = inc;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int u = 0; u < 1024 / 64; ++u) {
+    const int x = s_wave[u];
+    before += u < wv ? x : 0;
+    total += x;
+  }
+  int run = before + inc - acc;  // exclusive prefix of this thread's blocks
+#pragma unroll
   for (int q = 0; q < kPer; ++q) {
-    int i = tid * kPer + q;
-    if (i < n_blocks) w.blocksum[i] = run;
+    const int i = tid * kPer + q;
+    if (i < n_blocks) {
+      w.blocksum[i] = run;
+      s_bs[i] = run;
+    }
     run += v[q];
   }
-  if (tid == 1023) *w.total = s[1023];
-}
-
-// Samples of every hypothesis (difference of the offsets at its first ray and
-// past its last ray); the host reads these to size and plan the sample chunks.
-__global__ void k_hyp_totals(DevBatch b, DevWork w) {
-  int k = blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= b.K) return;
-  auto excl = [&](int r) { return r < b.n_rays ? w.blocksum[r / kScanBlock] + w.off[r] : *w.total; };
-  w.hyp_total[k] = excl((k + 1) * b.P) - excl(k * b.P);
+  if (tid == 0) *w.total = total;
+  __syncthreads();
+  auto excl = [&](int r) { return r < b.n_rays ? s_bs[r / kScanBlock] + w.off[r] : total; };
+  for (int k = tid; k < b.K; k += 1024) w.hyp_total[k] = excl((k + 1) * b.P) - excl(k * b.P);
 }
 
 // Second march of the rays of one sample chunk (rays ray_base .. of the counted
@@ -240,17 +308,7 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
     int n = wc.count[ray];
     if (lane == 0) wc.off[ray] = o;
     if (n == 0) continue;
-    RayGeom g;
-    g.o[0] = b.poses[12 * (ray / b.P) + 3];
-    g.o[1] = b.poses[12 * (ray / b.P) + 7];
-    g.o[2] = b.poses[12 * (ray / b.P) + 11];
-    g.d[0] = wc.rdx[ray];
-    g.d[1] = wc.rdy[ray];
-    g.d[2] = wc.rdz[ray];
-    g.tn = wc.rtn[ray];
-    g.tf = wc.rtf[ray];
-    g.delta = wc.rdelta[ray];
-    g.hit = 1;
+    const RayGeom g = stored_ray(b, wc, ray);
     march_wave<true>(f, g, lane, n, wc.t + o, j_out ? j_out + o : nullptr, wc.sray + o, ray);
   }
 }
@@ -259,14 +317,20 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
 
 hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w,
                               hipStream_t s) {
-  int n_scan = (b.n_rays + kScanBlock - 1) / kScanBlock;
+  const int n_scan = (b.n_rays + kScanBlock - 1) / kScanBlock;
   if (n_scan > kMaxScanBlocks) return hipErrorInvalidValue;
-  int rays_per_block = kRaysPerWave * (kRayBlock / 64);
-  int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
-  hipLaunchKernelGGL(k_ray_count, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w);
-  hipLaunchKernelGGL(k_scan_local, dim3(n_scan), dim3(kScanBlock), 0, s, b, w);
-  hipLaunchKernelGGL(k_scan_blocks, dim3(1), dim3(1024), 0, s, w, n_scan);
-  hipLaunchKernelGGL(k_hyp_totals, dim3((b.K + 255) / 256), dim3(256), 0, s, b, w);
+  const int n_setup = (b.n_rays + kRayBlock - 1) / kRayBlock;
+  if (f.march_mode == 0 && f.occ_res <= 0) {
+    // counts known at set-up: the first scan level runs in the same kernel
+    hipLaunchKernelGGL(k_ray_setup<true>, dim3(n_setup), dim3(kRayBlock), 0, s, f, b, w);
+  } else {
+    hipLaunchKernelGGL(k_ray_setup<false>, dim3(n_setup), dim3(kRayBlock), 0, s, f, b, w);
+    const int rays_per_block = kRaysPerWave * (kRayBlock / 64);
+    const int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
+    hipLaunchKernelGGL(k_ray_count, dim3(n_march), dim3(kRayBlock), 0, s, f, b, w);
+    hipLaunchKernelGGL(k_scan_local, dim3(n_scan), dim3(kScanBlock), 0, s, b, w);
+  }
+  hipLaunchKernelGGL(k_scan_finish, dim3(1), dim3(1024), 0, s, b, w, n_scan);
   return hipGetLastError();
 }
 
