@@ -308,19 +308,20 @@ class _Adam(C.Structure):
     _fields_ = [("lr_rot", C.c_float), ("lr_trans", C.c_float), ("beta1", C.c_float),
                 ("beta2", C.c_float), ("eps", C.c_float), ("decay_base", C.c_float),
                 ("decay_steps", C.c_int32), ("staircase", C.c_int32),
-                ("second_moment", C.c_int32)]
+                ("second_moment", C.c_int32), ("representation", C.c_int32)]
 
 
 def step_adam(poses, state, dpose, step, lr_rot, lr_trans, beta1=0.9, beta2=0.999, eps=1e-8,
-              decay_base=1.0, decay_steps=0, staircase=0, second_moment=0):
-    """Adam on SO(3) x T(3) (Sec. IV-A, IV-C); returns new (poses, state)."""
+              decay_base=1.0, decay_steps=0, staircase=0, second_moment=0, representation=0):
+    """Adam on SO(3) x T(3) (Sec. IV-A, IV-C), or on the coupled se(3) twist
+    (representation = 1); returns new (poses, state)."""
     poses = np.array(poses, dtype=np.float32, copy=True)
     state = np.array(state, dtype=np.float32, copy=True)
     dpose = np.ascontiguousarray(dpose, dtype=np.float32)
     K = poses.shape[0]
     assert state.shape == (K, ADAM_STATE) and dpose.shape == (K, 6)
     a = _Adam(lr_rot, lr_trans, beta1, beta2, eps, decay_base, decay_steps, staircase,
-              second_moment)
+              second_moment, representation)
     lib().orc_step_adam(K, _p(poses), _p(state), _p(dpose), step, C.byref(a))
     return poses, state
 

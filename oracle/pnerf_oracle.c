@@ -789,13 +789,55 @@ static double decayed_lr(double lr0, const orc_adam* a, int32_t step) {
   return lr0 * pow((double)a->decay_base, e);
 }
 
+/* SE(3) exponential of the twist (w, v) (Lynch and Park, Modern Robotics,
+ * Prop. 3.25): rotation Exp(w), translation V(w) v with
+ * V = I + (1 - cos th)/th^2 [w]x + (th - sin th)/th^3 [w]x^2 (series for tiny th). */
+static void exp_se3(const double w[3], const double v[3], double R[9], double t[3]) {
+  orc_exp_so3(w, R);
+  double th2 = w[0] * w[0] + w[1] * w[1] + w[2] * w[2], th = sqrt(th2);
+  double B, C;
+  if (th < 1e-4) {
+    B = 0.5 - th2 / 24.0;
+    C = 1.0 / 6.0 - th2 / 120.0;
+  } else {
+    B = (1.0 - cos(th)) / th2;
+    C = (th - sin(th)) / (th2 * th);
+  }
+  double Wx[9] = {0, -w[2], w[1], w[2], 0, -w[0], -w[1], w[0], 0};
+  double Wv[3], W2v[3];
+  for (int i = 0; i < 3; ++i) Wv[i] = Wx[3 * i] * v[0] + Wx[3 * i + 1] * v[1] + Wx[3 * i + 2] * v[2];
+  for (int i = 0; i < 3; ++i)
+    W2v[i] = Wx[3 * i] * Wv[0] + Wx[3 * i + 1] * Wv[1] + Wx[3 * i + 2] * Wv[2];
+  for (int i = 0; i < 3; ++i) t[i] = v[i] + B * Wv[i] + C * W2v[i];
+}
+
+/* T <- Exp(w, v) T for the twist (w, v) about the world origin: R <- E R,
+ * o <- E o + V v. */
+static void apply_twist(float* pose, const double w[3], const double v[3]) {
+  double E[9], tv[3], R[9], o[3];
+  exp_se3(w, v, E, tv);
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 3; ++j) R[3 * i + j] = (double)pose[4 * i + j];
+    o[i] = (double)pose[4 * i + 3];
+  }
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 3; ++j)
+      pose[4 * i + j] = (float)(E[3 * i] * R[j] + E[3 * i + 1] * R[3 + j] + E[3 * i + 2] * R[6 + j]);
+    pose[4 * i + 3] = (float)(E[3 * i] * o[0] + E[3 * i + 1] * o[1] + E[3 * i + 2] * o[2] + tv[i]);
+  }
+}
+
 /* Adam (Kingma and Ba, ICLR 2015, Algorithm 1) applied independently on the two
  * subspaces SO(3) and T(3) (Sec. IV-A, "Momentum-Based Optimization"): the
  * first moments are vectors (the rotational one built from the torque), and the
  * bias-corrected step is applied as a rotation Exp(u_w) of the orientation and
  * a shift u_t of the camera centre.  The second moment is kept per component,
  * or (second_moment = 1) as one squared norm per subspace.  State row per
- * hypothesis: m[6], v[6], its own step count t, three zeros. */
+ * hypothesis: m[6], v[6], its own step count t, three zeros.
+ * representation = 1 runs the same optimiser on the coupled se(3) twist that
+ * Sec. IV-A compares against (exponential coordinates about the world origin,
+ * as in iNeRF): the gradient w.r.t. the twist is (tau + o x g, g) for
+ * dpose = (tau, g) and camera centre o, and the step is T <- Exp(u) T. */
 void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, int32_t step,
                    const orc_adam* a) {
   const double b1 = (double)a->beta1, b2 = (double)a->beta2, eps = (double)a->eps;
@@ -803,18 +845,26 @@ void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, in
                            decayed_lr((double)a->lr_trans, a, step)};
   for (int32_t k = 0; k < K; ++k) {
     float* st = state + 16 * k;
+    double G[6];
+    for (int q = 0; q < 6; ++q) G[q] = (double)dpose[6 * k + q];
+    if (a->representation == 1) {
+      const double o[3] = {poses[12 * k + 3], poses[12 * k + 7], poses[12 * k + 11]};
+      G[0] += o[1] * G[5] - o[2] * G[4];
+      G[1] += o[2] * G[3] - o[0] * G[5];
+      G[2] += o[0] * G[4] - o[1] * G[3];
+    }
     double t = (double)st[12] + 1.0; /* t <- t + 1 */
     double u[6];
     for (int sub = 0; sub < 2; ++sub) {
-      const float* g = dpose + 6 * k + 3 * sub;
+      const double* g = G + 3 * sub;
       double m[3], v[3], sq = 0.0;
-      for (int i = 0; i < 3; ++i) sq += (double)g[i] * (double)g[i];
+      for (int i = 0; i < 3; ++i) sq += g[i] * g[i];
       for (int i = 0; i < 3; ++i) {
-        m[i] = b1 * (double)st[3 * sub + i] + (1.0 - b1) * (double)g[i];
+        m[i] = b1 * (double)st[3 * sub + i] + (1.0 - b1) * g[i];
         if (a->second_moment)
           v[i] = b2 * (double)st[6 + 3 * sub] + (1.0 - b2) * sq;
         else
-          v[i] = b2 * (double)st[6 + 3 * sub + i] + (1.0 - b2) * (double)g[i] * (double)g[i];
+          v[i] = b2 * (double)st[6 + 3 * sub + i] + (1.0 - b2) * g[i] * g[i];
       }
       for (int i = 0; i < 3; ++i) {
         double m_hat = m[i] / (1.0 - pow(b1, t));
@@ -825,7 +875,10 @@ void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, in
       }
     }
     st[12] = (float)t;
-    apply_update(poses + 12 * k, u, u + 3);
+    if (a->representation == 1)
+      apply_twist(poses + 12 * k, u, u + 3);
+    else
+      apply_update(poses + 12 * k, u, u + 3);
   }
 }
 

@@ -108,6 +108,7 @@ typedef struct {
   int32_t decay_steps;   /* 0: no decay */
   int32_t staircase;     /* 1: exponent floor(step / decay_steps) */
   int32_t second_moment; /* 0: per component; 1: squared norm per subspace */
+  int32_t representation; /* 0: SO(3) x T(3); 1: coupled se(3) twist, T <- Exp(u) T */
 } orc_adam;
 void orc_step_adam(int32_t K, float* poses, float* state, const float* dpose, int32_t step,
                    const orc_adam* a);
