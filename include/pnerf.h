@@ -194,12 +194,19 @@ pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum,
  *   lr_s(step) = lr_s * decay_base^floor(step / decay_steps)  (staircase = 1)
  * and no decay when decay_steps = 0.  The paper's setting is lr_rot 5e-3,
  * lr_trans 3e-3, decay_base 0.33, decay_steps 256.
+ * representation = 1 runs the same optimiser on the coupled se(3) twist that
+ * Sec. IV-A compares against (exponential coordinates about the world origin,
+ * as in iNeRF): g is replaced by the twist gradient (tau + o x f, f) for
+ * dpose = (tau, f) and camera centre o, and the step is T <- Exp(u) T, i.e.
+ * R <- Exp(u_w) R, o <- Exp(u_w) o + V(u_w) u_t with
+ * V(w) = I + (1 - cos|w|)/|w|^2 [w]x + (|w| - sin|w|)/|w|^3 [w]x^2.
  * state (device) float32 [K][PNERF_ADAM_STATE] = (m_w[3], m_t[3], v_w[3],
  * v_t[3], n, 0, 0, 0): all zero before a hypothesis's first step (also what
  * pnerf_resample_hypotheses leaves in a redrawn slot given state_dim =
  * PNERF_ADAM_STATE); n is exact up to 2^24 steps.  poses (device) [K][3][4],
  * dpose (device) [K][6], params (host).  Requires K >= 1, step >= 0, finite
- * lr >= 0, 0 <= beta < 1, eps > 0, decay_base > 0, decay_steps >= 0. */
+ * lr >= 0, 0 <= beta < 1, eps > 0, decay_base > 0, decay_steps >= 0,
+ * staircase, second_moment and representation each 0 or 1. */
 #define PNERF_ADAM_STATE 16
 typedef struct {
   float lr_rot, lr_trans;  /* learning rates at step 0 */
@@ -208,6 +215,7 @@ typedef struct {
   int32_t decay_steps;     /* 0: constant learning rates */
   int32_t staircase;       /* 0: continuous decay; 1: stepwise */
   int32_t second_moment;   /* 0: per component; 1: per subspace (rotation invariant) */
+  int32_t representation;  /* 0: SO(3) x T(3) (the paper's); 1: coupled se(3) twist */
 } pnerf_adam_params;
 
 pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float* dpose,

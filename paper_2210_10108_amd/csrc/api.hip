@@ -879,8 +879,9 @@ pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float*
   if (!(std::isfinite(p->eps) && p->eps > 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "eps");
   if (!(std::isfinite(p->decay_base) && p->decay_base > 0.0f) || p->decay_steps < 0)
     return fail(PNERF_ERR_INVALID_ARG, "decay_base/decay_steps");
-  if ((p->staircase != 0 && p->staircase != 1) || (p->second_moment != 0 && p->second_moment != 1))
-    return fail(PNERF_ERR_INVALID_ARG, "staircase/second_moment must be 0 or 1");
+  if ((p->staircase != 0 && p->staircase != 1) || (p->second_moment != 0 && p->second_moment != 1) ||
+      (p->representation != 0 && p->representation != 1))
+    return fail(PNERF_ERR_INVALID_ARG, "staircase/second_moment/representation must be 0 or 1");
   if (!poses || !state || !dpose) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
   // Learning-rate decay of Sec. IV-C, evaluated once per call in double.
   double scale = 1.0;
@@ -891,7 +892,7 @@ pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float*
   }
   HIP_TRY(launch_step_adam(K, poses, state, dpose, (double)p->lr_rot * scale,
                            (double)p->lr_trans * scale, p->beta1, p->beta2, p->eps,
-                           p->second_moment, (hipStream_t)stream));
+                           p->second_moment, p->representation, (hipStream_t)stream));
   return PNERF_OK;
 }
 

@@ -124,7 +124,7 @@ hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dp
                                 float beta, hipStream_t s);
 hipError_t launch_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
                             double lr_t, double b1, double b2, double eps, int per_subspace,
-                            hipStream_t s);
+                            int twist, hipStream_t s);
 hipError_t launch_resample(int K, float* poses, float* state, int state_dim, const float* loss,
                            int n_keep, float sr, float st, uint64_t seed, uint32_t round,
                            int32_t* scratch, hipStream_t s);

@@ -40,6 +40,39 @@ __device__ inline void apply(float* pose, const double w[3], const double v[3]) 
   }
 }
 
+// SE(3) exponential applied on the left, about the world origin: R <- E R,
+// o <- E o + V(w) v with E = Exp(w), V(w) = I + B [w]x + C [w]x^2,
+// B = (1 - cos th)/th^2, C = (th - sin th)/th^3 (series for small th).
+__device__ inline void apply_twist(float* pose, const double w[3], const double v[3]) {
+  double E[9];
+  exp_so3(w, E);
+  const double th2 = w[0] * w[0] + w[1] * w[1] + w[2] * w[2], th = sqrt(th2);
+  double B, C;
+  if (th < 1e-4) {
+    B = 0.5 - th2 / 24.0;
+    C = 1.0 / 6.0 - th2 / 120.0;
+  } else {
+    B = (1.0 - cos(th)) / th2;
+    C = (th - sin(th)) / (th2 * th);
+  }
+  const double wv[3] = {w[1] * v[2] - w[2] * v[1], w[2] * v[0] - w[0] * v[2],
+                        w[0] * v[1] - w[1] * v[0]};
+  const double wwv[3] = {w[1] * wv[2] - w[2] * wv[1], w[2] * wv[0] - w[0] * wv[2],
+                         w[0] * wv[1] - w[1] * wv[0]};
+  double R[9], o[3];
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 3; ++j) R[3 * i + j] = (double)pose[4 * i + j];
+    o[i] = (double)pose[4 * i + 3];
+  }
+  for (int i = 0; i < 3; ++i) {
+    for (int j = 0; j < 3; ++j)
+      pose[4 * i + j] =
+          (float)(E[3 * i] * R[j] + E[3 * i + 1] * R[3 + j] + E[3 * i + 2] * R[6 + j]);
+    pose[4 * i + 3] = (float)(E[3 * i] * o[0] + E[3 * i + 1] * o[1] + E[3 * i + 2] * o[2] +
+                              v[i] + B * wv[i] + C * wwv[i]);
+  }
+}
+
 __global__ void k_step_momentum(int K, float* poses, float* mom, const float* dpose, float lr,
                                 float beta) {
   int k = blockIdx.x * blockDim.x + threadIdx.x;
@@ -61,17 +94,28 @@ __global__ void k_step_momentum(int K, float* poses, float* mom, const float* dp
 
 // Adam (Kingma and Ba, Algorithm 1) run separately on the rotation and the
 // translation subspace.  State row: m[6], v[6], step count, 3 zero pads.
+// twist: the coupled se(3) representation -- gradient (tau + o x f, f) for
+// dpose = (tau, f), step T <- Exp(u) T.
 __global__ void k_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
-                            double lr_t, double b1, double b2, double eps, int per_subspace) {
+                            double lr_t, double b1, double b2, double eps, int per_subspace,
+                            int twist) {
   int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= K) return;
   float* st = state + (size_t)kAdamState * k;
+  double G[6];
+  for (int q = 0; q < 6; ++q) G[q] = (double)dpose[6 * k + q];
+  if (twist) {
+    const double o[3] = {poses[12 * k + 3], poses[12 * k + 7], poses[12 * k + 11]};
+    const double tf[3] = {o[1] * G[5] - o[2] * G[4], o[2] * G[3] - o[0] * G[5],
+                          o[0] * G[4] - o[1] * G[3]};
+    for (int a = 0; a < 3; ++a) G[a] += tf[a];
+  }
   double n = (double)st[12] + 1.0;
   double c1 = 1.0 - pow(b1, n), c2 = 1.0 - pow(b2, n);
   double u[6];
   for (int sub = 0; sub < 2; ++sub) {
     double g[3], m[3], v[3];
-    for (int a = 0; a < 3; ++a) g[a] = (double)dpose[6 * k + 3 * sub + a];
+    for (int a = 0; a < 3; ++a) g[a] = G[3 * sub + a];
     for (int a = 0; a < 3; ++a) m[a] = b1 * (double)st[3 * sub + a] + (1.0 - b1) * g[a];
     if (per_subspace) {
       double gg = g[0] * g[0] + g[1] * g[1] + g[2] * g[2];
@@ -90,7 +134,10 @@ __global__ void k_step_adam(int K, float* poses, float* state, const float* dpos
   st[12] = (float)n;
   float pose[12];
   for (int q = 0; q < 12; ++q) pose[q] = poses[12 * k + q];
-  apply(pose, u, u + 3);
+  if (twist)
+    apply_twist(pose, u, u + 3);
+  else
+    apply(pose, u, u + 3);
   for (int q = 0; q < 12; ++q) poses[12 * k + q] = pose[q];
 }
 
@@ -188,9 +235,9 @@ hipError_t launch_step_momentum(int K, float* poses, float* mom, const float* dp
 
 hipError_t launch_step_adam(int K, float* poses, float* state, const float* dpose, double lr_r,
                             double lr_t, double b1, double b2, double eps, int per_subspace,
-                            hipStream_t s) {
+                            int twist, hipStream_t s) {
   hipLaunchKernelGGL(k_step_adam, dim3((K + 63) / 64), dim3(64), 0, s, K, poses, state, dpose,
-                     lr_r, lr_t, b1, b2, eps, per_subspace);
+                     lr_r, lr_t, b1, b2, eps, per_subspace, twist);
   return hipGetLastError();
 }
 

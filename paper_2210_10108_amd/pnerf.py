@@ -281,12 +281,13 @@ class AdamParams(C.Structure):
     _fields_ = [("lr_rot", C.c_float), ("lr_trans", C.c_float), ("beta1", C.c_float),
                 ("beta2", C.c_float), ("eps", C.c_float), ("decay_base", C.c_float),
                 ("decay_steps", C.c_int32), ("staircase", C.c_int32),
-                ("second_moment", C.c_int32)]
+                ("second_moment", C.c_int32), ("representation", C.c_int32)]
 
     def __init__(self, lr_rot=5e-3, lr_trans=3e-3, beta1=0.9, beta2=0.999, eps=1e-8,
-                 decay_base=0.33, decay_steps=256, staircase=0, second_moment=0):
+                 decay_base=0.33, decay_steps=256, staircase=0, second_moment=0,
+                 representation=0):
         super().__init__(lr_rot, lr_trans, beta1, beta2, eps, decay_base, decay_steps,
-                         staircase, second_moment)
+                         staircase, second_moment, representation)
 
 
 def step_adam(poses, state, dpose, step: int, params: AdamParams, stream=None):

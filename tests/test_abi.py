@@ -54,6 +54,7 @@ int main(void) {{
   printf("astate %d\\n", PNERF_ADAM_STATE);
   printf("a.decay_base %zu\\n", offsetof(pnerf_adam_params, decay_base));
   printf("a.second_moment %zu\\n", offsetof(pnerf_adam_params, second_moment));
+  printf("a.representation %zu\\n", offsetof(pnerf_adam_params, representation));
   O(n_levels); O(level_res); O(table); O(w_color3); O(density_bias); O(aabb_max);
   O(march_mode); O(step); O(t_stop); O(occ_bits); O(occ_threshold); O(background);
   O(loss_type); O(loss_param); O(sh_dir_grad); O(max_workspace_bytes); O(overlap_chunks);
@@ -94,7 +95,7 @@ def test_host_validation_rejects_bad_arguments(pn):
     assert b"step" in L.pnerf_last_error()
     for field, bad in [("beta1", 1.0), ("beta2", -0.1), ("eps", 0.0), ("lr_rot", -1e-3),
                        ("lr_trans", float("nan")), ("decay_base", 0.0), ("decay_steps", -1),
-                       ("staircase", 2), ("second_moment", 3)]:
+                       ("staircase", 2), ("second_moment", 3), ("representation", 2)]:
         p = pn.AdamParams()
         setattr(p, field, bad)
         assert L.pnerf_step_adam(4, None, None, None, 0, C.byref(p), None) == \

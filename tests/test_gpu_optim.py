@@ -75,6 +75,41 @@ def test_step_adam_matches_oracle(pn, second_moment, staircase):
     assert np.array_equal(p_g[5], poses[5])    # zero gradient, fresh state: no motion
 
 
+@pytest.mark.parametrize("second_moment,lr", [(0, (5e-3, 3e-3)), (1, (5e-3, 3e-3)),
+                                               (1, (0.3, 0.5))])
+def test_step_adam_se3_twist_matches_oracle(pn, second_moment, lr):
+    """The coupled se(3) representation (Sec. IV-A's comparison): twist
+    gradient (tau + o x f, f) and T <- Exp(u) T, at the paper's rates and at
+    large steps where the exponential's coupling terms are not small."""
+    import torch
+    rng = np.random.default_rng(30 + second_moment)
+    K, n_steps = 37, 60
+    w = synth.WORKLOADS["tiny32"]
+    poses = synth.perturb_poses(synth.ground_truth_pose(w, 1), K, 40, 0.3, 6)
+    st = adam_state(rng, K, second_moment)
+    grads = (rng.normal(size=(n_steps, K, 6)) * rng.uniform(0.01, 3, (1, K, 6))).astype(np.float32)
+    hp = dict(lr_rot=lr[0], lr_trans=lr[1], decay_base=0.33, decay_steps=256,
+              second_moment=second_moment, representation=1)
+    prm = pn.AdamParams(**hp)
+    p_ref, s_ref = poses, st
+    p_d, s_d, g_d = G.to_dev(poses), G.to_dev(st), G.to_dev(grads)
+    for i in range(n_steps):
+        p_ref, s_ref = O.step_adam(p_ref, s_ref, grads[i], i, **hp)
+        pn.step_adam(p_d, s_d, g_d[i], i, prm)
+    torch.cuda.synchronize()
+    p_g, s_g = p_d.cpu().numpy(), s_d.cpu().numpy()
+    scale = max(1.0, np.abs(p_ref).max())
+    assert np.allclose(p_g, p_ref, atol=n_steps * 2.0 ** -23 * scale, rtol=0)
+    assert np.allclose(s_g, s_ref, rtol=1e-5, atol=1e-12)
+    # the decoupled step from the same state moves elsewhere
+    p0 = G.to_dev(poses)
+    pn.step_adam(p0, G.to_dev(st), g_d[0], 0, pn.AdamParams(**dict(hp, representation=0)))
+    p1 = G.to_dev(poses)
+    pn.step_adam(p1, G.to_dev(st), g_d[0], 0, prm)
+    torch.cuda.synchronize()
+    assert np.abs(p0.cpu().numpy() - p1.cpu().numpy()).max() > 1e-6
+
+
 def test_step_adam_paper_setting_single_step(pn):
     """One step at the paper's setting from a fresh state moves every component
     by its learning rate against the sign of its gradient."""
@@ -92,6 +127,65 @@ def test_step_adam_paper_setting_single_step(pn):
     assert np.allclose(p_d.cpu().numpy(), p_ref, atol=2.0 ** -22, rtol=0)
     assert np.allclose(p_d.cpu().numpy()[:, :, 3] - poses[:, :, 3], -3e-3 * np.sign(g[:, 3:]),
                        atol=1e-6)
+
+
+def _frobenius_dpose(T, Ts):
+    """(tau, f) of L = |R - R*|^2 + |o - o*|^2: tau by central differences of
+    a rotation about the camera centre, f = 2 (o - o*)."""
+    from scipy.spatial.transform import Rotation
+    R, o = T[:, :3].astype(np.float64), T[:, 3].astype(np.float64)
+
+    def L(Rm):
+        return np.sum((Rm - Ts[:, :3]) ** 2)
+    h = 1e-6
+    tau = np.zeros(3)
+    for a in range(3):
+        e = np.zeros(3)
+        e[a] = h
+        tau[a] = (L(Rotation.from_rotvec(e).as_matrix() @ R) -
+                  L(Rotation.from_rotvec(-e).as_matrix() @ R)) / (2 * h)
+    return np.concatenate([tau, 2 * (o - Ts[:, 3])]).astype(np.float32)[None]
+
+
+def test_decoupled_path_is_straight_and_coupled_path_curves(pn):
+    """The argument of Sec. IV-A (Fig. 2), in 3-D through the library's Adam
+    step: minimising |T - T*|^2, whose centre gradient always points at the
+    target centre, the SO(3) x T(3) representation moves the camera centre on
+    the straight segment to the target, while the coupled se(3) twist bends
+    its path and takes longer to converge.  (The paper's own toy is 2-D and
+    leaves its start, target and rates unstated: its step counts are not
+    reproduced.)"""
+    import torch
+    from scipy.spatial.transform import Rotation
+    T0 = np.zeros((1, 3, 4), np.float32)
+    T0[0, :, :3] = np.eye(3)
+    T0[0, :, 3] = [2.0, 0.0, 0.0]
+    Ts = np.zeros((3, 4))
+    Ts[:, :3] = Rotation.from_rotvec([0.0, 0.0, 1.2]).as_matrix()
+    Ts[:, 3] = [0.0, 1.0, 0.5]
+    a, b = T0[0, :, 3].astype(np.float64), Ts[:, 3]
+    result = {}
+    for rep in (0, 1):
+        prm = pn.AdamParams(lr_rot=0.02, lr_trans=0.02, decay_steps=0, second_moment=1,
+                            representation=rep)
+        p_d = G.to_dev(T0)
+        s_d = G.to_dev(np.zeros((1, O.ADAM_STATE), np.float32))
+        dev, conv = 0.0, None
+        for it in range(600):
+            T = p_d.cpu().numpy()[0]
+            pn.step_adam(p_d, s_d, G.to_dev(_frobenius_dpose(T, Ts)), it, prm)
+            torch.cuda.synchronize()
+            T = p_d.cpu().numpy()[0]
+            c = T[:, 3].astype(np.float64)
+            dev = max(dev, np.linalg.norm(np.cross(c - a, b - a)) / np.linalg.norm(b - a))
+            if conv is None and np.linalg.norm(T - Ts) < 1e-2:
+                conv = it + 1
+        result[rep] = (dev, conv, np.linalg.norm(T - Ts))
+    (dev0, conv0, err0), (dev1, conv1, err1) = result[0], result[1]
+    assert dev0 < 1e-5                      # straight up to float rounding
+    assert dev1 > 0.1                       # visibly curved
+    assert err0 < 1e-3 and err1 < 1e-3      # both converge
+    assert conv0 < conv1
 
 
 @pytest.mark.parametrize("K,keep", [(64, 0.25), (300, 0.1)])
