@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--optimizer", default="momentum", choices=("momentum", "adam"),
                     help="pose update: the workload's momentum SGD, or Adam with the "
                          "learning rates and decay of Sec. IV-C")
+    ap.add_argument("--sh-dir-grad", type=int, default=0, choices=(0, 1),
+                    help="1: also carry the gradient through the view-direction (SH) input")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--overlap-chunks", type=int, default=0,
@@ -143,7 +145,7 @@ def main():
         del src, dst
     w = synth.WORKLOADS[args.workload]
     fa = synth.make_field(w, args.seed)
-    spec = synth.field_spec(w, fa)        # occupancy (if any) built on the device
+    spec = synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad)  # occupancy built on the device
     field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
@@ -267,11 +269,14 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "mlp_arithmetic": "bf16 MFMA on split hi/lo operands, fp32 accumulation",
-        "data": "synthetic (seeded random frozen field; observation rendered at a seeded ground-truth pose)",
+        "data": ("synthetic (seeded random frozen field" +
+                 ("" if w.density == "random" else ", density shaped as one object in empty space") +
+                 "; observation rendered at a seeded ground-truth pose)"),
         "config": {"workload": w.name, "K": K, "P": w.P, "levels": w.n_levels,
                    "table": f"2^{w.log2_table}", "image": f"{w.width}x{w.height}",
                    "sampling": "uniform" if w.march_mode == 0 else "lattice+occupancy",
-                   "optimizer": args.optimizer, "parallelism": "single-gpu"},
+                   "optimizer": args.optimizer, "sh_dir_grad": args.sh_dir_grad,
+                   "parallelism": "single-gpu"},
         "hypothesis_iters_per_sec": K * S / elapsed,
         "samples_per_step": samples_per_step,
         "mean_samples_per_ray": samples_per_step / w.n_rays,

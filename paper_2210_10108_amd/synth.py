@@ -62,6 +62,7 @@ class Workload:
     resample_sigma_rot_deg: float = 5.0
     resample_sigma_trans: float = 0.03
     cam_radius: float = 2.5
+    density: str = "random"     # "random", or "bump": an object in empty space
 
     @property
     def table_size(self) -> int:
@@ -107,8 +108,19 @@ WORKLOADS = {
                       1, 0, 4.0 * math.sqrt(3.0) / 2048.0, 2048, 1e-4, 256, 0.01,
                       800, 800, 1111.0, 400.0, 400.0, 1024, 512, 60.0, 0.5, 1000,
                       resample_every=100, keep_frac=0.10),
+    # structured density: one object (a smooth density bump) in empty space, so
+    # that occupancy skipping and early ray termination take effect, as they
+    # do on the paper's object scenes
+    "ngp800_bump_occ128": Workload("ngp800_bump_occ128", 16, 2, 19, 16, 2048, "f32", *_UNIT, 1, 0,
+                                   math.sqrt(3.0) / 1024.0, 1024, 1e-4, 128, 0.01,
+                                   800, 800, 1111.0, 400.0, 400.0, 64, 4096, 30.0, 0.2, 300,
+                                   density="bump"),
+    "tiny_bump": Workload("tiny_bump", 4, 2, 13, 16, 64, "f32", *_UNIT, 1, 0,
+                          math.sqrt(3.0) / 128.0, 256, 1e-4, 32, 0.01,
+                          32, 32, 40.0, 16.0, 16.0, 4, 256, 20.0, 0.15, 10, density="bump"),
 }
-ORDER = ["tiny32", "ngp800_uniform", "ngp800_occ128", "cam640_f16_occ128", "large4m_occ256"]
+ORDER = ["tiny32", "ngp800_uniform", "ngp800_occ128", "cam640_f16_occ128", "large4m_occ256",
+         "ngp800_bump_occ128", "tiny_bump"]
 
 
 def level_resolutions(n_levels: int, n_min: int, n_max: int) -> np.ndarray:
@@ -142,11 +154,27 @@ class FieldArrays:
     density_bias: float = -1.0
 
 
+# Density bump of the "bump" fields: centre and radius in the unit box,
+# sigma = exp(BUMP_GAIN * relu(feature) - BUMP_OFFSET) with feature 0 of level 0
+# holding exp(-|p - c|^2 / r^2) at the level's vertices.
+BUMP_CENTER = (0.0, 0.0, 0.0)
+BUMP_RADIUS = 0.3
+BUMP_GAIN = 12.0
+BUMP_OFFSET = 6.0
+
+
 def make_field(w: Workload, seed: int) -> FieldArrays:
     """Draw the frozen field of workload `w` from `seed`.
 
     Stream order: table, W_d1, W_d2, W_c1, W_c2, W_c3.  Table entries are
     U(-1, 1); weights are Glorot-uniform on the padded shapes.
+
+    density = "bump" then shapes the density into one object in empty space:
+    feature 0 of level 0 (a dense level: vertex (i, j, k) at entry
+    i + j n1 + k n1^2) takes exp(-|p - c|^2 / r^2) at the vertex positions, the
+    first density-layer unit reads only that feature, the sigma logit reads
+    only that unit (gain BUMP_GAIN), and the density bias is -BUMP_OFFSET.  The
+    other weights, the other features and the colour stay random.
     """
     rng = np.random.default_rng(seed)
     L, F, T = w.n_levels, w.n_features, w.table_size
@@ -156,12 +184,31 @@ def make_field(w: Workload, seed: int) -> FieldArrays:
     wc1 = _glorot(rng, COLOR_IN, HIDDEN)
     wc2 = _glorot(rng, HIDDEN, HIDDEN)
     wc3 = _glorot(rng, HIDDEN, 3)
+    density_bias = -1.0
+    if w.density == "bump":
+        N = int(level_resolutions(L, w.n_min, w.n_max)[0])
+        n1 = N + 1
+        if n1 ** 3 > T:
+            raise ValueError("the bump needs a dense level 0: (N_min + 1)^3 <= T")
+        g = np.arange(n1, dtype=np.float64) / N
+        lo = np.asarray(w.aabb_min, np.float64)
+        ext = np.asarray(w.aabb_max, np.float64) - lo
+        x = lo[0] + g * ext[0] - BUMP_CENTER[0]
+        y = lo[1] + g * ext[1] - BUMP_CENTER[1]
+        z = lo[2] + g * ext[2] - BUMP_CENTER[2]
+        d2 = x[None, None, :] ** 2 + y[None, :, None] ** 2 + z[:, None, None] ** 2  # [k][j][i]
+        table[0, :n1 ** 3, 0] = np.exp(-d2 / BUMP_RADIUS ** 2).reshape(-1).astype(np.float32)
+        wd1[:, 0] = 0.0
+        wd1[0, 0] = 1.0
+        wd2[:, 0] = 0.0
+        wd2[0, 0] = BUMP_GAIN
+        density_bias = -BUMP_OFFSET
     if w.param_dtype == "f16":
         cast = lambda a: a.astype(np.float16)
     else:
         cast = lambda a: a
     return FieldArrays(level_resolutions(L, w.n_min, w.n_max), cast(table), cast(wd1),
-                       cast(wd2), cast(wc1), cast(wc2), cast(wc3))
+                       cast(wd2), cast(wc1), cast(wc2), cast(wc3), density_bias)
 
 
 def look_at_pose(cam_pos: np.ndarray, target=(0.0, 0.0, 0.0)) -> np.ndarray:

@@ -413,3 +413,49 @@ def test_loss_grad_large_scene_full_batch_sampled_hypotheses(pn):
     case = with_oracle_occupancy(G.make_case("large4m_occ256"), w.occ_res, w.occ_threshold)
     n = check_sampled_hypotheses(pn, case, [0, 511, 1023])
     assert n > 100_000_000
+
+
+# -------------------------------------------------------- structured density
+def test_device_occupancy_build_bump_field_matches_oracle(pn):
+    w = synth.WORKLOADS["ngp800_bump_occ128"]
+    case = G.make_case("ngp800_bump_occ128", K=2, P=64)
+    of0 = O.OracleField(dataclasses.replace(case.spec, occ_res=0, occ_bits=None))
+    R = w.occ_res
+    ref = synth.unpack_bits(of0.build_occupancy(R, w.occ_threshold), R)
+    f = pn.Field(dataclasses.replace(case.spec, occ_bits=None))
+    got = synth.unpack_bits(f.occupancy(), R)
+    f.close()
+    assert 0.05 < ref.mean() < 0.5
+    diff = np.argwhere(got != ref)
+    assert len(diff) <= 64
+    for z, y, x in diff:   # disagreements only where sigma is within rounding of thr
+        c = (np.array([x, y, z]) + 0.5) / R
+        feat, _ = of0.encode(c.astype(np.float32), c)
+        s = math.exp(of0.density_mlp(feat)[0] + case.spec.density_bias)
+        assert abs(s - w.occ_threshold) <= 1e-5 * w.occ_threshold
+
+
+@pytest.mark.parametrize("name,K,P", [("tiny_bump", None, None), ("ngp800_bump_occ128", None, None)])
+def test_march_bump_bitexact(pn, name, K, P):
+    w = synth.WORKLOADS[name]
+    case = with_oracle_occupancy(G.make_case(name, K=K, P=P), w.occ_res, w.occ_threshold)
+    total = check_march(pn, case)
+    assert 0 < total < case.pix.size * 64     # most candidates skipped
+
+
+def test_loss_grad_tiny_bump(pn):
+    w = synth.WORKLOADS["tiny_bump"]
+    case = with_oracle_occupancy(G.make_case("tiny_bump"), w.occ_res, w.occ_threshold)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, ex = check_full(pn, case, obs, ref)
+    cnt = np.diff(ref["march"][0])
+    assert np.sum(ref["stop"] < cnt) >= 5     # early termination took effect
+
+
+def test_loss_grad_ngp800_bump_full_batch_sampled_hypotheses(pn):
+    w = synth.WORKLOADS["ngp800_bump_occ128"]
+    case = with_oracle_occupancy(G.make_case("ngp800_bump_occ128"), w.occ_res, w.occ_threshold)
+    n = check_sampled_hypotheses(pn, case, [0, 31, 63])
+    assert n > 0

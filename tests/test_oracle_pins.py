@@ -711,6 +711,60 @@ def test_resample_clears_adam_state_rows(oracle_lib):
     assert np.array_equal(rank6, rank) and np.array_equal(p6, out_p) and np.array_equal(p0, out_p)
 
 
+# ------------------------------------------------------ structured density
+def test_bump_field_density_closed_form(oracle_lib):
+    """On the bump field only feature 0 of the dense level 0 drives the
+    density: sigma(p) = exp(GAIN relu(trilinear blend of the bump's vertex
+    values at p) - OFFSET), the blend written out with numpy."""
+    w = synth.WORKLOADS["tiny_bump"]
+    fa = synth.make_field(w, 0)
+    of = oracle_lib.OracleField(synth.field_spec(w, fa, occ_res=0))
+    N = int(fa.level_res[0])
+    n1 = N + 1
+    vals = fa.table[0, :n1 ** 3, 0].astype(np.float64).reshape(n1, n1, n1)  # [k][j][i]
+    rng = np.random.default_rng(3)
+    for x in rng.uniform(0.0, 1.0, size=(50, 3)):
+        feat, _ = of.encode(x.astype(np.float32), x)
+        sigma = math.exp(of.density_mlp(feat)[0] + fa.density_bias)
+        pos = x * N
+        i0 = np.minimum(pos.astype(int), N - 1)
+        t = pos - i0
+        v = 0.0
+        for dk in (0, 1):
+            for dj in (0, 1):
+                for di in (0, 1):
+                    wgt = ((t[0] if di else 1 - t[0]) * (t[1] if dj else 1 - t[1]) *
+                           (t[2] if dk else 1 - t[2]))
+                    v += wgt * vals[i0[2] + dk, i0[1] + dj, i0[0] + di]
+        want = math.exp(synth.BUMP_GAIN * max(v, 0.0) - synth.BUMP_OFFSET)
+        assert sigma == pytest.approx(want, rel=1e-6)
+
+
+def test_bump_workload_skips_and_stops_early(oracle_lib):
+    """The structured workload exercises occupancy skipping and early ray
+    termination (the random fields leave every cell occupied and no ray
+    opaque)."""
+    import dataclasses
+    w = synth.WORKLOADS["tiny_bump"]
+    spec = synth.field_spec(w, synth.make_field(w, 0))
+    of0 = oracle_lib.OracleField(dataclasses.replace(spec, occ_res=0, occ_bits=None))
+    bits = of0.build_occupancy(w.occ_res, w.occ_threshold)
+    occ = synth.unpack_bits(bits, w.occ_res)
+    assert 0.05 < occ.mean() < 0.5
+    of = oracle_lib.OracleField(dataclasses.replace(spec, occ_bits=bits))
+    gt = synth.ground_truth_pose(w, 0)
+    poses = synth.perturb_poses(gt, w.K, w.max_rot_deg, w.max_trans, 0)
+    pix = synth.pixel_batch(0, 0, w.K, w.P, w.width, w.height)
+    intr = synth.intrinsics(w)
+    m = of.march(poses, pix, intr)
+    cnt = np.diff(m[0])
+    out = of.shade(poses.astype(np.float64), pix, np.zeros((w.height, w.width, 3), np.float32),
+                   intr, m)
+    hit = cnt > 0
+    assert 0.05 < hit.mean() < 0.9
+    assert np.sum(out["stop"][hit] < cnt[hit]) >= 5          # opaque rays stop early
+
+
 # --------------------------------------------------------------- occupancy
 def test_occupancy_build(oracle_lib):
     w, spec = tiny_spec()
