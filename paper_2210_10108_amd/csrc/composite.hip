@@ -13,20 +13,8 @@ namespace {
 
 constexpr int kBlock = 256;
 
-__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    float y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  return x;
-}
-
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-  return x;
-}
+// Sum over the wavefront, in every lane.
+__device__ __forceinline__ float wave_sum(float x) { return lane_value(wave_incl_scan(x), 63); }
 
 // Pixel-based RGB loss of one channel (Sec. IV-C): r = C - y; returns the
 // loss and writes d loss / d C.  p: threshold of Huber (0) and Smooth L1 (7),
@@ -96,7 +84,7 @@ __device__ inline Chunk step_chunk(const DevField& f, const DevWork& w, int base
   ch.c[1] = valid ? w.cg[base + i] : 0.0f;
   ch.c[2] = valid ? w.cb[base + i] : 0.0f;
   ch.tau = ch.sig * delta;
-  float incl = wave_incl_scan(ch.tau, lane) + carry;
+  float incl = wave_incl_scan(ch.tau) + carry;
   incl_out = incl;
   ch.T_in = __expf(-(incl - ch.tau));
   ch.T_out = __expf(-incl);
@@ -133,7 +121,7 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
     bool use = ch.live && lane <= last;
 #pragma unroll
     for (int q = 0; q < 3; ++q) C[q] += wave_sum(use ? ch.w * ch.c[q] : 0.0f);
-    carry = __shfl(incl, last);
+    carry = lane_value(incl, last);
     if (st) break;
   }
   float T_end = __expf(-carry);
@@ -179,13 +167,13 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
 #pragma unroll
     for (int q = 0; q < 3; ++q) {
       float wc = use ? ch.w * ch.c[q] : 0.0f;
-      float p = wave_incl_scan(wc, lane) + pre[q];
-      pre[q] = __shfl(p, 63);
+      float p = wave_incl_scan(wc) + pre[q];
+      pre[q] = lane_value(p, 63);
       float S = C[q] - p;  // colour behind sample i (incl. background)
       gs += gC[q] * (ch.T_out * ch.c[q] - S);
       gz[q] = ch.w * gC[q] * ch.c[q] * (1.0f - ch.c[q]);
     }
-    carry2 = __shfl(incl, 63);
+    carry2 = lane_value(incl, 63);
     if (i < n) {
       w.sig[base + i] = use ? delta * gs * ch.sig : 0.0f;
       w.cr[base + i] = use ? gz[0] : 0.0f;

@@ -236,7 +236,7 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
       half_cell<F16, GRAD>(f, l, ps.x, ps.dx, side, p);
       const float keep = side ? p[1] : p[0];
       const float give = side ? p[0] : p[1];
-      __builtin_nontemporal_store(keep + __shfl_xor(give, 1),
+      __builtin_nontemporal_store(keep + lane_pair_swap(give),
                                   w.feat + (int64_t)feat_row(f, l, side) * cap + s);
       if (GRAD) {
         unsigned short* jr =
@@ -245,7 +245,7 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
         for (int a = 0; a < 3; ++a) {
           const float jk = side ? p[5 + a] : p[2 + a];
           const float jg = side ? p[2 + a] : p[5 + a];
-          float v = jk + __shfl_xor(jg, 1);
+          float v = jk + lane_pair_swap(jg);
           v = (ps.clamped >> a) & 1u ? 0.0f : v;
           __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)),
                                       jr + (int64_t)a * cap + s);

@@ -34,6 +34,34 @@ constexpr int kFD1 = 0, kFD2 = 4, kFC1 = 6, kFC2 = 10, kFC3 = 18, kFwdUnits = 20
 // K steps, density 2 (4 row tiles), density 1 (up to 2 row tiles x 2 K steps)
 constexpr int kBC2 = 0, kBC1 = 8, kBD2 = 12, kBD1 = 16, kBwdUnits = 20;
 
+// ---------------------------------------------------- wavefront primitives
+// Cross-lane data movement through DPP (data-parallel primitives of the
+// vector ALU) instead of the LDS crossbar that __shfl goes through.
+
+// The value of the partner lane (lane ^ 1).  Both lanes must be active.
+__device__ __forceinline__ float lane_pair_swap(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1 /* quad_perm
+                                                    [1,0,3,2] */, 0xF, 0xF, false));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront, all lanes active:
+// shifts by 1, 2, 4, 8 within each row of 16, then the last lane of row 0 (2)
+// into row 1 (3), and of row 1 into rows 2 and 3.  Fixed order.
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x111, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x112, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x114, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x118, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x142, 0xA, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x143, 0xC, 0xF, false));
+  return x;
+}
+
+// x of lane `lane` (uniform across the wavefront) in every lane.
+__device__ __forceinline__ float lane_value(float x, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
+}
+
 struct DevField {
   int32_t L, lpg;               // levels, levels per lane group (L / 4)
   uint32_t T;                   // table entries per level (power of two)
