@@ -109,9 +109,15 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   float C[3] = {0.f, 0.f, 0.f};
   float carry = 0.0f;
   int n_used = n;
+  Chunk first{};          // the ray's first step, reused by pass 2
+  float first_incl = 0.0f;
   for (int i0 = 0; i0 < n_used; i0 += 64) {
     float incl;
     Chunk ch = step_chunk(f, w, base, n, i0, delta, carry, lane, incl);
+    if (i0 == 0) {
+      first = ch;
+      first_incl = incl;
+    }
     uint64_t st = __ballot(ch.stop_here);
     int last = 63;
     if (st) {
@@ -160,8 +166,8 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
       }
       continue;
     }
-    float incl;
-    Chunk ch = step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
+    float incl = first_incl;
+    Chunk ch = i0 == 0 ? first : step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
     bool use = ch.live && i < n_used;
     float gs = 0.0f, gz[3];
 #pragma unroll
@@ -194,12 +200,12 @@ __device__ __forceinline__ void sample_terms(const DevField& f, const DevWork& w
 
 // Per-hypothesis reduction in two fixed-order stages.  Block (j, k) sums part
 // j of hypothesis k's rays (losses) and samples (torque and force terms): the
-// ranges are cut into n_parts equal pieces, each summed by a strided loop and a
-// tree in LDS.  k_reduce_final adds the n_parts partials of each hypothesis in
+// ranges are cut into n_parts equal pieces, each summed by a strided loop, a
+// wavefront scan and the four wavefronts' totals in order.  k_reduce_final adds the n_parts partials of each hypothesis in
 // order.  Same inputs give the same bits.
 __global__ __launch_bounds__(kBlock) void k_reduce_partial(DevField f, DevBatch b, DevWork w,
                                                            int n_parts, float* partial) {
-  __shared__ float red[7][kBlock];
+  __shared__ float red[7][kBlock / 64];
   int j = blockIdx.x, k = blockIdx.y, tid = threadIdx.x;
   int r0 = k * b.P, nr = b.P;
   int s0 = w.off[r0], ns = w.off[r0 + nr] - s0;
@@ -213,14 +219,18 @@ __global__ __launch_bounds__(kBlock) void k_reduce_partial(DevField f, DevBatch 
 #pragma unroll
     for (int q = 0; q < 6; ++q) acc[q] += o[q];
   }
-  for (int q = 0; q < 7; ++q) red[q][tid] = acc[q];
-  __syncthreads();
-  for (int stride = kBlock / 2; stride > 0; stride >>= 1) {
-    if (tid < stride)
-      for (int q = 0; q < 7; ++q) red[q][tid] += red[q][tid + stride];
-    __syncthreads();
+  const int lane = tid & 63, wv = tid >> 6;
+#pragma unroll
+  for (int q = 0; q < 7; ++q) {
+    const float v = wave_incl_scan(acc[q]);
+    if (lane == 63) red[q][wv] = v;
   }
-  if (tid < 7) partial[((size_t)k * n_parts + j) * 7 + tid] = red[tid][0];
+  __syncthreads();
+  if (tid < 7) {
+    float v = 0.0f;
+    for (int u = 0; u < kBlock / 64; ++u) v += red[tid][u];
+    partial[((size_t)k * n_parts + j) * 7 + tid] = v;
+  }
 }
 
 // One wavefront per hypothesis: lane j holds partial j (n_parts <= 64), then a
