@@ -335,3 +335,41 @@ def test_adam_mc_schedule_run_matches_oracle(pn):
     bound = n * (5e-6 * math.sqrt(3) * G.GRAD_RTOL + 2.0 ** -21)
     assert np.abs(p_g - p_ref).max() <= bound
     assert np.array_equal(state.cpu().numpy()[:, 12] > 0, np.ones(K, bool))
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_paper_schedule_converges_on_object_field(pn, seed):
+    """The whole method on the GPU: the Monte Carlo schedule of Sec. IV-B with
+    the constants and Adam of Sec. IV-C (64 hypotheses perturbed by up to 30
+    deg / 0.2, 2560 steps, 4 resampling rounds, 256 pixels per hypothesis per
+    step) on the object field.  The hypothesis with the lowest final loss
+    lands inside the paper's success thresholds (rotation error < 5 deg,
+    translation error < 0.05)."""
+    import dataclasses as dc
+    import torch
+    from paper_2210_10108_amd import driver
+    w = dc.replace(synth.WORKLOADS["ngp800_bump_occ128"], P=256)
+    f = pn.Field(synth.field_spec(w, synth.make_field(w, seed)))
+    gt = synth.ground_truth_pose(w, seed)
+    intr = synth.intrinsics(w)
+    dev = G.torch_dev()
+    n = w.width * w.height
+    obs = torch.empty(n, 3, dtype=torch.float32, device=dev)
+    gt_d = G.to_dev(gt[None])
+    for s in range(0, n, 1 << 16):
+        e = min(n, s + (1 << 16))
+        obs[s:e] = f.render(gt_d, torch.arange(s, e, dtype=torch.int32, device=dev)[None], intr)[0]
+    obs = obs.reshape(w.height, w.width, 3)
+    K = driver.PAPER_SCHEDULE.n_hypotheses
+    poses = G.to_dev(synth.perturb_poses(gt, K, w.max_rot_deg, w.max_trans, seed))
+    pix = [G.to_dev(synth.pixel_batch(seed, i, K, w.P, w.width, w.height)) for i in range(16)]
+    loss, _ = driver.invert(f, poses, obs, intr, lambda it: pix[it % 16], driver.PAPER_SCHEDULE,
+                            pn.AdamParams(), sigma_rot=math.radians(5.0), sigma_trans=0.03,
+                            seed=seed)
+    torch.cuda.synchronize()
+    f.close()
+    best = int(torch.argmin(loss).item())
+    p = poses.cpu().numpy()[best].astype(np.float64)
+    rot = math.degrees(math.acos(np.clip((np.trace(p[:, :3].T @ gt[:, :3]) - 1) / 2, -1, 1)))
+    trans = float(np.linalg.norm(p[:, 3] - gt[:, 3]))
+    assert rot < 5.0 and trans < 0.05, (rot, trans)
