@@ -31,7 +31,7 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kBlock = 256;  // 4 wavefronts
-constexpr int kFwdNT = 2;    // 16-sample column tiles per wavefront, forward
+constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
 constexpr int kBwdNT = 2;    // and backward
 
 struct Split {
@@ -178,7 +178,7 @@ __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float
 // GRAD = false (forward rendering only) skips the ReLU masks the backward
 // pass needs; it is a separate kernel so that profiles keep the two apart.
 template <int LPG, bool GRAD>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(3))) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
   constexpr int KD = 2 * LPG;  // features per lane group
   constexpr int NT = kFwdNT, TS = 16 * NT;
   __shared__ WeightUnit lds[kFwdUnits];
