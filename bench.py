@@ -48,6 +48,8 @@ def parse():
                          "Monte Carlo schedule of Sec. IV-B/IV-C (64 hypotheses, 2560 Adam "
                          "steps, 4 resampling rounds) on the workload's field and pixel count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="skip the on-box copy and bf16 GEMM reference rates")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--overlap-chunks", type=int, default=0,
                     help="field option: loss-gradient chunks pipelined over two streams "
@@ -123,10 +125,53 @@ def cpu_baseline(w, spec, gt, poses, pix_batches, budget_s):
         done_s += time.perf_counter() - t0
         samples += int(out["march"][0][-1])
         hyps += 1
+    # the same oracle on one thread, over one hypothesis
+    pix = pix_batches[0][0:1]
+    obs = np.zeros((w.height, w.width, 3), np.float32)
+    flat = np.unique(pix)
+    obs.reshape(-1, 3)[flat] = of.render(gt[None], flat[None].astype(np.int32), intr,
+                                         threads=threads)[0]
+    t0 = time.perf_counter()
+    out = of.render_loss_grad(poses[0:1], pix, obs, intr, threads=1)
+    one = int(out["march"][0][-1]) / (time.perf_counter() - t0)
     return {"value": samples / done_s, "unit": "ray-samples/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "single_thread_value": one,
             "sample": f"{hyps} hypotheses x {w.P} pixels (of {w.K} per batch; "
                       f"{samples} samples, {done_s:.1f} s timed, fp64 oracle, {threads} threads)"}
+
+
+def calibrate(dev):
+    """On-box reference rates, reported beside the published peaks: a 1 GiB
+    device-to-device copy (bytes read + written per second) and a large bf16
+    library GEMM (hipBLASLt through torch; 2 m n k flop per product)."""
+    import torch
+    out = {}
+    n = (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    out["copy_TBps"] = 10 * 2 * n * 4 / (time.perf_counter() - t0) / 1e12
+    del src, dst
+    m = 8192
+    a = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    b = torch.randn(m, m, dtype=torch.bfloat16, device=dev)
+    for _ in range(3):
+        c = a @ b
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(10):
+        c = a @ b
+    torch.cuda.synchronize()
+    out["bf16_gemm_TFLOPs"] = 10 * 2 * m ** 3 / (time.perf_counter() - t0) / 1e12
+    del a, b, c
+    torch.cuda.empty_cache()
+    return out
 
 
 def paper_run(args):
@@ -342,6 +387,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, spec, gt, poses0, pix_host, args.cpu_seconds)
+    if not args.no_calibration:
+        res["calibration"] = calibrate(dev)
     field.close()
     print(json.dumps(res))
 
