@@ -26,10 +26,14 @@
 // feature q of level l (the order in which the MLP kernels feed them to MFMA),
 // row stride = the workspace sample capacity.  The Jacobian d feature /
 // d pos of every level (pos = x N_l: bounded by the table's value
-// differences, zero along clamped components) is stored SoA in fp16 (rounding
-// below 2^-11 of each entry), row ((l % 4) LPG + l / 4) * 6 + 3 q + a, so that
-// lane group l % 4 of the MLP backward kernel reads one contiguous block of
-// rows; that kernel applies N_l and 1 / extent in fp32.
+// differences, zero along clamped components) is stored in fp16 (rounding
+// below 2^-11 of each entry) in blocks of 32 samples: block b, lane group
+// g = l % 4, row k = 6 (l / 4) + 3 q + a, at ((4 b + g) 6 LPG + k) 32 +
+// s % 32.  Lane group g of the MLP backward kernel reads its 6 LPG rows of a
+// 32-sample tile as one contiguous 384 LPG-byte run (one base, immediate
+// offsets), and the 3 rows of one level and feature fill whole cache lines, so
+// no line is written from two XCDs.  That kernel applies N_l and 1 / extent in
+// fp32.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -207,8 +211,11 @@ __device__ __forceinline__ int feat_row(const DevField& f, int l, int q) {
   return (l & 3) * 2 * f.lpg + (l >> 2) * 2 + q;
 }
 
-__device__ __forceinline__ int jac_row(const DevField& f, int l, int q, int a) {
-  return ((l & 3) * f.lpg + (l >> 2)) * 6 + 3 * q + a;
+// Index of the Jacobian entry (level l, feature q, axis 0) of sample s; axis a
+// is 32 entries further.
+__device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, int64_t s) {
+  const int kg = 6 * f.lpg;  // rows of one lane group
+  return ((s >> 5) * 4 + (l & 3)) * (int64_t)(kg * 32) + (6 * (l >> 2) + 3 * q) * 32 + (s & 31);
 }
 
 // ------------------------------------------------------------------ forward
@@ -239,16 +246,14 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
       __builtin_nontemporal_store(keep + lane_pair_swap(give),
                                   w.feat + (int64_t)feat_row(f, l, side) * cap + s);
       if (GRAD) {
-        unsigned short* jr =
-            reinterpret_cast<unsigned short*>(w.jac + (int64_t)jac_row(f, l, side, 0) * cap);
+        unsigned short* jr = reinterpret_cast<unsigned short*>(w.jac + jac_index(f, l, side, s));
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
           const float jk = side ? p[5 + a] : p[2 + a];
           const float jg = side ? p[2 + a] : p[5 + a];
           float v = jk + lane_pair_swap(jg);
           v = (ps.clamped >> a) & 1u ? 0.0f : v;
-          __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)),
-                                      jr + (int64_t)a * cap + s);
+          __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)), jr + 32 * a);
         }
       }
     }

@@ -436,11 +436,12 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     // d loss / d p = sum over the lane group's levels 4j + g of
     // d loss / d feature times the stored Jacobian, then over the 4 groups;
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
-    const __half* jrow = w.jac + (int64_t)(g * 6 * LPG) * w.cap;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       const int sc = s < S ? s : S - 1;
+      // this lane group's rows of the sample's 32-sample Jacobian block
+      const __half* jp = w.jac + ((int64_t)(sc >> 5) * 4 + g) * (6 * LPG * 32) + (sc & 31);
       float gx[3] = {0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < LPG; ++j) {
@@ -451,7 +452,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
           const float gq = gf[j / 2][nt][2 * (j % 2) + q];
 #pragma unroll
           for (int a = 0; a < 3; ++a)
-            gl[a] += gq * __half2float(jrow[(int64_t)(6 * j + 3 * q + a) * w.cap + sc]);
+            gl[a] += gq * __half2float(jp[(6 * j + 3 * q + a) * 32]);
         }
         const float N = (float)f.res[4 * j + g];
 #pragma unroll
