@@ -89,6 +89,7 @@ struct pnerf_field {
   hipEvent_t ev_start = nullptr, ev_enc[2] = {nullptr, nullptr}, ev_mlp[2] = {nullptr, nullptr};
   hipEvent_t ev_end_enc = nullptr, ev_end_mlp = nullptr;
   int32_t* d_totals = nullptr;  // [max_chunks] sample totals of the chunks, + 1 counted total
+  uint32_t* d_queue = nullptr;  // encoding work-queue counters (see DevWork::queue)
   int max_chunks = 0;
   int32_t* h_hyp = nullptr;     // pinned host copy of the per-hypothesis sample counts
   int h_hyp_cap = 0;
@@ -300,6 +301,7 @@ DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id, int slot) {
   w.ray_loss = r.ray_loss[slot];
   w.partial = r.partial[slot];
   w.total = F->d_totals + chunk_id;
+  w.queue = F->d_queue;
   return w;
 }
 
@@ -676,19 +678,15 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     d.dense[l] = (p->dense_coarse_levels && n1 * n1 * n1 <= d.T) ? 1u : 0u;
   }
   d.f16 = p->param_dtype == 1;
-  // level groups of the encoding kernels: two levels each, hashed levels spread
-  // first so that every group (and so every XCD) gets its share of them
+  // work queues of the encoding kernel, one per level: hashed levels first, so
+  // that the first queue of every XCD (queue x of XCD x) holds a hashed table
   {
-    std::vector<int> order;
+    int q = 0;
     for (int l = 0; l < L; ++l)
-      if (!d.dense[l]) order.push_back(l);
+      if (!d.dense[l]) d.q_level[q++] = l;
     for (int l = 0; l < L; ++l)
-      if (d.dense[l]) order.push_back(l);
-    d.n_groups = L / 2;
-    for (int g = 0; g < d.n_groups; ++g) {
-      d.grp_lv[g][0] = order[g];
-      d.grp_lv[g][1] = order[g + d.n_groups];
-    }
+      if (d.dense[l]) d.q_level[q++] = l;
+    for (; q < kMaxLevels; ++q) d.q_level[q] = 0;
   }
   d.density_bias = p->density_bias;
   for (int a = 0; a < 3; ++a) {
@@ -784,6 +782,7 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   F->n_cu = prop.multiProcessorCount;
   F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
   F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg);
+  CF_TRY(hipMalloc(&F->d_queue, sizeof(uint32_t) * kMaxLevels * kQueueStride));
   F->enc_blocks = encode_blocks(d, F->n_cu, 8);
   F->enc_blocks_overlap = encode_blocks(d, F->n_cu, 4);  // leave room for the networks
   F->overlap_chunks = p->overlap_chunks == 0 ? kDefaultOverlapChunks : p->overlap_chunks;
@@ -818,6 +817,7 @@ void pnerf_destroy_field(pnerf_field* F) {
   for (hipEvent_t e : evs)
     if (e) (void)hipEventDestroy(e);
   (void)hipFree(F->d_totals);
+  (void)hipFree(F->d_queue);
   if (F->h_hyp) (void)hipHostFree(F->h_hyp);
   delete F;
 }

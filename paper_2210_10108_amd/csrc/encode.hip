@@ -5,12 +5,8 @@
 // contracts this Jacobian with d loss / d feature, and nothing is re-gathered
 // or scattered).
 //
-// Work split: the levels are partitioned into NG groups of two levels each,
-// and block b works on group b % NG.  Workgroups are dispatched round-robin
-// over the XCDs, so every XCD (own 4 MB L2) serves the same one or two level
-// groups for the whole launch and its L2 holds only those levels' tables.
-// Each sample takes both levels of its group in turn (one position, twice the
-// independent gathers in flight).
+// Work split: one level at a time per work item (see k_encode): every XCD
+// (own 4 MB L2) works on one level table at a time, its home levels first.
 //
 // Two adjacent lanes handle one sample: lane side 0 gathers the four vertices
 // at the cell's lower x, side 1 the four at x + 1.  The two x neighbours of a
@@ -19,8 +15,7 @@
 // bits that the carry of x + 1 flips, the lowest bit for even x.  Each gather
 // instruction so touches about half as many lines as with one lane per sample,
 // and the gather's cost follows the lines, not the instructions.  Each lane
-// blends its half; one lane-pair exchange completes the sums.  Blocks are
-// persistent and stride over the compacted sample array.
+// blends its half; one lane-pair exchange completes the sums.
 //
 // Features are stored SoA, row p = (l % 4) * 2 LPG + (l / 4) * 2 + q for
 // feature q of level l (the order in which the MLP kernels feed them to MFMA),
@@ -31,9 +26,8 @@
 // g = l % 4, row k = 6 (l / 4) + 3 q + a, at ((4 b + g) 6 LPG + k) 32 +
 // s % 32.  Lane group g of the MLP backward kernel reads its 6 LPG rows of a
 // 32-sample tile as one contiguous 384 LPG-byte run (one base, immediate
-// offsets), and the 3 rows of one level and feature fill whole cache lines, so
-// no line is written from two XCDs.  That kernel applies N_l and 1 / extent in
-// fp32.
+// offsets), and the 6 rows of one level fill 3 whole cache lines, so no line
+// is written from two XCDs.  That kernel applies N_l and 1 / extent in fp32.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -219,44 +213,101 @@ __device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, in
 }
 
 // ------------------------------------------------------------------ forward
-// A lane pair: both levels of its group for one sample (the position is
-// computed by both lanes).  Lane side q keeps feature q and its Jacobian row:
-// it adds the partner's half of those to its own, and hands over its half of
-// the other feature.  Outputs are streamed out with non-temporal stores so that
-// they do not displace the level tables from L2.  GRAD: also the Jacobian.
+// Work items: kItem consecutive samples of one level, taken from that level's
+// queue (a counter of the items handed out) by one atomic per block.  Queue q
+// serves level q_level[q], hashed levels first.  Workgroups are dispatched
+// round-robin over the XCDs, so block b runs on XCD b % 8: it starts on its
+// home queues x, x + 8, ... (x = b % 8), one level at a time, so that each
+// XCD's L2 holds one level table at a time, and once those are drained it
+// takes what is left on every other queue in turn.  No XCD idles while
+// another still has work, and blocks that find no free slot at launch and
+// start late only take what is left.  The next item is claimed before the
+// current one is gathered, hiding the atomic's latency.
+constexpr int kXcds = 8;
+constexpr int kPerPair = 2;                      // samples per lane pair and item
+constexpr int kItem = kBlock / 2 * kPerPair;     // samples per work item
+
+__device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
+  return __hip_atomic_fetch_add(queue + q * kQueueStride, 1u, __ATOMIC_RELAXED,
+                                __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// A lane pair's share of level l for the sample at ps (index s): lane side q
+// keeps feature q and its Jacobian row, adding the partner's half of those to
+// its own, and hands over its half of the other feature.  Outputs are
+// streamed out with non-temporal stores so that they do not displace the
+// level tables from L2.  GRAD: also the Jacobian.
+template <bool F16, bool GRAD>
+__device__ __forceinline__ void encode_level(const DevField& f, const DevWork& w, int l,
+                                             const Pos& ps, int s, int side) {
+  float p[8];
+  half_cell<F16, GRAD>(f, l, ps.x, ps.dx, side, p);
+  const float keep = side ? p[1] : p[0];
+  const float give = side ? p[0] : p[1];
+  __builtin_nontemporal_store(keep + lane_pair_swap(give),
+                              w.feat + (int64_t)feat_row(f, l, side) * w.cap + s);
+  if (GRAD) {
+    unsigned short* jr = reinterpret_cast<unsigned short*>(w.jac + jac_index(f, l, side, s));
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      const float jk = side ? p[5 + a] : p[2 + a];
+      const float jg = side ? p[2 + a] : p[5 + a];
+      float v = jk + lane_pair_swap(jg);
+      v = (ps.clamped >> a) & 1u ? 0.0f : v;
+      __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)), jr + 32 * a);
+    }
+  }
+}
+
 template <bool F16, bool GRAD>
 __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWork w) {
-  constexpr int kSamples = kBlock / 2;
+  __shared__ uint32_t s_item[2];
   const int S = *w.total;
-  const int grp = blockIdx.x % f.n_groups;
-  const int stride = gridDim.x / f.n_groups;
-  const int64_t cap = w.cap;
+  const uint32_t n_items = (uint32_t)((S + kItem - 1) / kItem);
+  const int NQ = f.L;
   const int side = threadIdx.x & 1;
-  for (int sb = blockIdx.x / f.n_groups; sb * kSamples < S; sb += stride) {
-    const int s = sb * kSamples + (threadIdx.x >> 1);
-    if (s >= S) break;  // the two lanes of a pair leave together
-    Pos ps = sample_pos(f, b, w, s);
-#pragma unroll
-    for (int li = 0; li < 2; ++li) {
-      const int l = f.grp_lv[grp][li];
-      float p[8];
-      half_cell<F16, GRAD>(f, l, ps.x, ps.dx, side, p);
-      const float keep = side ? p[1] : p[0];
-      const float give = side ? p[0] : p[1];
-      __builtin_nontemporal_store(keep + lane_pair_swap(give),
-                                  w.feat + (int64_t)feat_row(f, l, side) * cap + s);
-      if (GRAD) {
-        unsigned short* jr = reinterpret_cast<unsigned short*>(w.jac + jac_index(f, l, side, s));
-#pragma unroll
-        for (int a = 0; a < 3; ++a) {
-          const float jk = side ? p[5 + a] : p[2 + a];
-          const float jg = side ? p[2 + a] : p[5 + a];
-          float v = jk + lane_pair_swap(jg);
-          v = (ps.clamped >> a) & 1u ? 0.0f : v;
-          __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)), jr + 32 * a);
-        }
+  const int home = (int)(blockIdx.x % kXcds) < NQ ? (int)(blockIdx.x % kXcds) : (int)(blockIdx.x % NQ);
+  int q = home;
+  int visit = 0;  // 0: on the home queues; v > 0: on queue (home + v) % NQ
+  int buf = 0;
+  if (threadIdx.x == 0) s_item[buf] = take_item(w.queue, q);
+  __syncthreads();
+  uint32_t item = s_item[buf];
+  // control flow below is uniform over the block: item, q and visit follow
+  // from the same shared words for every thread
+  while (true) {
+    if (item >= n_items) {  // queue q is drained: the next home queue, else the others in turn
+      if (visit == 0 && q + kXcds < NQ) {
+        q += kXcds;
+      } else {
+        if (visit == NQ) break;
+        ++visit;
+        q = (home + visit) % NQ;
       }
+      buf ^= 1;
+      if (threadIdx.x == 0) s_item[buf] = take_item(w.queue, q);
+      __syncthreads();
+      item = s_item[buf];
+      continue;
     }
+    uint32_t next = 0;
+    if (threadIdx.x == 0) next = take_item(w.queue, q);
+    const int l = f.q_level[q];
+    // the pair's kPerPair samples, kBlock / 2 apart: their gathers are in flight together
+    Pos ps[kPerPair];
+    int si[kPerPair];
+#pragma unroll
+    for (int j = 0; j < kPerPair; ++j) {
+      si[j] = (int)item * kItem + j * (kBlock / 2) + (threadIdx.x >> 1);
+      ps[j] = sample_pos(f, b, w, si[j] < S ? si[j] : S - 1);
+    }
+#pragma unroll
+    for (int j = 0; j < kPerPair; ++j)
+      if (si[j] < S) encode_level<F16, GRAD>(f, w, l, ps[j], si[j], side);  // pairs leave together
+    buf ^= 1;
+    if (threadIdx.x == 0) s_item[buf] = next;
+    __syncthreads();
+    item = s_item[buf];
   }
 }
 
@@ -312,12 +363,10 @@ __global__ __launch_bounds__(kBlock) void k_occupancy(DevField f, uint32_t* bits
 }  // namespace
 
 int encode_blocks(const DevField& f, int n_cu, int per_cu) {
-  // per_cu resident blocks of 256 threads per CU, rounded to a multiple of the
-  // group count and of 8 (XCDs) so that each block keeps its group's XCD
-  int unit = 8;
-  while (unit % f.n_groups) unit += 8;
-  int want = n_cu * per_cu;
-  return ((want + unit - 1) / unit) * unit;
+  // per_cu blocks of 256 threads per CU (the work queues balance whatever is
+  // resident)
+  (void)f;
+  return n_cu * per_cu;
 }
 
 hipError_t launch_encode(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,

@@ -300,6 +300,8 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
     *wc.total = chunk_total;
     wc.off[b.n_rays] = chunk_total;
   }
+  // the encoding of this chunk, next on the stream, starts from empty work queues
+  if (blockIdx.x == 0 && threadIdx.x < kMaxLevels) wc.queue[threadIdx.x * kQueueStride] = 0u;
   for (int q = 0; q < kRaysPerWave; ++q) {
     int ray = wave * kRaysPerWave + q;
     if (ray >= b.n_rays) break;

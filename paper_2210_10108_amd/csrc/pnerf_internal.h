@@ -12,7 +12,7 @@ constexpr int kMaxLevels = 16;
 constexpr int kHidden = 64;
 constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
 constexpr int kMaskWords = 8;      // ReLU-mask words per lane per 64 samples (2 per 16-sample column)
-constexpr int kMaxGroups = 8;      // level groups of the encoding kernels (two levels each)
+constexpr int kQueueStride = 32;   // uint32 words between the encoding's work-queue counters (one cache line)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
 constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
 constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
@@ -69,8 +69,7 @@ struct DevField {
   uint32_t dense[kMaxLevels];   // 1: vertex index i + j n1 + k n1^2
   uint32_t n1[kMaxLevels];      // res + 1
   int32_t f16;                  // table stored as fp16
-  int32_t n_groups;             // level groups (L / 2) of the encoding kernel
-  int32_t grp_lv[kMaxGroups][2];   // the two levels of each group
+  int32_t q_level[kMaxLevels];  // level served by encoding work queue q (hashed levels first)
   const float* table32;         // [L][T][2]
   const __half* table16;        // [L][T][2]
   const WeightUnit* wfwd;       // forward A-operand tiles [kFwdUnits]
@@ -124,6 +123,9 @@ struct DevWork {
   float* feat;                  // [2L][cap] features; after the backward rows 0..5 = torque, force
   __half* jac;                  // [6L][cap] d feature / d pos of every level (fp16)
   int64_t cap;                  // sample capacity (row stride of feat and jac)
+  uint32_t* queue;              // [kMaxLevels * kQueueStride] encoding work-queue counters
+                                // (word q * kQueueStride: items of queue q taken), zeroed by
+                                // k_ray_write before every encoding of the chunk
 };
 
 // ---- launchers (all enqueue on `s`, no synchronisation)
