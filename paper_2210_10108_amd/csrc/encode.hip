@@ -224,7 +224,7 @@ __device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, in
 // start late only take what is left.  The next item is claimed before the
 // current one is gathered, hiding the atomic's latency.
 constexpr int kXcds = 8;
-constexpr int kPerPair = 2;                      // samples per lane pair and item
+constexpr int kPerPair = 3;                      // samples per lane pair and item
 constexpr int kItem = kBlock / 2 * kPerPair;     // samples per work item
 
 __device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
