@@ -89,6 +89,18 @@ __device__ inline Pos sample_pos(const DevField& f, const DevBatch& b, const Dev
   return ps;
 }
 
+// The partner lane's position (lane ^ 1; both lanes active).
+__device__ __forceinline__ Pos pos_pair_swap(const Pos& p) {
+  Pos r;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    r.x[a] = lane_pair_swap(p.x[a]);
+    r.dx[a] = lane_pair_swap(p.dx[a]);
+  }
+  r.clamped = (uint32_t)__float_as_int(lane_pair_swap(__int_as_float((int)p.clamped)));
+  return r;
+}
+
 // Cell of one level: lower corner, interpolation weights, and the table index
 // of corner k (bit 0: x + 1, bit 1: y + 1, bit 2: z + 1).
 struct Cell {
@@ -113,8 +125,10 @@ __device__ __forceinline__ void make_cell(const DevField& f, int l, const float 
   }
 }
 
+// KIND: 0 the level's kind read from the field, 1 dense, 2 hashed.
+template <int KIND>
 __device__ __forceinline__ uint32_t corner_index(const DevField& f, int l, const Cell& c, int k) {
-  const bool dense = f.dense[l] != 0;
+  const bool dense = KIND == 0 ? f.dense[l] != 0 : KIND == 1;
   const uint32_t n1 = f.n1[l];
   const uint32_t sy = dense ? n1 : kPrime1;
   const uint32_t sz = dense ? n1 * n1 : kPrime2;
@@ -144,7 +158,7 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
   make_cell(f, l, x, dx, c);
   float2 v[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, corner_index(f, l, c, k));
+  for (int k = 0; k < 8; ++k) v[k] = vertex<F16>(f, corner_index<0>(f, l, c, k));
   const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
   const float ux = 1.0f - wx, uy = 1.0f - wy, uz = 1.0f - wz;
   float2 r;
@@ -172,15 +186,15 @@ __device__ __forceinline__ float2 level_feature(const DevField& f, int l, const 
 // One lane's half of level l: the four corners with x offset `side`, blended
 // with that side's x weight.  p = (feature_0, feature_1, then when GRAD the
 // half of d feature_q / d pos_a at 2 + 3 q + a).  The halves of the two lanes
-// of a pair add up to the whole cell's values.
-template <bool F16, bool GRAD>
+// of a pair add up to the whole cell's values.  KIND: see corner_index.
+template <bool F16, bool GRAD, int KIND>
 __device__ __forceinline__ void half_cell(const DevField& f, int l, const float x[3],
                                           const float dx[3], int side, float p[8]) {
   Cell c;
   make_cell(f, l, x, dx, c);
   float2 v[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) v[j] = vertex<F16>(f, corner_index(f, l, c, 2 * j + side));
+  for (int j = 0; j < 4; ++j) v[j] = vertex<F16>(f, corner_index<KIND>(f, l, c, 2 * j + side));
   const float wx = c.w[0], wy = c.w[1], wz = c.w[2];
   const float ux = 1.0f - wx, uy = 1.0f - wy, uz = 1.0f - wz;
   const float sx = side ? wx : ux;       // this side's x weight
@@ -224,7 +238,7 @@ __device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, in
 // start late only take what is left.  The next item is claimed before the
 // current one is gathered, hiding the atomic's latency.
 constexpr int kXcds = 8;
-constexpr int kPerPair = 3;                      // samples per lane pair and item
+constexpr int kPerPair = 4;                      // samples per lane pair and item
 constexpr int kItem = kBlock / 2 * kPerPair;     // samples per work item
 
 __device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
@@ -237,11 +251,11 @@ __device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
 // its own, and hands over its half of the other feature.  Outputs are
 // streamed out with non-temporal stores so that they do not displace the
 // level tables from L2.  GRAD: also the Jacobian.
-template <bool F16, bool GRAD>
+template <bool F16, bool GRAD, int KIND>
 __device__ __forceinline__ void encode_level(const DevField& f, const DevWork& w, int l,
                                              const Pos& ps, int s, int side) {
   float p[8];
-  half_cell<F16, GRAD>(f, l, ps.x, ps.dx, side, p);
+  half_cell<F16, GRAD, KIND>(f, l, ps.x, ps.dx, side, p);
   const float keep = side ? p[1] : p[0];
   const float give = side ? p[0] : p[1];
   __builtin_nontemporal_store(keep + lane_pair_swap(give),
@@ -293,17 +307,33 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
     uint32_t next = 0;
     if (threadIdx.x == 0) next = take_item(w.queue, q);
     const int l = f.q_level[q];
-    // the pair's kPerPair samples, kBlock / 2 apart: their gathers are in flight together
+    // the pair's kPerPair samples, kBlock / 2 apart: their gathers are in flight
+    // together.  Positions: lane side computes samples 2 k + side and the pair
+    // exchanges them (all lanes active); an odd last one both lanes compute.
+    const int s0 = (int)item * kItem + (threadIdx.x >> 1);
     Pos ps[kPerPair];
-    int si[kPerPair];
 #pragma unroll
-    for (int j = 0; j < kPerPair; ++j) {
-      si[j] = (int)item * kItem + j * (kBlock / 2) + (threadIdx.x >> 1);
-      ps[j] = sample_pos(f, b, w, si[j] < S ? si[j] : S - 1);
+    for (int k = 0; k < kPerPair / 2; ++k) {
+      const int sm = s0 + (2 * k + side) * (kBlock / 2);
+      const Pos mine = sample_pos(f, b, w, sm < S ? sm : S - 1);
+      const Pos theirs = pos_pair_swap(mine);
+      ps[2 * k] = side ? theirs : mine;
+      ps[2 * k + 1] = side ? mine : theirs;
     }
+    if (kPerPair & 1) {
+      const int sl = s0 + (kPerPair - 1) * (kBlock / 2);
+      ps[kPerPair - 1] = sample_pos(f, b, w, sl < S ? sl : S - 1);
+    }
+    // the level's kind is uniform over the item: one branch, no per-lane selects
+    if (f.dense[l]) {
 #pragma unroll
-    for (int j = 0; j < kPerPair; ++j)
-      if (si[j] < S) encode_level<F16, GRAD>(f, w, l, ps[j], si[j], side);  // pairs leave together
+      for (int j = 0; j < kPerPair; ++j)  // pairs leave together
+        if (s0 + j * (kBlock / 2) < S) encode_level<F16, GRAD, 1>(f, w, l, ps[j], s0 + j * (kBlock / 2), side);
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPerPair; ++j)
+        if (s0 + j * (kBlock / 2) < S) encode_level<F16, GRAD, 2>(f, w, l, ps[j], s0 + j * (kBlock / 2), side);
+    }
     buf ^= 1;
     if (threadIdx.x == 0) s_item[buf] = next;
     __syncthreads();
