@@ -89,15 +89,24 @@ __device__ inline Pos sample_pos(const DevField& f, const DevBatch& b, const Dev
   return ps;
 }
 
-// The partner lane's position (lane ^ 1; both lanes active).
-__device__ __forceinline__ Pos pos_pair_swap(const Pos& p) {
+// The position held by lane ODD of each lane pair, in both lanes of the pair
+// (DPP quad_perm [0,0,2,2] or [1,1,3,3]; all lanes active).
+template <int ODD>
+__device__ __forceinline__ float from_pair_lane(float v) {
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), ODD ? 0xF5 : 0xA0, 0xF, 0xF, false));
+}
+
+template <int ODD>
+__device__ __forceinline__ Pos pos_from_pair_lane(const Pos& p) {
+  auto bc = from_pair_lane<ODD>;
   Pos r;
 #pragma unroll
   for (int a = 0; a < 3; ++a) {
-    r.x[a] = lane_pair_swap(p.x[a]);
-    r.dx[a] = lane_pair_swap(p.dx[a]);
+    r.x[a] = bc(p.x[a]);
+    r.dx[a] = bc(p.dx[a]);
   }
-  r.clamped = (uint32_t)__float_as_int(lane_pair_swap(__int_as_float((int)p.clamped)));
+  r.clamped = (uint32_t)__float_as_int(bc(__int_as_float((int)p.clamped)));
   return r;
 }
 
@@ -240,28 +249,28 @@ __device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, in
 constexpr int kXcds = 8;
 constexpr int kPerPair = 4;                      // samples per lane pair and item
 constexpr int kItem = kBlock / 2 * kPerPair;     // samples per work item
+static_assert((kBlock / 2) % 32 == 0, "a lane-pair step must span whole 32-sample Jacobian blocks");
 
 __device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
   return __hip_atomic_fetch_add(queue + q * kQueueStride, 1u, __ATOMIC_RELAXED,
                                 __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// A lane pair's share of level l for the sample at ps (index s): lane side q
-// keeps feature q and its Jacobian row, adding the partner's half of those to
-// its own, and hands over its half of the other feature.  Outputs are
-// streamed out with non-temporal stores so that they do not displace the
-// level tables from L2.  GRAD: also the Jacobian.
+// A lane pair's share of level l for the sample at ps: lane side q keeps
+// feature q and its Jacobian row, adding the partner's half of those to its
+// own, and hands over its half of the other feature; it stores them at fo
+// (the sample's entry of feature row q) and jo (its Jacobian entry of feature
+// q, axis 0).  Outputs are streamed out with non-temporal stores so that they
+// do not displace the level tables from L2.  GRAD: also the Jacobian.
 template <bool F16, bool GRAD, int KIND>
-__device__ __forceinline__ void encode_level(const DevField& f, const DevWork& w, int l,
-                                             const Pos& ps, int s, int side) {
+__device__ __forceinline__ void encode_level(const DevField& f, int l, const Pos& ps, int side,
+                                             float* fo, unsigned short* jr) {
   float p[8];
   half_cell<F16, GRAD, KIND>(f, l, ps.x, ps.dx, side, p);
   const float keep = side ? p[1] : p[0];
   const float give = side ? p[0] : p[1];
-  __builtin_nontemporal_store(keep + lane_pair_swap(give),
-                              w.feat + (int64_t)feat_row(f, l, side) * w.cap + s);
+  __builtin_nontemporal_store(keep + lane_pair_swap(give), fo);
   if (GRAD) {
-    unsigned short* jr = reinterpret_cast<unsigned short*>(w.jac + jac_index(f, l, side, s));
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
       const float jk = side ? p[5 + a] : p[2 + a];
@@ -307,32 +316,40 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
     uint32_t next = 0;
     if (threadIdx.x == 0) next = take_item(w.queue, q);
     const int l = f.q_level[q];
-    // the pair's kPerPair samples, kBlock / 2 apart: their gathers are in flight
-    // together.  Positions: lane side computes samples 2 k + side and the pair
-    // exchanges them (all lanes active); an odd last one both lanes compute.
+    // the pair's kPerPair samples s0 + j kBlock / 2: their gathers are in flight
+    // together.  Positions: lane side computes samples 2 k + side and both lanes
+    // take each from the lane that computed it (all lanes active); an odd last
+    // one both lanes compute.
     const int s0 = (int)item * kItem + (threadIdx.x >> 1);
     Pos ps[kPerPair];
 #pragma unroll
     for (int k = 0; k < kPerPair / 2; ++k) {
       const int sm = s0 + (2 * k + side) * (kBlock / 2);
       const Pos mine = sample_pos(f, b, w, sm < S ? sm : S - 1);
-      const Pos theirs = pos_pair_swap(mine);
-      ps[2 * k] = side ? theirs : mine;
-      ps[2 * k + 1] = side ? mine : theirs;
+      ps[2 * k] = pos_from_pair_lane<0>(mine);
+      ps[2 * k + 1] = pos_from_pair_lane<1>(mine);
     }
     if (kPerPair & 1) {
       const int sl = s0 + (kPerPair - 1) * (kBlock / 2);
       ps[kPerPair - 1] = sample_pos(f, b, w, sl < S ? sl : S - 1);
     }
+    // output entries of sample s0; sample j is kBlock / 2 entries further along
+    // the feature row and kBlock / 64 Jacobian blocks further (kBlock / 2 is a
+    // multiple of 32)
+    float* fo = w.feat + (int64_t)feat_row(f, l, side) * w.cap + s0;
+    unsigned short* jo = reinterpret_cast<unsigned short*>(w.jac) + jac_index(f, l, side, s0);
+    const int64_t jstep = (int64_t)(kBlock / 64) * 4 * (6 * f.lpg * 32);
     // the level's kind is uniform over the item: one branch, no per-lane selects
     if (f.dense[l]) {
 #pragma unroll
       for (int j = 0; j < kPerPair; ++j)  // pairs leave together
-        if (s0 + j * (kBlock / 2) < S) encode_level<F16, GRAD, 1>(f, w, l, ps[j], s0 + j * (kBlock / 2), side);
+        if (s0 + j * (kBlock / 2) < S)
+          encode_level<F16, GRAD, 1>(f, l, ps[j], side, fo + j * (kBlock / 2), jo + j * jstep);
     } else {
 #pragma unroll
       for (int j = 0; j < kPerPair; ++j)
-        if (s0 + j * (kBlock / 2) < S) encode_level<F16, GRAD, 2>(f, w, l, ps[j], s0 + j * (kBlock / 2), side);
+        if (s0 + j * (kBlock / 2) < S)
+          encode_level<F16, GRAD, 2>(f, l, ps[j], side, fo + j * (kBlock / 2), jo + j * jstep);
     }
     buf ^= 1;
     if (threadIdx.x == 0) s_item[buf] = next;
