@@ -689,6 +689,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     for (; q < kMaxLevels; ++q) d.q_level[q] = 0;
   }
   d.density_bias = p->density_bias;
+  d.bf16_neg1[0] = 0x0000BF80u;  // low half -1, high half 0
+  d.bf16_neg1[1] = 0xBF800000u;  // low half 0, high half -1
   for (int a = 0; a < 3; ++a) {
     d.mn[a] = p->aabb_min[a];
     d.mx[a] = p->aabb_max[a];

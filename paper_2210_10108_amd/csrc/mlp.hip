@@ -9,7 +9,8 @@
 // (|r| <= 2^-17 |x|), and each product is accumulated in fp32 as
 // hi*hi + hi*lo + lo*hi by v_mfma_f32_16x16x32_bf16 (the dropped lo*lo and r
 // terms are about 2^-16 of the product).  The weights are split once at field
-// creation; fp16-stored weights split exactly.
+// creation; fp16-stored weights split exactly.  Activations are split two at a
+// time (split2): two packed converts and two bf16 dot products per pair.
 //
 // Work unit: one wavefront takes a tile of NT * 16 consecutive compacted
 // samples, as NT 16-sample column tiles.  The batch (sample) dimension is the MFMA N
@@ -29,6 +30,8 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 256;  // 4 wavefronts
 constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
@@ -38,15 +41,44 @@ struct Split {
   bf16x8 hi, lo;
 };
 
-// x = hi + lo (+ a remainder below 2^-17 |x|), both parts rounded to nearest.
-__device__ __forceinline__ Split split8(const float v[8]) {
-  Split s;
+// The bf16 pairs (-1, 0) and (0, -1).  They come from the field as data: an
+// inline constant for this instruction's packed bf16 operand is not read the
+// way the compiler encodes it (-1.0 lands in the upper half), so the kernels
+// never let it become one.
+struct SplitK {
+  bf16x2 m0, m1;
+};
+
+__device__ __forceinline__ SplitK split_k(const DevField& f) {
+  return {__builtin_bit_cast(bf16x2, f.bf16_neg1[0]), __builtin_bit_cast(bf16x2, f.bf16_neg1[1])};
+}
+
+// A pair x0, x1 as x = hi + lo (+ a remainder below 2^-17 |x|), both parts
+// rounded to nearest: hi by one packed convert; x - hi, exact in fp32, by one
+// bf16 dot product each (hi . (-1, 0) + x0, hi . (0, -1) + x1); lo by one
+// more packed convert.
+__device__ __forceinline__ void split2(float x0, float x1, const SplitK& k, uint32_t& hi,
+                                       uint32_t& lo) {
+  const bf16x2 h = {(__bf16)x0, (__bf16)x1};
+  const float l0 = __builtin_amdgcn_fdot2_f32_bf16(h, k.m0, x0, false);
+  const float l1 = __builtin_amdgcn_fdot2_f32_bf16(h, k.m1, x1, false);
+  const bf16x2 l = {(__bf16)l0, (__bf16)l1};
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, l);
+}
+
+__device__ __forceinline__ Split split8(const float v[8], const SplitK& k) {
+  u32x4 hw, lw;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const __bf16 h = (__bf16)v[i];
-    s.hi[i] = h;
-    s.lo[i] = (__bf16)(v[i] - (float)h);
+  for (int p = 0; p < 4; ++p) {
+    uint32_t h, l;
+    split2(v[2 * p], v[2 * p + 1], k, h, l);
+    hw[p] = h;
+    lw[p] = l;
   }
+  Split s;
+  s.hi = __builtin_bit_cast(bf16x8, hw);
+  s.lo = __builtin_bit_cast(bf16x8, lw);
   return s;
 }
 
@@ -67,9 +99,42 @@ __device__ __forceinline__ Split load_unit(const WeightUnit* lds, int u, int lan
 
 // B operand of one K step from two accumulator tiles (rows of tile t0 at
 // positions 0..3, of tile t1 at 4..7).
-__device__ __forceinline__ Split pack2(const floatx4& t0, const floatx4& t1) {
+__device__ __forceinline__ Split pack2(const floatx4& t0, const floatx4& t1, const SplitK& k) {
   const float v[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
-  return split8(v);
+  return split8(v, k);
+}
+
+// The same for a ReLU layer: the B operand of relu(t0), relu(t1) and, when
+// MASK, its mask bits.  Position v of the K step is value pair p = v / 2:
+// the pair's bits are at shift + p (even v) and shift + p + 16 (odd v) of mk.
+// max(bits, 0) as a signed integer is the ReLU (every non-positive float, -0
+// included, has a bit pattern <= 0); a unit counts as active when its hi part
+// is nonzero, which differs from x > 0 only for positive values below
+// 2^-133.  Both halves of the packed hi are then below 0x8000, so adding
+// 0x7FFF to each sets its top bit exactly when it is nonzero, without a carry
+// into the other half.
+template <bool MASK>
+__device__ __forceinline__ Split relu_pack2(const floatx4& t0, const floatx4& t1, const SplitK& k,
+                                            uint32_t& mk, int shift) {
+  float v[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = __int_as_float(max(__float_as_int(v[i]), 0));
+  u32x4 hw, lw;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    uint32_t h, l;
+    split2(v[2 * p], v[2 * p + 1], k, h, l);
+    hw[p] = h;
+    lw[p] = l;
+    if (MASK) {
+      const uint32_t top = h + 0x7FFF7FFFu;  // bits 15 and 31: the halves are nonzero
+      mk |= (top >> (15 - shift - p)) & (0x00010001u << (shift + p));
+    }
+  }
+  Split s;
+  s.hi = __builtin_bit_cast(bf16x8, hw);
+  s.lo = __builtin_bit_cast(bf16x8, lw);
+  return s;
 }
 
 __device__ inline void stage(WeightUnit* lds, const WeightUnit* src, int n_units) {
@@ -86,30 +151,18 @@ __device__ __forceinline__ void sample_dir(const DevWork& w, int s, float d[3]) 
   d[2] = w.rdz[ray];
 }
 
-// ReLU on 4 accumulator tiles of one column tile; bit 4m+i of the mask = unit
-// 16m + 4g + i was active.  Integer arithmetic on the bit patterns keeps it in
-// three vector instructions per value: max(bits, 0) as a signed integer is the
-// ReLU (every non-positive float, -0 included, has a bit pattern <= 0), and
-// min(bits, 1) of the result is its mask bit.
-__device__ __forceinline__ uint32_t relu_mask(floatx4 (&t)[4]) {
-  uint32_t mk = 0;
+// Mask bits of a ReLU layer's 16 values t[m][i] of one column tile (unit
+// 16m + 4g + i): value v = 4m + i is K position v % 8 of K step v / 8, so its
+// bit is base + 4 (v / 8) + (v % 8) / 2, plus 16 for odd v (see relu_pack2).
+__device__ __forceinline__ void apply_mask(floatx4 (&t)[4], uint32_t mk, int base) {
 #pragma unroll
   for (int m = 0; m < 4; ++m)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = max(__float_as_int(t[m][i]), 0);
-      t[m][i] = __int_as_float(r);
-      mk |= min((uint32_t)r, 1u) << (4 * m + i);
+      const int v = 4 * m + i;
+      const int bit = base + 4 * (v / 8) + (v % 8) / 2 + 16 * (v & 1);
+      if (!((mk >> bit) & 1u)) t[m][i] = 0.0f;
     }
-  return mk;
-}
-
-__device__ __forceinline__ void apply_mask(floatx4 (&t)[4], uint32_t mk) {
-#pragma unroll
-  for (int m = 0; m < 4; ++m)
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (!((mk >> (4 * m + i)) & 1u)) t[m][i] = 0.0f;
 }
 
 // Real SH of degree 0..3, the 4 functions 4g..4g+3 (no Condon-Shortley phase).
@@ -192,6 +245,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const int n_waves = gridDim.x * (kBlock / 64);
   const float* frow = w.feat + (int64_t)(g * KD) * w.cap;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  const SplitK sk = split_k(f);
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
     Split xf[NT];
@@ -205,7 +259,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       float v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = j < KD ? frow[(int64_t)j * w.cap + sc] : 0.0f;
-      xf[nt] = split8(v);
+      xf[nt] = split8(v, sk);
       float d[3];
       sample_dir(w, sc, d);
       sh4(d, g, shv[nt]);
@@ -218,10 +272,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[nt][m] = mfma3(a, xf[nt], zero);
     }
-    uint32_t mk_a[NT], mk_b1[NT], mk_b2[NT];
+    // mask words: layer a at base 0 and colour layer 1 at base 8 of word 0,
+    // colour layer 2 at base 0 of word 1 (bit layout: relu_pack2)
+    uint32_t mw0[NT], mw1[NT];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) mk_a[nt] = relu_mask(acc[nt]);
-    // density layer 2: h = W_d2^T a (16 outputs)
+    for (int nt = 0; nt < NT; ++nt) mw0[nt] = mw1[nt] = 0u;
+    // density layer 2: h = W_d2^T relu(a) (16 outputs)
     floatx4 h[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) h[nt] = zero;
@@ -230,7 +286,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       const Split a = load_unit(lds, kFD2 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        h[nt] = mfma3(a, pack2(acc[nt][2 * s2], acc[nt][2 * s2 + 1]), h[nt]);
+        h[nt] = mfma3(a, relu_pack2<GRAD>(acc[nt][2 * s2], acc[nt][2 * s2 + 1], sk, mw0[nt], 4 * s2),
+                      h[nt]);
     }
     // colour layer 1 on [h (h_0 has zero weights), SH_16]
     floatx4 b1[NT][4];
@@ -240,7 +297,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       for (int nt = 0; nt < NT; ++nt) {
         const float v[8] = {h[nt][0], h[nt][1], h[nt][2], h[nt][3],
                             shv[nt][0], shv[nt][1], shv[nt][2], shv[nt][3]};
-        xc[nt] = split8(v);
+        xc[nt] = split8(v, sk);
       }
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
@@ -249,9 +306,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         for (int nt = 0; nt < NT; ++nt) b1[nt][m] = mfma3(a, xc[nt], zero);
       }
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) mk_b1[nt] = relu_mask(b1[nt]);
-    // colour layer 2
+    // colour layer 2 on relu(b1)
     floatx4 b2[NT][4];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -261,7 +316,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int s2 = 0; s2 < 2; ++s2) {
       Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(b1[nt][2 * s2], b1[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt)
+        x[nt] = relu_pack2<GRAD>(b1[nt][2 * s2], b1[nt][2 * s2 + 1], sk, mw0[nt], 8 + 4 * s2);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kFC2 + 2 * m + s2, lane);
@@ -269,9 +325,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
         for (int nt = 0; nt < NT; ++nt) b2[nt][m] = mfma3(a, x[nt], b2[nt][m]);
       }
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) mk_b2[nt] = relu_mask(b2[nt]);
-    // colour layer 3 (3 outputs in rows 0..2)
+    // colour layer 3 on relu(b2) (3 outputs in rows 0..2)
     floatx4 z[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) z[nt] = zero;
@@ -280,7 +334,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       const Split a = load_unit(lds, kFC3 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        z[nt] = mfma3(a, pack2(b2[nt][2 * s2], b2[nt][2 * s2 + 1]), z[nt]);
+        z[nt] = mfma3(a, relu_pack2<GRAD>(b2[nt][2 * s2], b2[nt][2 * s2 + 1], sk, mw1[nt], 4 * s2),
+                      z[nt]);
     }
     // outputs: rows 0..3 live in lane group 0
 #pragma unroll
@@ -298,8 +353,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        mw[(2 * nt) * 64] = mk_a[nt] | (mk_b1[nt] << 16);
-        mw[(2 * nt + 1) * 64] = mk_b2[nt];
+        mw[(2 * nt) * 64] = mw0[nt];
+        mw[(2 * nt + 1) * 64] = mw1[nt];
       }
     }
   }
@@ -323,19 +378,20 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   const int n_waves = gridDim.x * (kBlock / 64);
   const bool dir_grad = f.sh_dir_grad != 0;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  const SplitK sk = split_k(f);
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
     // the weight units are re-read from LDS every tile: hoisted out of the
     // loop they would pin ~150 registers and cap occupancy at 1 wave/SIMD
     asm volatile("" ::: "memory");
     const uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
-    uint32_t mk_a[NT], mk_b1[NT], mk_b2[NT];
+    // word 0: density layer 1 (base 0) and colour layer 1 (base 8); word 1:
+    // colour layer 2 (base 0)
+    uint32_t mw0[NT], mw1[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint32_t v = mw[(2 * nt) * 64];
-      mk_a[nt] = v & 0xFFFFu;
-      mk_b1[nt] = v >> 16;
-      mk_b2[nt] = mw[(2 * nt + 1) * 64];
+      mw0[nt] = mw[(2 * nt) * 64];
+      mw1[nt] = mw[(2 * nt + 1) * 64];
     }
     // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
     // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
@@ -357,7 +413,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
           const float* c3 = s_c3 + 3 * (16 * m + 4 * g + i);
           gb2[nt][m][i] = c3[0] * z0 + c3[1] * z1 + c3[2] * z2;
         }
-      apply_mask(gb2[nt], mk_b2[nt]);
+      apply_mask(gb2[nt], mw1[nt], 0);
     }
     // colour layer 2 transposed
     floatx4 gb1[NT][4];
@@ -369,7 +425,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     for (int s2 = 0; s2 < 2; ++s2) {
       Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1], sk);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kBC2 + 2 * m + s2, lane);
@@ -378,7 +434,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) apply_mask(gb1[nt], mk_b1[nt]);
+    for (int nt = 0; nt < NT; ++nt) apply_mask(gb1[nt], mw0[nt], 8);
     // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
     floatx4 gh[NT], gsh[NT];
 #pragma unroll
@@ -387,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     for (int s2 = 0; s2 < 2; ++s2) {
       Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1], sk);
       const Split a = load_unit(lds, kBC1 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
@@ -404,7 +460,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     {
       Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gh[nt], zero);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gh[nt], zero, sk);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const Split a = load_unit(lds, kBD2 + m, lane);
@@ -413,7 +469,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       }
     }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) apply_mask(ga[nt], mk_a[nt]);
+    for (int nt = 0; nt < NT; ++nt) apply_mask(ga[nt], mw0[nt], 0);
     // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
     // level 4 (2 mm + i / 2) + g, so lane group g gets its own levels
     floatx4 gf[MD][NT];
@@ -425,7 +481,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     for (int s2 = 0; s2 < 2; ++s2) {
       Split x[NT];
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1]);
+      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1], sk);
 #pragma unroll
       for (int mm = 0; mm < MD; ++mm) {
         const Split a = load_unit(lds, kBD1 + 2 * mm + s2, lane);

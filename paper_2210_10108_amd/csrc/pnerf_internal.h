@@ -78,6 +78,8 @@ struct DevField {
   const float* wd1;             // plain W_d1 [2L][64] and W_d2 [64][16] (occupancy build)
   const float* wd2;
   float density_bias;
+  uint32_t bf16_neg1[2];        // bf16 pairs (-1, 0) and (0, -1): the MLP kernels' split
+                                // multipliers, read as data (see split2 in mlp.hip)
   float mn[3], mx[3], inv_ext[3];
   float inv_ext_err[3];         // inv_ext * extent - 1 (relative rounding of the reciprocal)
   int32_t march_mode, n_uniform;
