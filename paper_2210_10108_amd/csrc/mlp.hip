@@ -33,7 +33,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlock = 256;  // 4 wavefronts
+constexpr int kBlock = 512;  // 8 wavefronts: one LDS copy of the weight units serves 8 waves
 constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
 constexpr int kBwdNT = 2;    // and backward
 
