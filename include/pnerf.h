@@ -272,8 +272,11 @@ pnerf_status pnerf_field_inspect(pnerf_field* field, int32_t what, float* dst, i
 pnerf_status pnerf_field_occupancy(pnerf_field* field, uint32_t* bits_host, void* stream);
 
 /* Total number of samples processed by the last render_loss_grad / render /
- * march call on this field (sum over hypothesis chunks; known on the host, so
- * `stream` is not used). */
+ * march call on this field (sum over hypothesis chunks).  When that call planned
+ * its chunks on the host, the count is known there and `stream` is not used;
+ * when it sized its buffer for the worst case (a loss gradient whose every ray
+ * at its sample cap fits the workspace), the count is read from the device on
+ * `stream`, which this call then synchronises. */
 pnerf_status pnerf_field_last_sample_count(pnerf_field* field, int64_t* count, void* stream);
 
 /* Per-kernel timing with HIP events recorded on the call's stream around every

@@ -95,6 +95,7 @@ struct pnerf_field {
   int h_hyp_cap = 0;
   int last_chunks = 0;
   int64_t last_total = 0;
+  const int32_t* last_total_dev = nullptr;  // the last call's total, when only the device holds it
   int64_t budget = 0;
   int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0, enc_blocks_overlap = 0;
   // profiling
@@ -479,6 +480,7 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
                  float* dpose, float* rgb, int64_t* ray_offset, float* t_out, int32_t* j_out,
                  int64_t capacity, hipStream_t s) {
   HIP_TRY(hipSetDevice(F->device));
+  F->last_total_dev = nullptr;
   const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
   if (P > max_rays)
     return fail(PNERF_ERR_CAPACITY, "P=%d rays per hypothesis exceeds %lld", P, (long long)max_rays);
@@ -505,39 +507,52 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
   for (int h0 = 0; h0 < K; h0 += kr) {
     const int hn = std::min(kr, K - h0);
     DevBatch bb = make_batch(hn, poses + (size_t)12 * h0, P, pix + (size_t)P * h0, obs, intr);
-    st = ensure_samples(F, 0, slot_limit, chunk_id + 1, 1, s);  // totals array for the counted batch
+    // A loss gradient whose worst case (every ray at its sample cap) fits one
+    // buffer runs as one chunk in a buffer sized for that worst case: the host
+    // needs no sample totals, so the call never waits for the device.
+    const int64_t worst = (int64_t)hn * P * F->dev.max_per_ray;
+    const bool device_sized = mode == kLossGrad && !pipe && hn == K && worst <= limit &&
+                              worst * per_sample <= kDeviceSizedBytes;
+    // the totals array for the counted batch (and, device-sized, the whole buffer)
+    st = ensure_samples(F, device_sized ? worst : 0, slot_limit, chunk_id + 1, 1, s);
     if (st != PNERF_OK) return st;
     DevWork wb = counted_work(F);
     HIP_TRY(timed(F, "march", s, [&] { return launch_march_count(F->dev, bb, wb, s); }));
-    HIP_TRY(hipMemcpyAsync(F->h_hyp, wb.hyp_total, sizeof(int32_t) * hn, hipMemcpyDeviceToHost, s));
-    HIP_TRY(hipStreamSynchronize(s));
-    // chunks of whole hypotheses: about 1/n_target of the samples each (when
-    // pipelined) and never more than a buffer holds
-    int64_t counted = 0;
-    for (int k = 0; k < hn; ++k) counted += F->h_hyp[k];
-    const bool pipe_here = pipe && hn > 1 && counted >= (int64_t)kMinOverlapSamples;
-    const int64_t cap_c = pipe_here ? slot_limit : limit;
-    const int64_t goal = pipe_here ? (counted + n_target - 1) / n_target : cap_c;
     std::vector<int> cut{0};
-    std::vector<int64_t> sums;
-    int64_t biggest = 0;
-    for (int a = 0; a < hn;) {
-      int64_t sum = 0;
-      int b = a;
-      while (b < hn && sum + F->h_hyp[b] <= cap_c && (sum < goal || b == a)) sum += F->h_hyp[b++];
-      if (b == a)
-        return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace budget "
-                    "holds (%lld)", h0 + a, F->h_hyp[a], (long long)cap_c);
-      cut.push_back(b);
-      sums.push_back(sum);
-      biggest = std::max(biggest, sum);
-      a = b;
+    std::vector<int64_t> sums;  // samples per chunk; -1: the counted total, on the device
+    int64_t counted = 0;
+    bool overlap = false;
+    if (device_sized) {
+      cut.push_back(hn);
+      sums.push_back(-1);
+    } else {
+      HIP_TRY(hipMemcpyAsync(F->h_hyp, wb.hyp_total, sizeof(int32_t) * hn, hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      // chunks of whole hypotheses: about 1/n_target of the samples each (when
+      // pipelined) and never more than a buffer holds
+      for (int k = 0; k < hn; ++k) counted += F->h_hyp[k];
+      const bool pipe_here = pipe && hn > 1 && counted >= (int64_t)kMinOverlapSamples;
+      const int64_t cap_c = pipe_here ? slot_limit : limit;
+      const int64_t goal = pipe_here ? (counted + n_target - 1) / n_target : cap_c;
+      int64_t biggest = 0;
+      for (int a = 0; a < hn;) {
+        int64_t sum = 0;
+        int b = a;
+        while (b < hn && sum + F->h_hyp[b] <= cap_c && (sum < goal || b == a)) sum += F->h_hyp[b++];
+        if (b == a)
+          return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace "
+                      "budget holds (%lld)", h0 + a, F->h_hyp[a], (long long)cap_c);
+        cut.push_back(b);
+        sums.push_back(sum);
+        biggest = std::max(biggest, sum);
+        a = b;
+      }
+      overlap = pipe_here && sums.size() > 1;
+      st = ensure_samples(F, biggest, cap_c, chunk_id + (int)sums.size(), overlap ? 2 : 1, s);
+      if (st != PNERF_OK) return st;
+      wb = counted_work(F);
     }
     const int n_chunks = (int)sums.size();
-    const bool overlap = pipe_here && n_chunks > 1;
-    st = ensure_samples(F, biggest, cap_c, chunk_id + n_chunks, overlap ? 2 : 1, s);
-    if (st != PNERF_OK) return st;
-    wb = counted_work(F);
     hipStream_t se = overlap ? F->s_enc : s, sm = overlap ? F->s_mlp : s;
     if (overlap) {
       HIP_TRY(hipEventRecord(F->ev_start, s));
@@ -587,7 +602,7 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
         }));
         if (overlap) HIP_TRY(hipEventRecord(F->ev_mlp[slot], sm));
       }
-      base += sums[c];
+      base += device_sized ? 0 : sums[c];
     }
     if (overlap) {
       // the caller's stream continues once both internal streams are done
@@ -597,6 +612,7 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       HIP_TRY(hipStreamWaitEvent(s, F->ev_end_mlp, 0));
     }
     grand += counted;
+    F->last_total_dev = device_sized ? wb.total : nullptr;
   }
   F->last_chunks = chunk_id;
   F->last_total = grand;
@@ -945,7 +961,14 @@ pnerf_status pnerf_field_occupancy(pnerf_field* F, uint32_t* bits_host, void* st
 
 pnerf_status pnerf_field_last_sample_count(pnerf_field* F, int64_t* count, void* stream) {
   if (!F || !count) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");
-  (void)stream;
+  if (F->last_total_dev) {  // the call sized its buffer for the worst case: read the total
+    int32_t n = 0;
+    hipStream_t s = (hipStream_t)stream;
+    HIP_TRY(hipMemcpyAsync(&n, F->last_total_dev, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    *count = n;
+    return PNERF_OK;
+  }
   *count = F->last_total;  // counted on the host when the call planned its chunks
   return PNERF_OK;
 }

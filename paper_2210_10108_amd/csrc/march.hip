@@ -290,6 +290,8 @@ __global__ __launch_bounds__(1024) void k_scan_finish(DevBatch b, DevWork w, int
 // batch `wb`), writing their kept samples into the chunk's sample arrays at
 // offset (exclusive offset in the counted batch) - sample_base, and the chunk's
 // ray offsets into wc.off (wc's per-ray arrays start at the chunk's first ray).
+// chunk_total < 0: the chunk is the whole counted batch, whose total the scan
+// left on the device.
 __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork wb,
                                                          DevWork wc, int ray_base,
                                                          int sample_base, int chunk_total,
@@ -297,8 +299,9 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
   int lane = threadIdx.x & 63;
   int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    *wc.total = chunk_total;
-    wc.off[b.n_rays] = chunk_total;
+    const int total = chunk_total >= 0 ? chunk_total : *wb.total;
+    *wc.total = total;
+    wc.off[b.n_rays] = total;
   }
   // the encoding of this chunk, next on the stream, starts from empty work queues
   if (blockIdx.x == 0 && threadIdx.x < kMaxLevels) wc.queue[threadIdx.x * kQueueStride] = 0u;

@@ -17,6 +17,9 @@ constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points teste
 constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
 constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
 constexpr int kMinOverlapSamples = 1 << 16;  // smaller batches run as one chunk
+constexpr int64_t kDeviceSizedBytes = (int64_t)16 << 30;  // worst-case sample buffer a loss
+                                                           // gradient may allocate to skip the
+                                                           // host's read of the sample totals
 constexpr int kReduceParts = 64;      // parts per hypothesis of the reduction (lanes of one wave)
 constexpr int kAdamState = 16;        // Adam state floats per hypothesis: m[6], v[6], n, 3 pads
 

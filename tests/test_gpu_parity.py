@@ -273,6 +273,21 @@ def test_loss_grad_chunked_matches_single_chunk(pn):
     assert np.allclose(l1, l2, rtol=1e-5) and np.allclose(g1, g2, rtol=1e-4, atol=1e-9)
 
 
+def test_loss_grad_device_sized_matches_host_planned(pn):
+    # with room for every ray's sample cap (32 x 1024 samples here) the call
+    # sizes its buffer for that worst case and never reads the totals back; a
+    # budget below the worst case but above the actual total makes the host
+    # read them and plan the same single chunk: same bits, same sample count
+    case = G.make_case("tiny32", K=4, P=256)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr)
+    l1, g1, n1 = run_loss_grad(pn, case, obs)
+    l2, g2, n2 = run_loss_grad(pn, case, obs, max_ws=3_000_000)  # about 21k samples
+    assert n1 == n2 == int(ref["march"][0][-1]) < 32 * 1024
+    assert np.array_equal(l1, l2) and np.array_equal(g1, g2)
+
+
 @pytest.mark.parametrize("chunks", [2, 4, 7])
 def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks):
     # the pipelined loss gradient (encoding of one chunk alongside the networks
