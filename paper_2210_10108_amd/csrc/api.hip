@@ -219,7 +219,7 @@ struct Carver {
 // Per-ray arrays for n_rays rays (one counted batch).  `offc` receives the
 // sample chunks' own exclusive offsets.
 struct RayWs {
-  float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta, *rex, *rey, *rez;
+  float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta, *rex, *rey, *rez, *rsh;
   int32_t *count, *off, *blocksum, *hyp_total;
   int32_t* offc[2];             // per sample buffer: the chunk's own offsets,
   float *ray_loss[2], *partial[2];  // per-ray losses and reduction partials
@@ -239,6 +239,7 @@ size_t carve_rays(int n_rays, int n_hyp, RayWs* r, char* base) {
   x.rex = c.take<float>(R);
   x.rey = c.take<float>(R);
   x.rez = c.take<float>(R);
+  x.rsh = c.take<float>(R * 16);
   x.count = c.take<int32_t>(R);
   x.off = c.take<int32_t>(R + 1);
   x.blocksum = c.take<int32_t>((R + 255) / 256);
@@ -279,6 +280,7 @@ DevWork counted_work(pnerf_field* F) {
   w.rdx = r.rdx; w.rdy = r.rdy; w.rdz = r.rdz;
   w.rtn = r.rtn; w.rtf = r.rtf; w.rdelta = r.rdelta;
   w.rex = r.rex; w.rey = r.rey; w.rez = r.rez;
+  w.rsh = r.rsh;
   w.count = r.count;
   w.off = r.off;
   w.blocksum = r.blocksum;
@@ -295,6 +297,7 @@ DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id, int slot) {
   w.rdx = r.rdx + ray_base; w.rdy = r.rdy + ray_base; w.rdz = r.rdz + ray_base;
   w.rtn = r.rtn + ray_base; w.rtf = r.rtf + ray_base; w.rdelta = r.rdelta + ray_base;
   w.rex = r.rex + ray_base; w.rey = r.rey + ray_base; w.rez = r.rez + ray_base;
+  w.rsh = r.rsh + (size_t)16 * ray_base;
   w.count = r.count + ray_base;
   w.off = r.offc[slot];
   w.blocksum = nullptr;

@@ -161,7 +161,7 @@ __device__ inline int block_exclusive_scan(int c, int* s_wave, int* block_total)
 
 // One thread per ray: ray generation and box clip, stored for the kernels
 // that follow (their float values decide the samples, so they are computed
-// once).  Without an occupancy grid a uniform-mode ray keeps all its
+// once), and the SH basis of the ray's direction for the colour network.  Without an occupancy grid a uniform-mode ray keeps all its
 // candidates, so its count is known here; SCAN then also takes the first
 // level of the offset scan (as k_scan_local does).
 template <bool SCAN>
@@ -177,6 +177,11 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_setup(DevField f, DevBatch b,
     w.rex[ray] = g.de[0];
     w.rey[ray] = g.de[1];
     w.rez[ray] = g.de[2];
+    float sh[16];
+    sh16(g.d, sh);
+    float4* o = reinterpret_cast<float4*>(w.rsh + (size_t)16 * ray);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = make_float4(sh[4 * q], sh[4 * q + 1], sh[4 * q + 2], sh[4 * q + 3]);
     w.rtn[ray] = g.tn;
     w.rtf[ray] = g.tf;
     w.rdelta[ray] = g.delta;

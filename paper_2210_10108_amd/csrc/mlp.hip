@@ -165,35 +165,6 @@ __device__ __forceinline__ void apply_mask(floatx4 (&t)[4], uint32_t mk, int bas
     }
 }
 
-// Real SH of degree 0..3, the 4 functions 4g..4g+3 (no Condon-Shortley phase).
-__device__ inline void sh4(const float d[3], int g, float out[4]) {
-  const float x = d[0], y = d[1], z = d[2];
-  const float C0 = 0.28209479177387814f, C1 = 0.4886025119029199f;
-  const float C2a = 1.0925484305920792f, C2b = 0.31539156525252005f, C2c = 0.5462742152960396f;
-  const float C3a = 0.5900435899266435f, C3b = 2.890611442640554f, C3c = 0.4570457994644658f;
-  const float C3d = 0.3731763325901154f, C3e = 1.445305721320277f;
-  float v[16];
-  v[0] = C0;
-  v[1] = C1 * y;
-  v[2] = C1 * z;
-  v[3] = C1 * x;
-  v[4] = C2a * x * y;
-  v[5] = C2a * y * z;
-  v[6] = C2b * (3.0f * z * z - 1.0f);
-  v[7] = C2a * x * z;
-  v[8] = C2c * (x * x - y * y);
-  v[9] = C3a * y * (3.0f * x * x - y * y);
-  v[10] = C3b * x * y * z;
-  v[11] = C3c * y * (5.0f * z * z - 1.0f);
-  v[12] = C3d * z * (5.0f * z * z - 3.0f);
-  v[13] = C3c * x * (5.0f * z * z - 1.0f);
-  v[14] = C3e * z * (x * x - y * y);
-  v[15] = C3a * x * (x * x - 3.0f * y * y);
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    out[i] = g == 0 ? v[i] : (g == 1 ? v[4 + i] : (g == 2 ? v[8 + i] : v[12 + i]));
-}
-
 // Gradient of SH functions 4g..4g+3 w.r.t. the direction, contracted with gs.
 __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float gd[3]) {
   const float x = d[0], y = d[1], z = d[2];
@@ -248,6 +219,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
   const SplitK sk = split_k(f);
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
+    // the weight units are re-read from LDS every tile (hoisted, they would
+    // take ~160 registers and spill)
+    asm volatile("" ::: "memory");
     Split xf[NT];
     float shv[NT][4];
     int sidx[NT];
@@ -260,9 +234,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = j < KD ? frow[(int64_t)j * w.cap + sc] : 0.0f;
       xf[nt] = split8(v, sk);
-      float d[3];
-      sample_dir(w, sc, d);
-      sh4(d, g, shv[nt]);
+      // SH functions 4g..4g+3 of the sample's ray (sh16, stored per ray)
+      const float4 sh = reinterpret_cast<const float4*>(w.rsh)[4 * w.sray[sc] + g];
+      shv[nt][0] = sh.x;
+      shv[nt][1] = sh.y;
+      shv[nt][2] = sh.z;
+      shv[nt][3] = sh.w;
     }
     // density layer 1: a = relu(W_d1^T feat), 4 row tiles of 16 hidden units
     floatx4 acc[NT][4];
@@ -342,10 +319,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       if (g == 0 && s < S) {
+        // sigmoid with the hardware reciprocal (1 ulp)
         w.sig[s] = __expf(h[nt][0] + f.density_bias);
-        w.cr[s] = 1.0f / (1.0f + __expf(-z[nt][0]));
-        w.cg[s] = 1.0f / (1.0f + __expf(-z[nt][1]));
-        w.cb[s] = 1.0f / (1.0f + __expf(-z[nt][2]));
+        w.cr[s] = __builtin_amdgcn_rcpf(1.0f + __expf(-z[nt][0]));
+        w.cg[s] = __builtin_amdgcn_rcpf(1.0f + __expf(-z[nt][1]));
+        w.cb[s] = __builtin_amdgcn_rcpf(1.0f + __expf(-z[nt][2]));
       }
     }
     if (GRAD) {

@@ -41,6 +41,32 @@ constexpr int kBC2 = 0, kBC1 = 8, kBD2 = 12, kBD1 = 16, kBwdUnits = 20;
 // Cross-lane data movement through DPP (data-parallel primitives of the
 // vector ALU) instead of the LDS crossbar that __shfl goes through.
 
+// Real spherical harmonics of degree 0..3 (16 functions, no Condon-Shortley
+// phase) of the unit direction d: the colour network's view-direction input.
+__device__ inline void sh16(const float d[3], float v[16]) {
+  const float x = d[0], y = d[1], z = d[2];
+  const float C0 = 0.28209479177387814f, C1 = 0.4886025119029199f;
+  const float C2a = 1.0925484305920792f, C2b = 0.31539156525252005f, C2c = 0.5462742152960396f;
+  const float C3a = 0.5900435899266435f, C3b = 2.890611442640554f, C3c = 0.4570457994644658f;
+  const float C3d = 0.3731763325901154f, C3e = 1.445305721320277f;
+  v[0] = C0;
+  v[1] = C1 * y;
+  v[2] = C1 * z;
+  v[3] = C1 * x;
+  v[4] = C2a * x * y;
+  v[5] = C2a * y * z;
+  v[6] = C2b * (3.0f * z * z - 1.0f);
+  v[7] = C2a * x * z;
+  v[8] = C2c * (x * x - y * y);
+  v[9] = C3a * y * (3.0f * x * x - y * y);
+  v[10] = C3b * x * y * z;
+  v[11] = C3c * y * (5.0f * z * z - 1.0f);
+  v[12] = C3d * z * (5.0f * z * z - 3.0f);
+  v[13] = C3c * x * (5.0f * z * z - 1.0f);
+  v[14] = C3e * z * (x * x - y * y);
+  v[15] = C3a * x * (x * x - 3.0f * y * y);
+}
+
 // The value of the partner lane (lane ^ 1).  Both lanes must be active.
 __device__ __forceinline__ float lane_pair_swap(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1 /* quad_perm
@@ -111,6 +137,7 @@ struct DevWork {
   // per ray (SoA)
   float *rdx, *rdy, *rdz, *rtn, *rtf, *rdelta;
   float *rex, *rey, *rez;       // direction correction: exact unit direction - (rdx, rdy, rdz)
+  float* rsh;                   // [n_rays][16] SH basis of each ray's direction (sh16)
   int32_t* count;               // kept samples per ray
   int32_t* off;                 // counted batch: offset inside each 256-ray block;
                                 // sample chunk: [n_rays + 1] exclusive offsets
