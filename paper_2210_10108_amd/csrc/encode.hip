@@ -22,12 +22,14 @@
 // row stride = the workspace sample capacity.  The Jacobian d feature /
 // d pos of every level (pos = x N_l: bounded by the table's value
 // differences, zero along clamped components) is stored in fp16 (rounding
-// below 2^-11 of each entry) in blocks of 32 samples: block b, lane group
-// g = l % 4, row k = 6 (l / 4) + 3 q + a, at ((4 b + g) 6 LPG + k) 32 +
-// s % 32.  Lane group g of the MLP backward kernel reads its 6 LPG rows of a
-// 32-sample tile as one contiguous 384 LPG-byte run (one base, immediate
-// offsets), and the 6 rows of one level fill 3 whole cache lines, so no line
-// is written from two XCDs.  That kernel applies N_l and 1 / extent in fp32.
+// below 2^-11 of each entry), as one 12-byte record per sample and level (the
+// six values d feature_q / d pos_a at 3 q + a), grouped in blocks of 32
+// samples: block b, lane group g = l % 4, level l / 4 of the group, sample
+// s % 32, at ((4 b + g) LPG 32 + (l / 4) 32 + s % 32) 6 halves.  The MLP
+// backward kernel reads each of its samples' records of a lane group with one
+// 12-byte load per level, and the 32 records of one level and block fill 3
+// whole cache lines, so no line is written from two XCDs.  That kernel applies
+// N_l and 1 / extent in fp32.
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -228,11 +230,16 @@ __device__ __forceinline__ int feat_row(const DevField& f, int l, int q) {
   return (l & 3) * 2 * f.lpg + (l >> 2) * 2 + q;
 }
 
-// Index of the Jacobian entry (level l, feature q, axis 0) of sample s; axis a
-// is 32 entries further.
-__device__ __forceinline__ int64_t jac_index(const DevField& f, int l, int q, int64_t s) {
-  const int kg = 6 * f.lpg;  // rows of one lane group
-  return ((s >> 5) * 4 + (l & 3)) * (int64_t)(kg * 32) + (6 * (l >> 2) + 3 * q) * 32 + (s & 31);
+// Index (in 32-bit words) of the Jacobian record of level l and sample s: six
+// fp16 values d feature_q / d pos_a at 3 q + a, three words.
+__device__ __forceinline__ int64_t jac_record(const DevField& f, int l, int64_t s) {
+  const int kg = 6 * f.lpg * 32;  // halves of one lane group's share of a 32-sample block
+  return (((s >> 5) * 4 + (l & 3)) * (int64_t)kg + ((l >> 2) * 32 + (s & 31)) * 6) / 2;
+}
+
+__device__ __forceinline__ uint32_t pack_half2(float lo, float hi) {
+  return (uint32_t)__half_as_ushort(__float2half_rn(lo)) |
+         ((uint32_t)__half_as_ushort(__float2half_rn(hi)) << 16);
 }
 
 // ------------------------------------------------------------------ forward
@@ -258,26 +265,34 @@ __device__ __forceinline__ uint32_t take_item(uint32_t* queue, int q) {
 
 // A lane pair's share of level l for the sample at ps: lane side q keeps
 // feature q and its Jacobian row, adding the partner's half of those to its
-// own, and hands over its half of the other feature; it stores them at fo
-// (the sample's entry of feature row q) and jo (its Jacobian entry of feature
-// q, axis 0).  Outputs are streamed out with non-temporal stores so that they
-// do not displace the level tables from L2.  GRAD: also the Jacobian.
+// own, and hands over its half of the other feature; it stores feature q at fo
+// (the sample's entry of feature row q).  GRAD: lane side 0 also takes the
+// partner's Jacobian row and stores the sample's whole record at jr.  Outputs
+// are streamed out with non-temporal stores so that they do not displace the
+// level tables from L2.
 template <bool F16, bool GRAD, int KIND>
 __device__ __forceinline__ void encode_level(const DevField& f, int l, const Pos& ps, int side,
-                                             float* fo, unsigned short* jr) {
+                                             float* fo, uint32_t* jr) {
   float p[8];
   half_cell<F16, GRAD, KIND>(f, l, ps.x, ps.dx, side, p);
   const float keep = side ? p[1] : p[0];
   const float give = side ? p[0] : p[1];
   __builtin_nontemporal_store(keep + lane_pair_swap(give), fo);
   if (GRAD) {
+    float v[3], o[3];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
       const float jk = side ? p[5 + a] : p[2 + a];
       const float jg = side ? p[2 + a] : p[5 + a];
-      float v = jk + lane_pair_swap(jg);
-      v = (ps.clamped >> a) & 1u ? 0.0f : v;
-      __builtin_nontemporal_store(__half_as_ushort(__float2half_rn(v)), jr + 32 * a);
+      v[a] = jk + lane_pair_swap(jg);
+      v[a] = (ps.clamped >> a) & 1u ? 0.0f : v[a];
+    }
+#pragma unroll
+    for (int a = 0; a < 3; ++a) o[a] = lane_pair_swap(v[a]);  // side 0: feature 1's row
+    if (side == 0) {
+      __builtin_nontemporal_store(pack_half2(v[0], v[1]), jr);
+      __builtin_nontemporal_store(pack_half2(v[2], o[0]), jr + 1);
+      __builtin_nontemporal_store(pack_half2(o[1], o[2]), jr + 2);
     }
   }
 }
@@ -337,8 +352,8 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
     // the feature row and kBlock / 64 Jacobian blocks further (kBlock / 2 is a
     // multiple of 32)
     float* fo = w.feat + (int64_t)feat_row(f, l, side) * w.cap + s0;
-    unsigned short* jo = reinterpret_cast<unsigned short*>(w.jac) + jac_index(f, l, side, s0);
-    const int64_t jstep = (int64_t)(kBlock / 64) * 4 * (6 * f.lpg * 32);
+    uint32_t* jo = reinterpret_cast<uint32_t*>(w.jac) + jac_record(f, l, s0);
+    const int64_t jstep = (int64_t)(kBlock / 64) * 4 * (6 * f.lpg * 32) / 2;  // words
     // the level's kind is uniform over the item: one branch, no per-lane selects
     if (f.dense[l]) {
 #pragma unroll

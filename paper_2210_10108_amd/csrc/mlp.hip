@@ -474,19 +474,26 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     for (int nt = 0; nt < NT; ++nt) {
       const int s = sidx[nt];
       const int sc = s < S ? s : S - 1;
-      // this lane group's rows of the sample's 32-sample Jacobian block
-      const __half* jp = w.jac + ((int64_t)(sc >> 5) * 4 + g) * (6 * LPG * 32) + (sc & 31);
+      // this lane group's Jacobian records of the sample (level 4j + g at
+      // record j): six fp16 values d feature_q / d pos_a at 3 q + a
+      const uint32_t* jp = reinterpret_cast<const uint32_t*>(w.jac) +
+                           (((int64_t)(sc >> 5) * 4 + g) * (6 * LPG * 32) + (sc & 31) * 6) / 2;
       float gx[3] = {0.f, 0.f, 0.f};
 #pragma unroll
       for (int j = 0; j < LPG; ++j) {
         // level 4j + g: d loss / d pos_l = sum_q gf * J, then times N_l
+        const uint32_t* rec = jp + j * (32 * 6 / 2);
+        const uint32_t r[3] = {rec[0], rec[1], rec[2]};
+        float J[6];
+#pragma unroll
+        for (int k = 0; k < 6; ++k)
+          J[k] = __half2float(__ushort_as_half((unsigned short)(r[k / 2] >> (16 * (k % 2)))));
         float gl[3] = {0.f, 0.f, 0.f};
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
           const float gq = gf[j / 2][nt][2 * (j % 2) + q];
 #pragma unroll
-          for (int a = 0; a < 3; ++a)
-            gl[a] += gq * __half2float(jp[(6 * j + 3 * q + a) * 32]);
+          for (int a = 0; a < 3; ++a) gl[a] += gq * J[3 * q + a];
         }
         const float N = (float)f.res[4 * j + g];
 #pragma unroll

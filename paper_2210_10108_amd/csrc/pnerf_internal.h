@@ -153,7 +153,8 @@ struct DevWork {
   float *cr, *cg, *cb;          // colour (forward) -> d loss / d z (after composite)
   uint32_t* masks;              // [column tiles of 16][2][64] ReLU masks
   float* feat;                  // [2L][cap] features; after the backward rows 0..5 = torque, force
-  __half* jac;                  // [6L][cap] d feature / d pos of every level (fp16)
+  __half* jac;                  // [6L][cap] d feature / d pos: 12-byte records per sample and
+                                // level in 32-sample blocks (jac_record in encode.hip)
   int64_t cap;                  // sample capacity (row stride of feat and jac)
   uint32_t* queue;              // [kMaxLevels * kQueueStride] encoding work-queue counters
                                 // (word q * kQueueStride: items of queue q taken), zeroed by
