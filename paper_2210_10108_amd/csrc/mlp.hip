@@ -483,7 +483,9 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       for (int j = 0; j < LPG; ++j) {
         // level 4j + g: d loss / d pos_l = sum_q gf * J, then times N_l
         const uint32_t* rec = jp + j * (32 * 6 / 2);
-        const uint32_t r[3] = {rec[0], rec[1], rec[2]};
+        // read once: non-temporal, so that they do not displace cached data
+        const uint32_t r[3] = {__builtin_nontemporal_load(rec), __builtin_nontemporal_load(rec + 1),
+                               __builtin_nontemporal_load(rec + 2)};
         float J[6];
 #pragma unroll
         for (int k = 0; k < 6; ++k)
