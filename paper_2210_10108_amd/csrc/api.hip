@@ -520,7 +520,10 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
     st = ensure_samples(F, device_sized ? worst : 0, slot_limit, chunk_id + 1, 1, s);
     if (st != PNERF_OK) return st;
     DevWork wb = counted_work(F);
-    HIP_TRY(timed(F, "march", s, [&] { return launch_march_count(F->dev, bb, wb, s); }));
+    int raw_blocks = 0;  // device-sized: the write pass may finish the offset scan itself
+    HIP_TRY(timed(F, "march", s, [&] {
+      return launch_march_count(F->dev, bb, wb, device_sized, &raw_blocks, s);
+    }));
     std::vector<int> cut{0};
     std::vector<int64_t> sums;  // samples per chunk; -1: the counted total, on the device
     int64_t counted = 0;
@@ -573,7 +576,8 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       // inspection: lattice indices go to the (otherwise unused) blue-channel buffer
       int32_t* j_tmp = mode == kMarch ? reinterpret_cast<int32_t*>(w.cb) : nullptr;
       HIP_TRY(timed(F, "march_write", se, [&] {
-        return launch_march_write(F->dev, b, wb, w, a * P, (int)base, (int)sums[c], j_tmp, se);
+        return launch_march_write(F->dev, b, wb, w, a * P, (int)base, (int)sums[c], raw_blocks, j_tmp,
+                                  se);
       }));
       if (mode == kMarch) {
         const bool last = k0 + kn == K;

@@ -296,17 +296,33 @@ __global__ __launch_bounds__(1024) void k_scan_finish(DevBatch b, DevWork w, int
 // offset (exclusive offset in the counted batch) - sample_base, and the chunk's
 // ray offsets into wc.off (wc's per-ray arrays start at the chunk's first ray).
 // chunk_total < 0: the chunk is the whole counted batch, whose total the scan
-// left on the device.
+// left on the device.  RAW: the scan stopped at the raw sums of its
+// raw_blocks (<= 64) blocks, and every wavefront scans them itself (then the
+// chunk is the whole counted batch, and block 0 also stores its total).
+template <bool RAW>
 __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b, DevWork wb,
                                                          DevWork wc, int ray_base,
                                                          int sample_base, int chunk_total,
-                                                         int32_t* j_out) {
+                                                         int raw_blocks, int32_t* j_out) {
   int lane = threadIdx.x & 63;
   int wave = blockIdx.x * (kRayBlock / 64) + (threadIdx.x >> 6);
+  int raw_excl = 0, raw_total = 0;  // RAW: lane i holds the exclusive prefix of block i
+  if (RAW) {
+    const int v = lane < raw_blocks ? wb.blocksum[lane] : 0;
+    int inc = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int x = __shfl_up(inc, d);
+      if (lane >= d) inc += x;
+    }
+    raw_excl = inc - v;
+    raw_total = __shfl(inc, 63);
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    const int total = chunk_total >= 0 ? chunk_total : *wb.total;
+    const int total = RAW ? raw_total : (chunk_total >= 0 ? chunk_total : *wb.total);
     *wc.total = total;
     wc.off[b.n_rays] = total;
+    if (RAW) *wb.total = total;  // the counted batch's total (read back on demand)
   }
   // the encoding of this chunk, next on the stream, starts from empty work queues
   if (blockIdx.x == 0 && threadIdx.x < kMaxLevels) wc.queue[threadIdx.x * kQueueStride] = 0u;
@@ -314,7 +330,8 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
     int ray = wave * kRaysPerWave + q;
     if (ray >= b.n_rays) break;
     int rb = ray_base + ray;
-    int o = wb.blocksum[rb / kScanBlock] + wb.off[rb] - sample_base;
+    const int before = RAW ? __shfl(raw_excl, rb / kScanBlock) : wb.blocksum[rb / kScanBlock];
+    int o = before + wb.off[rb] - sample_base;
     int n = wc.count[ray];
     if (lane == 0) wc.off[ray] = o;
     if (n == 0) continue;
@@ -325,14 +342,19 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
 
 }  // namespace
 
-hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w,
-                              hipStream_t s) {
+hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w, bool raw_ok,
+                              int* raw_blocks, hipStream_t s) {
   const int n_scan = (b.n_rays + kScanBlock - 1) / kScanBlock;
   if (n_scan > kMaxScanBlocks) return hipErrorInvalidValue;
   const int n_setup = (b.n_rays + kRayBlock - 1) / kRayBlock;
+  *raw_blocks = 0;
   if (f.march_mode == 0 && f.occ_res <= 0) {
     // counts known at set-up: the first scan level runs in the same kernel
     hipLaunchKernelGGL(k_ray_setup<true>, dim3(n_setup), dim3(kRayBlock), 0, s, f, b, w);
+    if (raw_ok && n_scan <= kMaxRawScanBlocks) {  // the write pass scans the block sums
+      *raw_blocks = n_scan;
+      return hipGetLastError();
+    }
   } else {
     hipLaunchKernelGGL(k_ray_setup<false>, dim3(n_setup), dim3(kRayBlock), 0, s, f, b, w);
     const int rays_per_block = kRaysPerWave * (kRayBlock / 64);
@@ -346,11 +368,17 @@ hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWor
 
 hipError_t launch_march_write(const DevField& f, const DevBatch& b, const DevWork& wb,
                               const DevWork& wc, int ray_base, int sample_base, int chunk_total,
-                              int32_t* lattice_j_out, hipStream_t s) {
+                              int raw_blocks, int32_t* lattice_j_out, hipStream_t s) {
   int rays_per_block = kRaysPerWave * (kRayBlock / 64);
   int n_march = (b.n_rays + rays_per_block - 1) / rays_per_block;
-  hipLaunchKernelGGL(k_ray_write, dim3(n_march), dim3(kRayBlock), 0, s, f, b, wb, wc, ray_base,
-                     sample_base, chunk_total, lattice_j_out);
+  if (raw_blocks > kMaxRawScanBlocks || (raw_blocks > 0 && (ray_base != 0 || sample_base != 0)))
+    return hipErrorInvalidValue;
+  if (raw_blocks > 0)
+    hipLaunchKernelGGL(k_ray_write<true>, dim3(n_march), dim3(kRayBlock), 0, s, f, b, wb, wc,
+                       ray_base, sample_base, chunk_total, raw_blocks, lattice_j_out);
+  else
+    hipLaunchKernelGGL(k_ray_write<false>, dim3(n_march), dim3(kRayBlock), 0, s, f, b, wb, wc,
+                       ray_base, sample_base, chunk_total, 0, lattice_j_out);
   return hipGetLastError();
 }
 

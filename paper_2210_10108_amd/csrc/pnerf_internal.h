@@ -15,6 +15,7 @@ constexpr int kMaskWords = 8;      // ReLU-mask words per lane per 64 samples (2
 constexpr int kQueueStride = 32;   // uint32 words between the encoding's work-queue counters (one cache line)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
 constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
+constexpr int kMaxRawScanBlocks = 64;  // block sums the write pass may scan itself (one wavefront)
 constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
 constexpr int kMinOverlapSamples = 1 << 16;  // smaller batches run as one chunk
 constexpr int64_t kDeviceSizedBytes = (int64_t)16 << 30;  // worst-case sample buffer a loss
@@ -162,11 +163,13 @@ struct DevWork {
 };
 
 // ---- launchers (all enqueue on `s`, no synchronisation)
-hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w,
-                              hipStream_t s);
+// raw_ok: the caller lets the write pass scan up to kMaxRawScanBlocks raw block
+// sums itself; returns (in *raw_blocks) how many it left raw (0: scanned here)
+hipError_t launch_march_count(const DevField& f, const DevBatch& b, const DevWork& w, bool raw_ok,
+                              int* raw_blocks, hipStream_t s);
 hipError_t launch_march_write(const DevField& f, const DevBatch& b, const DevWork& wb,
                               const DevWork& wc, int ray_base, int sample_base, int chunk_total,
-                              int32_t* lattice_j_out, hipStream_t s);
+                              int raw_blocks, int32_t* lattice_j_out, hipStream_t s);
 hipError_t launch_encode(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                          int with_grad, hipStream_t s);
 hipError_t launch_mlp_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
