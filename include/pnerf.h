@@ -276,7 +276,8 @@ pnerf_status pnerf_field_occupancy(pnerf_field* field, uint32_t* bits_host, void
  * its chunks on the host, the count is known there and `stream` is not used;
  * when it sized its buffer for the worst case (a loss gradient whose every ray
  * at its sample cap fits the workspace), the count is read from the device on
- * `stream`, which this call then synchronises. */
+ * `stream`, which this call then synchronises: pass the stream of that call
+ * (or one ordered after it). */
 pnerf_status pnerf_field_last_sample_count(pnerf_field* field, int64_t* count, void* stream);
 
 /* Per-kernel timing with HIP events recorded on the call's stream around every
