@@ -331,10 +331,14 @@ __global__ __launch_bounds__(kBlock) void k_encode(DevField f, DevBatch b, DevWo
     uint32_t next = 0;
     if (threadIdx.x == 0) next = take_item(w.queue, q);
     const int l = f.q_level[q];
-    // the pair's kPerPair samples s0 + j kBlock / 2: their gathers are in flight
-    // together.  Positions: lane side computes samples 2 k + side and both lanes
-    // take each from the lane that computed it (all lanes active); an odd last
-    // one both lanes compute.
+    // the pair's kPerPair samples s0 + j kBlock / 2.  The bounds test makes each
+    // sample a block of code of its own, so a wavefront gathers its samples one
+    // after the other (4 loads in flight) and the 7-8 resident wavefronts per
+    // SIMD overlap each other's waits; issuing all 16 loads at once doubles the
+    // registers, halves the resident wavefronts and is slower, since the CU's
+    // L1 already holds as many L2 misses in flight as it can.  Positions: lane
+    // side computes samples 2 k + side and both lanes take each from the lane
+    // that computed it (all lanes active); an odd last one both lanes compute.
     const int s0 = (int)item * kItem + (threadIdx.x >> 1);
     Pos ps[kPerPair];
 #pragma unroll
