@@ -4,8 +4,8 @@
 //
 // One wavefront per ray; 64 samples per step.  Transmittance comes from a
 // wavefront prefix sum of sigma*delta carried across steps; the backward pass
-// re-sweeps the ray and takes the colour still to come behind sample i as
-// C - (prefix of w c up to i).
+// re-sweeps the ray (keeping the first two steps from the forward sweep) and
+// takes the colour still to come behind sample i as C - (prefix of w c up to i).
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -73,16 +73,30 @@ struct Chunk {
   bool stop_here;
 };
 
+// One lane's sample of a 64-sample step: density and colour (zero past the
+// ray's end).
+struct Raw {
+  float sig, c[3];
+};
+
+__device__ __forceinline__ Raw load_raw(const DevWork& w, int base, int n, int i0, int lane) {
+  Raw r;
+  const int i = i0 + lane;
+  const bool valid = i < n;
+  r.sig = valid ? w.sig[base + i] : 0.0f;
+  r.c[0] = valid ? w.cr[base + i] : 0.0f;
+  r.c[1] = valid ? w.cg[base + i] : 0.0f;
+  r.c[2] = valid ? w.cb[base + i] : 0.0f;
+  return r;
+}
+
 // Evaluate one 64-sample step of a ray: transmittance in and out, weight.
-__device__ inline Chunk step_chunk(const DevField& f, const DevWork& w, int base, int n, int i0,
-                                   float delta, float carry, int lane, float& incl_out) {
+__device__ inline Chunk make_chunk(const DevField& f, const Raw& r, bool valid, float delta,
+                                   float carry, float& incl_out) {
   Chunk ch;
-  int i = i0 + lane;
-  bool valid = i < n;
-  ch.sig = valid ? w.sig[base + i] : 0.0f;
-  ch.c[0] = valid ? w.cr[base + i] : 0.0f;
-  ch.c[1] = valid ? w.cg[base + i] : 0.0f;
-  ch.c[2] = valid ? w.cb[base + i] : 0.0f;
+  ch.sig = r.sig;
+#pragma unroll
+  for (int q = 0; q < 3; ++q) ch.c[q] = r.c[q];
   ch.tau = ch.sig * delta;
   float incl = wave_incl_scan(ch.tau) + carry;
   incl_out = incl;
@@ -95,6 +109,11 @@ __device__ inline Chunk step_chunk(const DevField& f, const DevWork& w, int base
   return ch;
 }
 
+__device__ inline Chunk step_chunk(const DevField& f, const DevWork& w, int base, int n, int i0,
+                                   float delta, float carry, int lane, float& incl_out) {
+  return make_chunk(f, load_raw(w, base, n, i0, lane), i0 + lane < n, delta, carry, incl_out);
+}
+
 template <int WITH_GRAD>
 __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, DevWork w,
                                                       float* rgb_out) {
@@ -104,19 +123,37 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   const int base = w.off[ray];
   const int n = w.off[ray + 1] - base;
   const float delta = w.rdelta[ray];
+  // the observed pixel, loaded before the sweeps so that its two dependent
+  // loads overlap them
+  float y[3] = {0.f, 0.f, 0.f};
+  if (WITH_GRAD) {
+    int pix = b.pix[ray];
+    const int n_pix = b.W * b.H;
+    pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);
+    const float* I = b.obs + 3 * (size_t)pix;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) y[q] = I[q];
+  }
 
-  // pass 1: colour, transmittance, stop index
+  // pass 1: colour, transmittance, stop index.  The first two steps' samples
+  // are loaded together up front, and both steps are kept for pass 2, which
+  // would compute them again from the same carry.
   float C[3] = {0.f, 0.f, 0.f};
   float carry = 0.0f;
   int n_used = n;
-  Chunk first{};          // the ray's first step, reused by pass 2
-  float first_incl = 0.0f;
+  const Raw r0 = load_raw(w, base, n, 0, lane), r1 = load_raw(w, base, n, 64, lane);
+  Chunk first{}, second{};  // the ray's first two steps, reused by pass 2
+  float first_incl = 0.0f, second_incl = 0.0f;
   for (int i0 = 0; i0 < n_used; i0 += 64) {
     float incl;
-    Chunk ch = step_chunk(f, w, base, n, i0, delta, carry, lane, incl);
+    const Raw r = i0 == 0 ? r0 : (i0 == 64 ? r1 : load_raw(w, base, n, i0, lane));
+    Chunk ch = make_chunk(f, r, i0 + lane < n, delta, carry, incl);
     if (i0 == 0) {
       first = ch;
       first_incl = incl;
+    } else if (i0 == 64) {
+      second = ch;
+      second_incl = incl;
     }
     uint64_t st = __ballot(ch.stop_here);
     int last = 63;
@@ -139,15 +176,11 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
   }
 
   // loss on the observed pixel: mean over the P pixels and 3 channels
-  int pix = b.pix[ray];
-  const int n_pix = b.W * b.H;
-  pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);
-  const float* I = b.obs + 3 * (size_t)pix;
   const float norm = 1.0f / (3.0f * (float)b.P);
   float gC[3], L = 0.0f;
   for (int q = 0; q < 3; ++q) {
     float gq;
-    L += pixel_loss(f.loss_type, C[q], I[q], f.loss_param, gq);
+    L += pixel_loss(f.loss_type, C[q], y[q], f.loss_param, gq);
     gC[q] = gq * norm;
   }
   if (lane == 0) w.ray_loss[ray] = L * norm;
@@ -166,8 +199,10 @@ __global__ __launch_bounds__(kBlock) void k_composite(DevField f, DevBatch b, De
       }
       continue;
     }
-    float incl = first_incl;
-    Chunk ch = i0 == 0 ? first : step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
+    float incl = i0 == 0 ? first_incl : second_incl;
+    Chunk ch = i0 == 0    ? first
+               : i0 == 64 ? second
+                          : step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
     bool use = ch.live && i < n_used;
     float gs = 0.0f, gz[3];
 #pragma unroll
