@@ -326,17 +326,29 @@ __global__ __launch_bounds__(kRayBlock) void k_ray_write(DevField f, DevBatch b,
   }
   // the encoding of this chunk, next on the stream, starts from empty work queues
   if (blockIdx.x == 0 && threadIdx.x < kMaxLevels) wc.queue[threadIdx.x * kQueueStride] = 0u;
+  // every load the wavefront's rays need is issued before the first is
+  // marched (a ray past the end loads the last ray's values and is skipped);
+  // each wavefront reads only its own rays' offsets, which it then overwrites
+  int off[kRaysPerWave], cnt[kRaysPerWave];
+  RayGeom geo[kRaysPerWave];
+#pragma unroll
   for (int q = 0; q < kRaysPerWave; ++q) {
-    int ray = wave * kRaysPerWave + q;
-    if (ray >= b.n_rays) break;
-    int rb = ray_base + ray;
+    const int ray = wave * kRaysPerWave + q;
+    const int rc = ray < b.n_rays ? ray : b.n_rays - 1;
+    const int rb = ray_base + rc;
     const int before = RAW ? __shfl(raw_excl, rb / kScanBlock) : wb.blocksum[rb / kScanBlock];
-    int o = before + wb.off[rb] - sample_base;
-    int n = wc.count[ray];
+    off[q] = before + wb.off[rb] - sample_base;
+    cnt[q] = wc.count[rc];
+    geo[q] = stored_ray(b, wc, rc);
+  }
+#pragma unroll
+  for (int q = 0; q < kRaysPerWave; ++q) {
+    const int ray = wave * kRaysPerWave + q;
+    if (ray >= b.n_rays) break;
+    const int o = off[q], n = cnt[q];
     if (lane == 0) wc.off[ray] = o;
     if (n == 0) continue;
-    const RayGeom g = stored_ray(b, wc, ray);
-    march_wave<true>(f, g, lane, n, wc.t + o, j_out ? j_out + o : nullptr, wc.sray + o, ray);
+    march_wave<true>(f, geo[q], lane, n, wc.t + o, j_out ? j_out + o : nullptr, wc.sray + o, ray);
   }
 }
 
