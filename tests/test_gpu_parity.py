@@ -196,15 +196,25 @@ def test_loss_grad_pixel_losses(pn, loss_type, param):
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
-def test_loss_grad_early_stop_and_occupancy(pn):
+# (steps per box diagonal, density bias, range of the stop indices the case
+# must contain): the compositing kernel takes 64 samples per step and keeps
+# the first two steps for its backward sweep, so stops fall in the first step,
+# in the second, and later (with longer rays that never stop beside them)
+@pytest.mark.parametrize("div,bias,stops", [(96, 3.0, (0, 64)), (384, 2.5, (64, 128)),
+                                            (768, 2.5, (128, 10**9))])
+def test_loss_grad_early_stop_and_occupancy(pn, div, bias, stops):
     R = 16
-    case = G.make_case("tiny32", K=3, P=200, march_mode=1, step=math.sqrt(3) / 96,
-                       max_samples=200, t_stop=1e-2, occ_res=R, density_bias=3.0,
+    case = G.make_case("tiny32", K=3, P=200, march_mode=1, step=math.sqrt(3) / div,
+                       max_samples=600, t_stop=1e-2, occ_res=R, density_bias=bias,
                        occ_bits=synth.occupancy_pattern("sphere", R), background=(0.5, 0.2, 0.9))
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    assert np.any(ref["stop"] < np.diff(ref["march"][0]))
+    cnt = np.diff(ref["march"][0])
+    stopped = ref["stop"] < cnt
+    assert np.sum(stopped & (ref["stop"] >= stops[0]) & (ref["stop"] < stops[1])) >= 5
+    if stops[0] >= 128:
+        assert np.sum(~stopped & (cnt > 128)) >= 5
     check_full(pn, case, obs, ref)
 
 
