@@ -188,7 +188,7 @@ Units build_bwd_units(const Weights& W, int lpg) {
         const int o = kpos(s2, g, j);  // the layer's output unit (K of the transpose)
         for (int m = 0; m < 4; ++m) U.put(kBC2 + 2 * m + s2, lane, j, W.C2(16 * m + r, o));
         U.put(kBC1 + s2, lane, j, r >= 1 ? W.C1(r - 1, o) : 0.0f);  // h rows
-        U.put(kBC1 + 2 + s2, lane, j, W.C1(15 + r, o));              // SH rows
+        U.put(kBSH + s2, lane, j, W.C1(15 + r, o));                  // SH rows
         // density 1: row r = feature (r % 4) % 2 of level 4 (2 mm + (r % 4) / 2) + r / 4
         for (int mm = 0; mm < MD; ++mm) {
           const int jl = 2 * mm + (r % 4) / 2;
@@ -806,7 +806,7 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   CF_TRY(hipGetDeviceProperties(&prop, F->device));
   F->n_cu = prop.multiProcessorCount;
   F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
-  F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg);
+  F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad);
   CF_TRY(hipMalloc(&F->d_queue, sizeof(uint32_t) * kMaxLevels * kQueueStride));
   F->enc_blocks = encode_blocks(d, F->n_cu, 8);
   F->enc_blocks_overlap = encode_blocks(d, F->n_cu, 4);  // leave room for the networks

@@ -339,13 +339,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 }
 
 // ----------------------------------------------------------------- backward
-template <int LPG>
+// DIR: the SH direction path (sh_dir_grad) is on; without it the SH rows of
+// colour layer 1 are not staged, and four blocks fit a CU's LDS.
+template <int LPG, bool DIR>
 __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevWork w) {
   constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
   constexpr int NT = kBwdNT, TS = 16 * NT;
-  __shared__ WeightUnit lds[kBwdUnits];
+  constexpr int NU = DIR ? kBwdUnits : kBSH;  // staged weight units
+  __shared__ WeightUnit lds[NU];
   __shared__ float s_c3[64 * 3];
-  stage(lds, f.wbwd, kBwdUnits);
+  stage(lds, f.wbwd, NU);
   for (int i = threadIdx.x; i < 64 * 3; i += kBlock) s_c3[i] = f.wc3[i];
   __syncthreads();
 
@@ -354,7 +357,6 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
-  const bool dir_grad = f.sh_dir_grad != 0;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   const SplitK sk = split_k(f);
 
@@ -425,8 +427,8 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       const Split a = load_unit(lds, kBC1 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
-      if (dir_grad) {
-        const Split a2 = load_unit(lds, kBC1 + 2 + s2, lane);
+      if (DIR) {
+        const Split a2 = load_unit(lds, kBSH + s2, lane);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) gsh[nt] = mfma3(a2, x[nt], gsh[nt]);
       }
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
       float gd[3] = {0.f, 0.f, 0.f};
       float d[3];
       sample_dir(w, sc, d);
-      if (dir_grad) {
+      if (DIR) {
         float gs[4] = {gsh[nt][0], gsh[nt][1], gsh[nt][2], gsh[nt][3]};
         sh4_vjp(d, g, gs, gd);
       }
@@ -553,14 +555,15 @@ int mlp_fwd_blocks_per_cu(int lpg) {
   return e == hipSuccess && n > 0 ? n : 1;
 }
 
-int mlp_bwd_blocks_per_cu(int lpg) {
+int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad) {
   int n = 0;
   hipError_t e = hipErrorInvalidValue;
+  const bool dir = sh_dir_grad != 0;
   switch (lpg) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_bwd<1>, kBlock, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_bwd<2>, kBlock, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_bwd<3>, kBlock, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_bwd<4>, kBlock, 0); break;
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<1, true> : k_mlp_bwd<1, false>, kBlock, 0); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<2, true> : k_mlp_bwd<2, false>, kBlock, 0); break;
+    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<3, true> : k_mlp_bwd<3, false>, kBlock, 0); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<4, true> : k_mlp_bwd<4, false>, kBlock, 0); break;
   }
   return e == hipSuccess && n > 0 ? n : 1;
 }
@@ -588,16 +591,26 @@ hipError_t launch_mlp_fwd(const DevField& f, const DevBatch& b, const DevWork& w
   return hipGetLastError();
 }
 
-hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                          hipStream_t s) {
+namespace {
+template <bool DIR>
+hipError_t launch_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                      hipStream_t s) {
   switch (f.lpg) {
-    case 1: hipLaunchKernelGGL(k_mlp_bwd<1>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 2: hipLaunchKernelGGL(k_mlp_bwd<2>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 3: hipLaunchKernelGGL(k_mlp_bwd<3>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 4: hipLaunchKernelGGL(k_mlp_bwd<4>, dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 1: hipLaunchKernelGGL((k_mlp_bwd<1, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_mlp_bwd<2, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_mlp_bwd<3, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_mlp_bwd<4, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                          hipStream_t s) {
+  if (f.sh_dir_grad)
+    return launch_bwd<true>(f, b, w, n_blocks, s);
+  return launch_bwd<false>(f, b, w, n_blocks, s);
 }
 
 }  // namespace pnerf

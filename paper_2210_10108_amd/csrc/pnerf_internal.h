@@ -34,9 +34,10 @@ struct alignas(16) WeightUnit {
 // unit indices of the forward tiles: density layer 1 (4 row tiles), layer 2
 // (2 K steps), colour layer 1 (4 row tiles), layer 2 (4 x 2), layer 3 (2 K steps)
 constexpr int kFD1 = 0, kFD2 = 4, kFC1 = 6, kFC2 = 10, kFC3 = 18, kFwdUnits = 20;
-// backward (transposed layers): colour 2 (4 x 2), colour 1 (h rows, SH rows) x 2
-// K steps, density 2 (4 row tiles), density 1 (up to 2 row tiles x 2 K steps)
-constexpr int kBC2 = 0, kBC1 = 8, kBD2 = 12, kBD1 = 16, kBwdUnits = 20;
+// backward (transposed layers): colour 2 (4 x 2), colour 1 h rows (2 K steps),
+// density 2 (4 row tiles), density 1 (up to 2 row tiles x 2 K steps), then
+// colour 1 SH rows (2 K steps; staged only when the direction path is on)
+constexpr int kBC2 = 0, kBC1 = 8, kBD2 = 10, kBD1 = 14, kBSH = 18, kBwdUnits = 20;
 
 // ---------------------------------------------------- wavefront primitives
 // Cross-lane data movement through DPP (data-parallel primitives of the
@@ -197,7 +198,7 @@ hipError_t launch_resample(int K, float* poses, float* state, int state_dim, con
 
 int reduce_parts(int K);
 int mlp_fwd_blocks_per_cu(int lpg);
-int mlp_bwd_blocks_per_cu(int lpg);
+int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad);
 int encode_blocks(const DevField& f, int n_cu, int per_cu);
 
 }  // namespace pnerf
