@@ -340,7 +340,8 @@ def main():
     dom_name = max(rooflines, key=lambda k: prof[k]["avg_ms"] * prof[k]["launches"])
     lpg = w.n_levels // 4
     keys = {"encode": f"k_encode<{'true' if w.param_dtype == 'f16' else 'false'}, true>",
-            "mlp_fwd": f"k_mlp_fwd<{lpg}, true>", "mlp_bwd": f"k_mlp_bwd<{lpg}>"}
+            "mlp_fwd": f"k_mlp_fwd<{lpg}, true>",
+            "mlp_bwd": f"k_mlp_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}>"}
     for kname, r in rooflines.items():
         tr = measured_traffic(w.name, keys[kname])
         # HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE), same units as achieved
