@@ -167,15 +167,17 @@ def test_loss_grad_tiny(pn, overrides):
     assert np.abs(ex["gz"][ok] - so[ok, 5:8]).max() <= 1e-3 * np.abs(so[:, 5:8]).max()
 
 
-@pytest.mark.parametrize("n_levels,dense", [(8, 0), (12, 1), (16, 1)])
-def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense):
+@pytest.mark.parametrize("n_levels,dense,sh_dir", [(8, 0, 0), (12, 1, 0), (16, 1, 0), (16, 1, 1),
+                                                    (12, 1, 1)])
+def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense, sh_dir):
     """8, 12 and 16 levels: as many encoding work queues, fewer than, as many
-    as and more than the 8 XCDs, with and without dense coarse levels."""
+    as and more than the 8 XCDs, with and without dense coarse levels; and
+    the backward kernel built with the SH direction path at 12 and 16 levels."""
     name = f"tiny32_l{n_levels}"
     w = dataclasses.replace(synth.WORKLOADS["tiny32"], name=name, n_levels=n_levels,
                             log2_table=14)
     monkeypatch.setitem(synth.WORKLOADS, name, w)
-    case = G.make_case(name, K=8, P=256, dense_coarse_levels=dense)
+    case = G.make_case(name, K=8, P=256, dense_coarse_levels=dense, sh_dir_grad=sh_dir)
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
