@@ -10,7 +10,7 @@ namespace pnerf {
 
 constexpr int kMaxLevels = 16;
 constexpr int kHidden = 64;
-constexpr int kTile = 64;          // samples per wavefront tile (4 MFMA column tiles of 16)
+constexpr int kTile = 64;          // granule of the per-sample capacity (a multiple of every kernel's tile)
 constexpr int kMaskWords = 8;      // ReLU-mask words per lane per 64 samples (2 per 16-sample column)
 constexpr int kQueueStride = 32;   // uint32 words between the encoding's work-queue counters (one cache line)
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray

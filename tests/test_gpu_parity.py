@@ -242,6 +242,19 @@ def test_loss_grad_ragged_shapes(pn, K, P):
     check_full(pn, case, obs, ref)
 
 
+def test_loss_grad_uniform_scanned_offsets(pn):
+    """Uniform sampling over more rays than the write pass scans itself (96
+    scan blocks of 256 rays, against 64): the counts known at ray set-up go
+    through the separate scan finish."""
+    case = G.make_case("tiny32", K=24, P=1024, pix_seed=7)
+    assert case.pix.size > 64 * 256
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, _ = check_full(pn, case, obs, ref)
+    assert stats["samples"] == int(ref["march"][0][-1])
+
+
 def test_loss_grad_zero_at_ground_truth(pn):
     case = G.make_case("tiny32")
     of = O.OracleField(case.spec)
