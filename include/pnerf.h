@@ -164,7 +164,7 @@ void pnerf_destroy_field(pnerf_field* field);
  *                 (+ sum_rays d x dL/dd through SH when sh_dir_grad = 1)
  * poses (device) [K][3][4]; pixel_ids (device) int32 [K][P], each in [0, W*H);
  * observed (device) float32 [H][W][3]; loss (device) [K]; dpose (device) [K][6].
- * Limits: K >= 1, P >= 1, K*P < 2^31, pixel ids in range (not checked on the
+ * Limits: 1 <= K <= 65535, P >= 1, K*P < 2^31, pixel ids in range (not checked on the
  * device: out-of-range ids are undefined behaviour). */
 pnerf_status pnerf_render_loss_grad(pnerf_field* field, int32_t K, const float* poses,
                                     int32_t P, const int32_t* pixel_ids,
@@ -238,7 +238,7 @@ pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* opt_state
                                        uint32_t round_idx, void* stream);
 
 /* Forward rendering only (the composite colour of each pixel's ray).
- * rgb (device) float32 [K][P][3]. */
+ * rgb (device) float32 [K][P][3].  Limits as for pnerf_render_loss_grad. */
 pnerf_status pnerf_render(pnerf_field* field, int32_t K, const float* poses, int32_t P,
                           const int32_t* pixel_ids, const pnerf_intrinsics* intr,
                           float* rgb, void* stream);
@@ -249,7 +249,8 @@ pnerf_status pnerf_render(pnerf_field* field, int32_t K, const float* poses, int
  * float32 and lattice_j (device) int32 [capacity] receive each sample's
  * distance and lattice / segment index; otherwise only ray_offset is written
  * and the call still returns PNERF_OK (compare the total with capacity).
- * Requires K*P <= 2^21 (else PNERF_ERR_CAPACITY). */
+ * Requires K*P <= 2^21 (else PNERF_ERR_CAPACITY) and the limits of
+ * pnerf_render_loss_grad. */
 pnerf_status pnerf_march(pnerf_field* field, int32_t K, const float* poses, int32_t P,
                          const int32_t* pixel_ids, const pnerf_intrinsics* intr,
                          int64_t* ray_offset, float* t, int32_t* lattice_j, int64_t capacity,

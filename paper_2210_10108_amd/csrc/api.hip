@@ -442,6 +442,8 @@ pnerf_status check_batch(pnerf_field* F, int32_t K, const float* poses, int32_t 
                          const int32_t* pix, const pnerf_intrinsics* intr) {
   if (!F) return fail(PNERF_ERR_INVALID_ARG, "field is NULL");
   if (K < 1 || P < 1) return fail(PNERF_ERR_INVALID_ARG, "K=%d and P=%d must be >= 1", K, P);
+  // the per-hypothesis reduction runs one grid row per hypothesis
+  if (K > 65535) return fail(PNERF_ERR_INVALID_ARG, "K=%d exceeds 65535", K);
   if ((int64_t)K * P >= ((int64_t)1 << 31))
     return fail(PNERF_ERR_INVALID_ARG, "K*P=%lld exceeds 2^31-1", (long long)K * P);
   if (!poses || !pix || !intr) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");

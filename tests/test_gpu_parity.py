@@ -255,6 +255,27 @@ def test_loss_grad_uniform_scanned_offsets(pn):
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
+def test_loss_grad_most_hypotheses(pn):
+    """K = 65535 hypotheses of one pixel each (the reduction's grid rows), and
+    one more is an argument error, not a failed launch.  The observed image is
+    random, so that no one-pixel loss is a near-zero residual, whose relative
+    error float32 colour alone would set."""
+    import torch
+    case = G.make_case("tiny32", K=65535, P=1, pix_seed=11)
+    of = O.OracleField(case.spec)
+    obs = np.random.default_rng(5).uniform(0.0, 1.0, (32, 32, 3)).astype(np.float32)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    check_full(pn, case, obs, ref)
+    f = pn.Field(case.spec)
+    poses = G.to_dev(np.concatenate([case.poses, case.poses[:1]]))
+    pix = G.to_dev(np.concatenate([case.pix, case.pix[:1]]))
+    with pytest.raises(pn.PnerfError) as e:
+        f.render_loss_grad(poses, pix, G.to_dev(obs), case.intr)
+    assert e.value.status == pn.ERR_INVALID_ARG and "65535" in str(e.value)
+    torch.cuda.synchronize()
+    f.close()
+
+
 def test_loss_grad_zero_at_ground_truth(pn):
     case = G.make_case("tiny32")
     of = O.OracleField(case.spec)
