@@ -35,7 +35,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlock = 512;  // 8 wavefronts: one LDS copy of the weight units serves 8 waves
 constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
-constexpr int kBwdNT = 1;    // and backward (66 registers: 3 blocks, 6 wavefronts per SIMD)
+constexpr int kBwdNT = 1;    // and backward (62 registers without the SH direction path: 8 wavefronts per SIMD)
 
 struct Split {
   bf16x8 hi, lo;
