@@ -2,7 +2,7 @@
 
 A step is one pass of the whole hot path over one batch: render -> Huber loss
 -> pose gradient for K hypotheses (pnerf_render_loss_grad), the pose update
-(pnerf_step_momentum, or pnerf_step_adam at the setting of Sec. IV-C with
+(pnerf_step_momentum, or pnerf_step_adam at the setting of Sec. IV-D with
 --optimizer adam) and, at the workload's resampling interval, Monte Carlo
 resampling (pnerf_resample_hypotheses).  Inputs (field, observation, pixel
 batches, poses) are resident in HBM before timing starts.
@@ -36,16 +36,18 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="ngp800_uniform", choices=synth.ORDER)
+    # default: the largest single-GPU workload (1024 x 512 rays in the [-2,2]^3
+    # box, T = 2^21, 256^3 occupancy, up to 2048 samples per ray)
+    ap.add_argument("--workload", default="large4m_occ256", choices=synth.ORDER)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--optimizer", default="momentum", choices=("momentum", "adam"),
                     help="pose update: the workload's momentum SGD, or Adam with the "
-                         "learning rates and decay of Sec. IV-C")
+                         "learning rates and decay of Sec. IV-D")
     ap.add_argument("--sh-dir-grad", type=int, default=0, choices=(0, 1),
                     help="1: also carry the gradient through the view-direction (SH) input")
     ap.add_argument("--paper-run", action="store_true",
                     help="instead of the step benchmark, time one whole pose estimate: the "
-                         "Monte Carlo schedule of Sec. IV-B/IV-C (64 hypotheses, 2560 Adam "
+                         "Monte Carlo schedule of Sec. IV-B/IV-D (64 hypotheses, 2560 Adam "
                          "steps, 4 resampling rounds) on the workload's field and pixel count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-calibration", action="store_true",
@@ -213,7 +215,8 @@ def paper_run(args):
     rot_err = math.degrees(np.arccos(np.clip((np.trace(p[:, :3].T @ gt[:, :3]) - 1) / 2, -1, 1)))
     print(json.dumps({
         "metric": "seconds per pose estimate (paper schedule)", "value": elapsed, "unit": "s",
-        "n_gpus": 1, "higher_is_better": False, "data": "synthetic", "dtype": "f32",
+        "n_gpus": 1, "higher_is_better": False, "data": "synthetic",
+        "dtype": ("f16-storage" if w.param_dtype == "f16" else "f32") + "+split-bf16x3-mfma",
         "steps": sched.total_steps, "hypotheses": K,
         "hypothesis_iters_per_sec": K * sched.total_steps / elapsed,
         "config": {"workload": w.name, "P": w.P, "rays_per_step": K * w.P,
@@ -369,8 +372,11 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
-        "mlp_arithmetic": "bf16 MFMA on split hi/lo operands, fp32 accumulation",
+        # the path's arithmetic: fp32 (or fp16-stored) table and weights, fp32
+        # encoding and compositing; the MLPs as three bf16 MFMA products per fp32
+        # product (hi*hi + hi*lo + lo*hi), accumulated in fp32
+        "dtype": ("f16-storage" if w.param_dtype == "f16" else "f32") + "+split-bf16x3-mfma",
+        "mlp_arithmetic": "bf16 MFMA on split hi/lo operands (3 products), fp32 accumulation",
         "data": ("synthetic (seeded random frozen field" +
                  ("" if w.density == "random" else ", density shaped as one object in empty space") +
                  "; observation rendered at a seeded ground-truth pose)"),
