@@ -9,7 +9,7 @@
  * image.  This library evaluates, for K pose hypotheses at once (Sec. IV-B),
  * the loss and its gradient split into a rotation part (the torque of Eq. 3)
  * and a translation part (the force of Eq. 2), applies a momentum or Adam update
- * on SO(3) x T(3) (Sec. IV-A, IV-C), and resamples hypotheses (Sec. IV-B).
+ * on SO(3) x T(3) (Sec. IV-A; setting of Sec. IV-D), and resamples hypotheses (Sec. IV-B).
  *
  * Conventions shared by every entry point
  *  - Poses are camera-to-world float32 [K][3][4] = [R | o], row major: o is the
@@ -188,7 +188,7 @@ pnerf_status pnerf_step_momentum(int32_t K, float* poses, float* momentum,
  *                                          subspace s, stored in its 3 slots)
  *   u = -lr_s(step) (m / (1 - beta1^n)) / (sqrt(v / (1 - beta2^n)) + eps)
  *   R <- Exp(u_w) R,  o <- o + u_t
- * with the learning rates of Sec. IV-C decaying exponentially in the global
+ * with the learning rates of Sec. IV-D decaying exponentially in the global
  * step index `step` (0 for the first step of a run):
  *   lr_s(step) = lr_s * decay_base^(step / decay_steps)       (staircase = 0)
  *   lr_s(step) = lr_s * decay_base^floor(step / decay_steps)  (staircase = 1)
@@ -289,6 +289,32 @@ pnerf_status pnerf_field_last_sample_count(pnerf_field* field, int64_t* count, v
 pnerf_status pnerf_field_set_profiling(pnerf_field* field, int32_t enable);
 pnerf_status pnerf_field_profile_read(pnerf_field* field, int32_t index, const char** name,
                                       int64_t* launches, double* total_ms);
+
+/* Batch planning (host only: no device call, usable without a GPU).  The
+ * rendering calls count every ray's samples for a "counted batch" of whole
+ * hypotheses at a time, with 32-bit counts and offsets, then cut the counted
+ * batch into chunks of whole hypotheses whose samples fit the workspace
+ * (Sec. IV-B: hypotheses are independent, so any cut gives the same results).
+ *
+ * pnerf_plan_counted_batch: *hyps_per_batch = hypotheses per counted batch for
+ * P rays per hypothesis of at most max_per_ray samples each: at most K, at most
+ * 2^21 rays, and a worst case (every ray at its cap) below 2^31 samples.
+ * PNERF_ERR_CAPACITY when P > 2^21 or P * max_per_ray >= 2^31 (one hypothesis
+ * alone could overflow the counts); PNERF_ERR_INVALID_ARG for K, P or
+ * max_per_ray below 1.  The rendering calls return these errors before any
+ * device work is enqueued. */
+pnerf_status pnerf_plan_counted_batch(int32_t K, int32_t P, int32_t max_per_ray,
+                                      int32_t* hyps_per_batch);
+
+/* pnerf_plan_chunks: cut n hypotheses with hyp_samples[k] samples (host) into
+ * consecutive chunks: each chunk takes hypotheses while its sum stays within
+ * `capacity` and is below `goal` (a chunk always takes at least one).  Writes
+ * cut[0..c] (chunk i = hypotheses cut[i] .. cut[i+1]-1; cut[0] = 0, cut[c] = n),
+ * sums[0..c-1] and *n_chunks = c; cut needs n + 1 entries, sums n.
+ * PNERF_ERR_CAPACITY if one hypothesis exceeds capacity, INVALID_ARG for a
+ * negative count, n < 1 or capacity < 1. */
+pnerf_status pnerf_plan_chunks(const int32_t* hyp_samples, int32_t n, int64_t capacity,
+                               int64_t goal, int32_t* cut, int64_t* sums, int32_t* n_chunks);
 
 /* Message of the last non-OK status returned on this thread ("" if none). */
 const char* pnerf_last_error(void);

@@ -487,12 +487,12 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
   HIP_TRY(hipSetDevice(F->device));
   F->last_total_dev = nullptr;
   const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
-  if (P > max_rays)
-    return fail(PNERF_ERR_CAPACITY, "P=%d rays per hypothesis exceeds %lld", P, (long long)max_rays);
-  const int kr = (int)std::min<int64_t>(K, max_rays / P);
+  int32_t kr = 0;
+  pnerf_status st = pnerf_plan_counted_batch(K, P, F->dev.max_per_ray, &kr);
+  if (st != PNERF_OK) return st;
   if (mode == kMarch && kr < K)
     return fail(PNERF_ERR_CAPACITY, "march inspection needs K*P <= %lld rays", (long long)max_rays);
-  pnerf_status st = ensure_rays(F, kr * P, kr, s);
+  st = ensure_rays(F, kr * P, kr, s);
   if (st != PNERF_OK) return st;
   const int64_t per_sample = bytes_per_sample(F->dev);  // per buffer
   const int64_t limit = std::min<int64_t>(
@@ -542,19 +542,15 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       const bool pipe_here = pipe && hn > 1 && counted >= (int64_t)kMinOverlapSamples;
       const int64_t cap_c = pipe_here ? slot_limit : limit;
       const int64_t goal = pipe_here ? (counted + n_target - 1) / n_target : cap_c;
+      cut.assign((size_t)hn + 1, 0);
+      sums.assign((size_t)hn, 0);
+      int32_t nc = 0;
+      st = pnerf_plan_chunks(F->h_hyp, hn, cap_c, goal, cut.data(), sums.data(), &nc);
+      if (st != PNERF_OK) return fail(st, "hypotheses %d..%d: %s", h0, h0 + hn - 1, g_err.c_str());
+      cut.resize((size_t)nc + 1);
+      sums.resize((size_t)nc);
       int64_t biggest = 0;
-      for (int a = 0; a < hn;) {
-        int64_t sum = 0;
-        int b = a;
-        while (b < hn && sum + F->h_hyp[b] <= cap_c && (sum < goal || b == a)) sum += F->h_hyp[b++];
-        if (b == a)
-          return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace "
-                      "budget holds (%lld)", h0 + a, F->h_hyp[a], (long long)cap_c);
-        cut.push_back(b);
-        sums.push_back(sum);
-        biggest = std::max(biggest, sum);
-        a = b;
-      }
+      for (int64_t v : sums) biggest = std::max(biggest, v);
       overlap = pipe_here && sums.size() > 1;
       st = ensure_samples(F, biggest, cap_c, chunk_id + (int)sums.size(), overlap ? 2 : 1, s);
       if (st != PNERF_OK) return st;
@@ -634,6 +630,52 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
 extern "C" {
 
 const char* pnerf_last_error(void) { return g_err.c_str(); }
+
+pnerf_status pnerf_plan_counted_batch(int32_t K, int32_t P, int32_t max_per_ray,
+                                      int32_t* hyps_per_batch) {
+  if (!hyps_per_batch) return fail(PNERF_ERR_INVALID_ARG, "NULL hyps_per_batch");
+  *hyps_per_batch = 0;
+  if (K < 1 || P < 1 || max_per_ray < 1)
+    return fail(PNERF_ERR_INVALID_ARG, "K=%d, P=%d and max_per_ray=%d must be >= 1", K, P,
+                max_per_ray);
+  const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
+  if (P > max_rays)
+    return fail(PNERF_ERR_CAPACITY, "P=%d rays per hypothesis exceeds %lld", P, (long long)max_rays);
+  // counts, block sums, hypothesis totals and offsets of a counted batch are
+  // 32-bit: its worst case (every ray at its cap) must stay below 2^31
+  const int64_t hyp_worst = (int64_t)P * max_per_ray;
+  if (hyp_worst > kMaxCountedSamples)
+    return fail(PNERF_ERR_CAPACITY, "P=%d rays of up to %d samples each (%lld) may exceed the "
+                "%lld samples one hypothesis can hold", P, max_per_ray, (long long)hyp_worst,
+                (long long)kMaxCountedSamples);
+  *hyps_per_batch =
+      (int32_t)std::min<int64_t>(std::min<int64_t>(K, max_rays / P), kMaxCountedSamples / hyp_worst);
+  return PNERF_OK;
+}
+
+pnerf_status pnerf_plan_chunks(const int32_t* hyp_samples, int32_t n, int64_t capacity, int64_t goal,
+                               int32_t* cut, int64_t* sums, int32_t* n_chunks) {
+  if (!hyp_samples || !cut || !sums || !n_chunks || n < 1 || capacity < 1)
+    return fail(PNERF_ERR_INVALID_ARG, "invalid chunk-planning arguments");
+  *n_chunks = 0;
+  for (int32_t k = 0; k < n; ++k)
+    if (hyp_samples[k] < 0) return fail(PNERF_ERR_INVALID_ARG, "hypothesis %d: %d samples", k, hyp_samples[k]);
+  int32_t c = 0;
+  cut[0] = 0;
+  for (int32_t a = 0; a < n;) {
+    int64_t sum = 0;
+    int32_t b = a;
+    while (b < n && sum + hyp_samples[b] <= capacity && (sum < goal || b == a)) sum += hyp_samples[b++];
+    if (b == a)
+      return fail(PNERF_ERR_CAPACITY, "hypothesis %d has %d samples, more than the workspace "
+                  "budget holds (%lld)", a, hyp_samples[a], (long long)capacity);
+    sums[c] = sum;
+    cut[++c] = b;
+    a = b;
+  }
+  *n_chunks = c;
+  return PNERF_OK;
+}
 
 pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf_field** out) {
   if (!p || !out) return fail(PNERF_ERR_INVALID_ARG, "NULL params or out");
@@ -910,7 +952,7 @@ pnerf_status pnerf_step_adam(int32_t K, float* poses, float* state, const float*
       (p->representation != 0 && p->representation != 1))
     return fail(PNERF_ERR_INVALID_ARG, "staircase/second_moment/representation must be 0 or 1");
   if (!poses || !state || !dpose) return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
-  // Learning-rate decay of Sec. IV-C, evaluated once per call in double.
+  // Learning-rate decay of Sec. IV-D, evaluated once per call in double.
   double scale = 1.0;
   if (p->decay_steps > 0) {
     double e = p->staircase ? std::floor((double)step / (double)p->decay_steps)

@@ -16,6 +16,7 @@ constexpr int kQueueStride = 32;   // uint32 words between the encoding's work-q
 constexpr int kMaxLatticeCandidates = 1 << 20;  // bound on lattice points tested per ray
 constexpr int kMaxScanBlocks = 8192;  // offset scan: at most 8192 x 256 rays per counted batch
 constexpr int kMaxRawScanBlocks = 64;  // block sums the write pass may scan itself (one wavefront)
+constexpr int64_t kMaxCountedSamples = ((int64_t)1 << 31) - 1;  // int32 counts of a counted batch
 constexpr int kDefaultOverlapChunks = 1;   // loss-gradient chunks pipelined over two streams (1 = off)
 constexpr int kMinOverlapSamples = 1 << 16;  // smaller batches run as one chunk
 constexpr int64_t kDeviceSizedBytes = (int64_t)16 << 30;  // worst-case sample buffer a loss

@@ -73,6 +73,9 @@ _SIGS = {
     "pnerf_field_set_profiling": (C.c_int, [C.c_void_p, C.c_int32]),
     "pnerf_field_profile_read": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                            C.c_void_p]),
+    "pnerf_plan_counted_batch": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
+    "pnerf_plan_chunks": (C.c_int, [C.c_void_p, C.c_int32, C.c_int64, C.c_int64, C.c_void_p,
+                                    C.c_void_p, C.c_void_p]),
     "pnerf_last_error": (C.c_char_p, []),
 }
 
@@ -277,7 +280,7 @@ ADAM_STATE = 16  # floats of Adam state per hypothesis (PNERF_ADAM_STATE)
 
 
 class AdamParams(C.Structure):
-    """pnerf_adam_params; the defaults are the setting of Sec. IV-C."""
+    """pnerf_adam_params; the defaults are the setting of Sec. IV-D."""
     _fields_ = [("lr_rot", C.c_float), ("lr_trans", C.c_float), ("beta1", C.c_float),
                 ("beta2", C.c_float), ("eps", C.c_float), ("decay_base", C.c_float),
                 ("decay_steps", C.c_int32), ("staircase", C.c_int32),
@@ -311,3 +314,25 @@ def resample_hypotheses(poses, state, loss, keep_frac: float, sigma_rot: float,
         None if state is None else _dev(state, torch.float32, (K, dim), "state"), dim,
         _dev(loss, torch.float32, (K,), "loss"), keep_frac, sigma_rot, sigma_trans,
         seed & 0xFFFFFFFFFFFFFFFF, round_idx, _stream(stream)))
+
+
+def plan_counted_batch(K: int, P: int, max_per_ray: int) -> int:
+    """Hypotheses per counted batch (pnerf_plan_counted_batch; host only)."""
+    n = C.c_int32()
+    _check(lib().pnerf_plan_counted_batch(K, P, max_per_ray, C.byref(n)))
+    return n.value
+
+
+def plan_chunks(hyp_samples, capacity: int, goal: int):
+    """Chunks of whole hypotheses (pnerf_plan_chunks; host only): returns the
+    cut points [c + 1] and the samples of every chunk [c]."""
+    import numpy as np
+    h = np.ascontiguousarray(hyp_samples, dtype=np.int32)
+    n = len(h)
+    cut = np.zeros(n + 1, np.int32)
+    sums = np.zeros(max(n, 1), np.int64)
+    c = C.c_int32()
+    _check(lib().pnerf_plan_chunks(h.ctypes.data_as(C.c_void_p), n, capacity, goal,
+                                   cut.ctypes.data_as(C.c_void_p),
+                                   sums.ctypes.data_as(C.c_void_p), C.byref(c)))
+    return cut[:c.value + 1].copy(), sums[:c.value].copy()

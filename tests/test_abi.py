@@ -132,3 +132,60 @@ def test_product_path_does_not_reference_the_oracle():
                 text = open(os.path.join(dirpath, fn)).read()
                 assert not re.search(r"^\s*(from|import)\s+oracle\b", text, re.M), fn
                 assert "liboracle" not in text and "pnerf_oracle" not in text, fn
+
+
+# ------------------------------------------------ batch planning (host only)
+def test_plan_counted_batch_limits(pn):
+    # hypotheses per counted batch: at most K, 2^21 rays, and a worst case
+    # (every ray at its sample cap) below 2^31 samples
+    assert pn.plan_counted_batch(1024, 512, 2048) == 1024          # the 2^21-table workload
+    assert pn.plan_counted_batch(64, 4096, 1024) == 64
+    assert pn.plan_counted_batch(65535, 1, 32) == 65535
+    assert pn.plan_counted_batch(10_000, 256, 32) == (1 << 21) // 256
+    # 2^18 rays of up to 4096 samples: a worst case of 2^30 each, one per batch
+    assert pn.plan_counted_batch(5, 1 << 18, 4096) == 1
+    # 2^19 rays at 4096 samples reach 2^31: refused before any device work
+    with pytest.raises(pn.PnerfError) as e:
+        pn.plan_counted_batch(1, 1 << 19, 4096)
+    assert e.value.status == pn.ERR_CAPACITY and "2147483647" in str(e.value)
+    # every counted batch's worst case stays within int32 at the largest sizes
+    for P in (1, 7, 255, 4096, 65535, 1 << 17, (1 << 18) - 1):
+        for cap in (1, 32, 1024, 4096, 8192):
+            if P * cap >= 1 << 31:
+                continue
+            kr = pn.plan_counted_batch(65535, P, cap)
+            assert 1 <= kr and kr * P <= 1 << 21 and kr * P * cap < 1 << 31, (P, cap)
+    with pytest.raises(pn.PnerfError) as e:
+        pn.plan_counted_batch(1, (1 << 21) + 1, 1)
+    assert e.value.status == pn.ERR_CAPACITY
+    with pytest.raises(pn.PnerfError) as e:
+        pn.plan_counted_batch(0, 1, 1)
+    assert e.value.status == pn.ERR_INVALID_ARG
+
+
+def test_plan_chunks_cuts_whole_hypotheses(pn):
+    import numpy as np
+    rng = np.random.default_rng(3)
+    for trial in range(200):
+        n = int(rng.integers(1, 60))
+        h = rng.integers(0, 1000, n)
+        cap = int(rng.integers(max(int(h.max()), 1), 5000))
+        goal = int(rng.integers(1, cap + 1))
+        cut, sums = pn.plan_chunks(h, cap, goal)
+        assert cut[0] == 0 and cut[-1] == n and np.all(np.diff(cut) >= 1)
+        for i in range(len(sums)):
+            part = h[cut[i]:cut[i + 1]]
+            assert sums[i] == part.sum() <= cap
+            # greedy: a chunk stops only at the goal, the capacity or the end
+            if cut[i + 1] < n and part.sum() < goal:
+                assert part.sum() + h[cut[i + 1]] > cap
+            # and never takes another hypothesis once it has reached the goal
+            if len(part) > 1:
+                assert part[:-1].sum() < goal
+    # one hypothesis above the capacity, and a negative count, are refused
+    with pytest.raises(pn.PnerfError) as e:
+        pn.plan_chunks([5, 11, 3], 10, 10)
+    assert e.value.status == pn.ERR_CAPACITY and "hypothesis 1" in str(e.value)
+    with pytest.raises(pn.PnerfError) as e:
+        pn.plan_chunks([5, -2], 10, 10)
+    assert e.value.status == pn.ERR_INVALID_ARG

@@ -138,13 +138,18 @@ def oracle_subset(of, case, obs, hyps):
     return of.render_loss_grad(case.poses[hyps], case.pix[hyps], obs, case.intr, per_sample=True)
 
 
-def check_full(pn, case, obs, ref, hyps=None):
+def check_full(pn, case, obs, ref, of, hyps=None):
+    """The whole batch on the GPU as one chunk; `ref` is the oracle's per-sample
+    result for hypotheses `hyps` (all by default), computed by `of`."""
+    import os
     loss, dpose, n, ex = run_loss_grad(pn, case, obs, per_sample=True)
     P = case.pix.shape[1]
     hyps = list(range(case.pix.shape[0])) if hyps is None else list(hyps)
     ranges = [(int(ex["off"][k * P]), int(ex["off"][(k + 1) * P])) for k in hyps]
+    alt = G.Alt(of, case.poses[hyps], case.pix[hyps], obs, case.intr)
+    label = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
     return G.assert_loss_grad_close(loss, dpose, ref, hyps=hyps, gpu_samples=ex["out6"],
-                                    gpu_ranges=ranges), ex
+                                    gpu_ranges=ranges, alt=alt, label=label), ex
 
 
 @pytest.mark.parametrize("overrides", [
@@ -158,11 +163,12 @@ def test_loss_grad_tiny(pn, overrides):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, ex = check_full(pn, case, obs, ref)
+    stats, ex = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
     # stage parity element by element: d loss / d h0 and d loss / d z of every sample
     so = ref["samples"]
-    ok = ~G.ambiguous(so)
+    relu, ray = G.set_aside(so)
+    ok = ~(relu | ray)
     assert np.abs(ex["gh0"][ok] - so[ok, 4]).max() <= 1e-3 * np.abs(so[:, 4]).max()
     assert np.abs(ex["gz"][ok] - so[ok, 5:8]).max() <= 1e-3 * np.abs(so[:, 5:8]).max()
 
@@ -181,7 +187,7 @@ def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense, sh_dir):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref)
+    stats, _ = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -194,7 +200,7 @@ def test_loss_grad_pixel_losses(pn, loss_type, param):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref)
+    stats, _ = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -217,7 +223,7 @@ def test_loss_grad_early_stop_and_occupancy(pn, div, bias, stops):
     assert np.sum(stopped & (ref["stop"] >= stops[0]) & (ref["stop"] < stops[1])) >= 5
     if stops[0] >= 128:
         assert np.sum(~stopped & (cnt > 128)) >= 5
-    check_full(pn, case, obs, ref)
+    check_full(pn, case, obs, ref, of)
 
 
 def test_loss_grad_empty_grid_is_background_only(pn):
@@ -239,7 +245,7 @@ def test_loss_grad_ragged_shapes(pn, K, P):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    check_full(pn, case, obs, ref)
+    check_full(pn, case, obs, ref, of)
 
 
 def test_loss_grad_uniform_scanned_offsets(pn):
@@ -251,7 +257,7 @@ def test_loss_grad_uniform_scanned_offsets(pn):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref)
+    stats, _ = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -265,7 +271,7 @@ def test_loss_grad_most_hypotheses(pn):
     of = O.OracleField(case.spec)
     obs = np.random.default_rng(5).uniform(0.0, 1.0, (32, 32, 3)).astype(np.float32)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    check_full(pn, case, obs, ref)
+    check_full(pn, case, obs, ref, of)
     f = pn.Field(case.spec)
     poses = G.to_dev(np.concatenate([case.poses, case.poses[:1]]))
     pix = G.to_dev(np.concatenate([case.pix, case.pix[:1]]))
@@ -273,6 +279,28 @@ def test_loss_grad_most_hypotheses(pn):
         f.render_loss_grad(poses, pix, G.to_dev(obs), case.intr)
     assert e.value.status == pn.ERR_INVALID_ARG and "65535" in str(e.value)
     torch.cuda.synchronize()
+    f.close()
+
+
+def test_loss_grad_refuses_a_batch_whose_counts_could_overflow(pn):
+    """2^19 rays of up to 4096 samples each could count 2^31 samples, past the
+    32-bit counts: refused with a capacity error before any device work, and
+    the field still works afterwards."""
+    import torch
+    case = G.make_case("tiny32", K=1, P=4, n_uniform=4096)
+    f = pn.Field(case.spec)
+    P = 1 << 19
+    poses = G.to_dev(case.poses)
+    pix = torch.zeros(1, P, dtype=torch.int32, device=G.torch_dev())
+    obs = torch.zeros(32, 32, 3, dtype=torch.float32, device=G.torch_dev())
+    with pytest.raises(pn.PnerfError) as e:
+        f.render_loss_grad(poses, pix, obs, case.intr)
+    assert e.value.status == pn.ERR_CAPACITY and "2147483647" in str(e.value)
+    loss, dpose = f.render_loss_grad(poses, G.to_dev(case.pix), obs, case.intr)
+    torch.cuda.synchronize()
+    n = f.last_sample_count()
+    assert n % 4096 == 0 and 0 < n <= 4 * 4096   # every ray that meets the box has 4096
+    assert np.isfinite(loss.cpu().numpy()).all()
     f.close()
 
 
@@ -291,7 +319,7 @@ def test_loss_grad_ngp800_uniform_full_batch(pn):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref)
+    stats, _ = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -307,7 +335,7 @@ def test_loss_grad_ngp800_occ128_full_batch_sampled_hypotheses(pn):
     hyps = [0, 31, 63]
     obs = G.oracle_observation(of, case.gt, case.pix[hyps], case.intr)
     ref = oracle_subset(of, case, obs, hyps)
-    check_full(pn, case, obs, ref, hyps=hyps)
+    check_full(pn, case, obs, ref, of, hyps=hyps)
 
 
 def test_loss_grad_chunked_matches_single_chunk(pn):
@@ -452,7 +480,7 @@ def test_loss_grad_tiny_fp16_storage(pn, overrides):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, ex = check_full(pn, case, obs, ref)
+    stats, ex = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -526,7 +554,7 @@ def test_loss_grad_tiny_bump(pn):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, ex = check_full(pn, case, obs, ref)
+    stats, ex = check_full(pn, case, obs, ref, of)
     cnt = np.diff(ref["march"][0])
     assert np.sum(ref["stop"] < cnt) >= 5     # early termination took effect
 
