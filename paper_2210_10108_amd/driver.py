@@ -1,5 +1,5 @@
 """Pose-estimation driver: the parallel Monte Carlo schedule of Sec. IV-B run
-with the optimiser of Sec. IV-A and the setting of Sec. IV-C.
+with the optimiser of Sec. IV-A and the setting of Sec. IV-D.
 
 Phase 1 optimises P_N hypotheses independently for s1 steps.  Phase 2 is
 repeated S times: rank the hypotheses by loss, keep the lowest-loss fraction r
@@ -23,7 +23,7 @@ from . import pnerf
 
 @dataclasses.dataclass(frozen=True)
 class MCSchedule:
-    """Constants of the Monte Carlo schedule (Sec. IV-B, values of Sec. IV-C)."""
+    """Constants of the Monte Carlo schedule (Sec. IV-B, values of Sec. IV-D)."""
     n_hypotheses: int = 64   # P_N
     s1: int = 512            # free-exploration steps
     s2: int = 512            # steps after each resampling round

@@ -1,5 +1,5 @@
 """Parity of the pose optimisers and of whole optimisation runs with the CPU
-oracle: the Adam step on SO(3) x T(3) (Sec. IV-A, IV-C), resampling with Adam
+oracle: the Adam step on SO(3) x T(3) (Sec. IV-A, IV-D), resampling with Adam
 state (Sec. IV-B), and short runs of render -> loss -> gradient -> update ->
 resample on both sides from the same seeded start."""
 import math
@@ -340,7 +340,7 @@ def test_adam_mc_schedule_run_matches_oracle(pn):
 @pytest.mark.parametrize("seed", [0, 1])
 def test_paper_schedule_converges_on_object_field(pn, seed):
     """The whole method on the GPU: the Monte Carlo schedule of Sec. IV-B with
-    the constants and Adam of Sec. IV-C (64 hypotheses perturbed by up to 30
+    the constants and Adam of Sec. IV-D (64 hypotheses perturbed by up to 30
     deg / 0.2, 2560 steps, 4 resampling rounds, 256 pixels per hypothesis per
     step) on the object field.  The hypothesis with the lowest final loss
     lands inside the paper's success thresholds (rotation error < 5 deg,

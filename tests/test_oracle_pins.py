@@ -460,7 +460,7 @@ def _adam_run(oracle_lib, pose0, grads, **kw):
 
 @pytest.mark.parametrize("decay_steps,staircase", [(0, 0), (64, 0), (64, 1)])
 def test_adam_per_component_matches_torch_adam(oracle_lib, decay_steps, staircase):
-    """Sec. IV-A/IV-C Adam with per-component second moments: the translation
+    """Sec. IV-A/IV-D Adam with per-component second moments: the translation
     follows torch's Adam on the camera centre, and the orientation is the
     product of the rotations given by torch's Adam steps on a rotation vector."""
     w, _ = tiny_spec()

@@ -1,5 +1,5 @@
 """Host logic of the Monte Carlo schedule (Sec. IV-B with the constants of
-Sec. IV-C).  CPU only."""
+Sec. IV-D).  CPU only."""
 import pytest
 
 from paper_2210_10108_amd.driver import MCSchedule, PAPER_SCHEDULE
