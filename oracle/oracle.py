@@ -65,6 +65,12 @@ def lib():
         L.orc_shade.restype = i32
         L.orc_shade.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                 vp, vp, i32]
+        L.orc_shade_ray_variant.restype = i32
+        L.orc_shade_ray_variant.argtypes = [vp, vp, i32, i32, vp, vp, vp, i32, f32, vp, vp, vp,
+                                            vp, vp, vp, vp]
+        L.orc_shade_ray_jobs.restype = i32
+        L.orc_shade_ray_jobs.argtypes = [vp, vp, i32, vp, vp, vp, f64, i32, vp, vp, vp, vp, vp,
+                                         vp, i32]
         L.orc_encode.argtypes = [vp, vp, vp, vp, vp, vp]
         L.orc_sh16.argtypes = [vp, vp, vp]
         L.orc_density_mlp.argtypes = [vp, vp, vp]
@@ -102,6 +108,20 @@ def n_threads_default() -> int:
 def intr_struct(intr: dict) -> _Intr:
     return _Intr(int(intr["width"]), int(intr["height"]), float(intr["fx"]), float(intr["fy"]),
                  float(intr["cx"]), float(intr["cy"]))
+
+
+SAMPLE_COLS = 17  # columns of the per-sample output (ORC_SAMPLE_COLS)
+
+
+class _Variant(C.Structure):
+    _fields_ = [("relu_margin", C.c_double), ("relu_pattern", C.c_void_p),
+                ("relu_pattern_all", C.c_int32), ("stop", C.c_int32), ("loss_sign", C.c_int32 * 3)]
+
+
+# one ray of a batch of variant shadings (orc_ray_job)
+RAY_JOB = np.dtype([("hyp", np.int32), ("pix", np.int32), ("t0", np.int64), ("n", np.int32),
+                    ("delta", np.float32), ("stop", np.int32), ("loss_sign", np.int32, 3),
+                    ("relu_pattern", np.int32)], align=True)
 
 
 class OracleField:
@@ -201,7 +221,7 @@ class OracleField:
         rgb = np.zeros((K * P, 3))
         stop = np.zeros(K * P, dtype=np.int32)
         sig = np.zeros(1, dtype=np.uint64)
-        so = np.zeros((max(int(off[-1]), 1), 16)) if per_sample else None
+        so = np.zeros((max(int(off[-1]), 1), SAMPLE_COLS)) if per_sample else None
         it = intr_struct(intr)
         rc = lib().orc_shade(self.ptr, K, _p(poses64), P, _p(pix), _p(obs), C.byref(it), _p(off),
                              _p(t), _p(delta), _p(sd), _p(loss), _p(dpose), _p(rgb), _p(stop),
@@ -213,6 +233,61 @@ class OracleField:
         if per_sample:
             out["samples"] = so[: int(off[-1])]
         return out
+
+    def shade_ray_variant(self, pose, P, pix, obs, intr, t, delta, relu_margin=0.0,
+                          relu_pattern=None, stop=-1, loss_sign=(0, 0, 0)):
+        """One ray (pixel `pix` of a hypothesis with `pose` and P pixels, samples t
+        at spacing delta) with chosen threshold decisions taken the other way
+        (orc_shade_ray_variant).  Returns dict(samples [n][SAMPLE_COLS], near [n],
+        loss, g [6], rgb [3], stop)."""
+        pose = np.ascontiguousarray(np.asarray(pose, np.float32).astype(np.float64).reshape(12))
+        t = np.ascontiguousarray(t, dtype=np.float32)
+        n = int(t.size)
+        obs = np.ascontiguousarray(obs, dtype=np.float32)
+        pat = None if relu_pattern is None else np.ascontiguousarray(relu_pattern, np.int32)
+        assert pat is None or pat.size == n
+        v = _Variant(float(relu_margin), None if pat is None else _p(pat).value, 0, int(stop),
+                     (C.c_int32 * 3)(*[int(x) for x in loss_sign]))
+        so = np.zeros((max(n, 1), SAMPLE_COLS))
+        near = np.zeros(max(n, 1), np.int32)
+        loss = np.zeros(1)
+        g = np.zeros(6)
+        rgb = np.zeros(3)
+        used = np.zeros(1, np.int32)
+        it = intr_struct(intr)
+        tt = t if n else np.zeros(1, np.float32)
+        rc = lib().orc_shade_ray_variant(self.ptr, _p(pose), int(P), int(pix), _p(obs),
+                                         C.byref(it), _p(tt), n, float(delta), C.byref(v),
+                                         _p(so), _p(near), _p(loss), _p(g), _p(rgb), _p(used))
+        if rc != 0:
+            raise ValueError("oracle: unsupported field configuration")
+        return dict(samples=so[:n], near=near[:n], loss=float(loss[0]), g=g, rgb=rgb,
+                    stop=int(used[0]))
+
+    def shade_ray_jobs(self, poses, P, obs, intr, t, jobs, relu_margin, threads=None):
+        """Many rays with chosen decisions taken the other way (orc_shade_ray_jobs).
+        jobs: a RAY_JOB array.  Returns (samples [sum n][SAMPLE_COLS], near [sum n],
+        first row of each job [n_jobs], loss [n_jobs], g [n_jobs][6])."""
+        poses = np.ascontiguousarray(np.asarray(poses, np.float32).astype(np.float64).reshape(-1, 12))
+        jobs = np.ascontiguousarray(jobs, dtype=RAY_JOB)
+        nj = len(jobs)
+        rows = np.zeros(max(nj, 1), np.int64)
+        if nj:
+            rows[1:nj] = np.cumsum(jobs["n"].astype(np.int64))[:-1]
+        total = int(jobs["n"].sum()) if nj else 0
+        so = np.zeros((max(total, 1), SAMPLE_COLS))
+        near = np.zeros(max(total, 1), np.int32)
+        loss = np.zeros(max(nj, 1))
+        g = np.zeros((max(nj, 1), 6))
+        t = np.ascontiguousarray(t if np.size(t) else np.zeros(1, np.float32), dtype=np.float32)
+        obs = np.ascontiguousarray(obs, dtype=np.float32)
+        it = intr_struct(intr)
+        rc = lib().orc_shade_ray_jobs(self.ptr, _p(poses), int(P), _p(obs), C.byref(it), _p(t),
+                                      float(relu_margin), nj, _p(jobs), _p(rows), _p(so), _p(near),
+                                      _p(loss), _p(g), threads or n_threads_default())
+        if rc != 0:
+            raise ValueError("oracle: unsupported field configuration")
+        return so[:total], near[:total], rows[:nj], loss[:nj], g[:nj]
 
     def render_loss_grad(self, poses, pix, obs, intr, threads=None, per_sample=False):
         m = self.march(poses, pix, intr)
@@ -313,7 +388,7 @@ class _Adam(C.Structure):
 
 def step_adam(poses, state, dpose, step, lr_rot, lr_trans, beta1=0.9, beta2=0.999, eps=1e-8,
               decay_base=1.0, decay_steps=0, staircase=0, second_moment=0, representation=0):
-    """Adam on SO(3) x T(3) (Sec. IV-A, IV-C), or on the coupled se(3) twist
+    """Adam on SO(3) x T(3) (Sec. IV-A; setting of Sec. IV-D), or on the coupled se(3) twist
     (representation = 1); returns new (poses, state)."""
     poses = np.array(poses, dtype=np.float32, copy=True)
     state = np.array(state, dtype=np.float32, copy=True)

@@ -379,9 +379,12 @@ void orc_composite_grad(int32_t n, const double* sigma, const double* rgb, doubl
  *   5 MAPE        |r| / (|y| + p)
  *   6 sMAPE       2 |r| / (|C| + |y| + p)
  *   7 Smooth L1   0.5 r^2 / p (|r| < p), |r| - p / 2 */
-static double pixel_loss(int type, double C, double y, double p, double* grad, int* branch,
-                         double* kink) {
-  const double r = C - y, ar = fabs(r), sr = r > 0.0 ? 1.0 : (r < 0.0 ? -1.0 : 0.0);
+static double pixel_loss(int type, double C, double y, double p, int force_sign, double* grad,
+                         int* branch, double* kink) {
+  const double r = C - y, ar = fabs(r);
+  /* the sign of r in the derivative; force_sign = +1 / -1 takes the derivative
+   * on that side of r = 0 (the other valid choice next to the jump) */
+  const double sr = force_sign ? (double)force_sign : (r > 0.0 ? 1.0 : (r < 0.0 ? -1.0 : 0.0));
   *branch = r > 0.0 ? 1 : (r < 0.0 ? 2 : 0);
   *kink = INFINITY;
   switch (type) {
@@ -431,8 +434,8 @@ static double pixel_loss(int type, double C, double y, double p, double* grad, i
         *branch = 0;
         return 0.5 * r * r / p;
       }
+      /* C^1 at |r| = p: r / p and sign(r) meet, no jump of the derivative */
       *grad = sr;
-      *kink = fabs(ar - p);
       return ar - 0.5 * p;
   }
 }
@@ -440,7 +443,7 @@ static double pixel_loss(int type, double C, double y, double p, double* grad, i
 /* One channel's loss for testing: value, derivative and kink distance. */
 double orc_pixel_loss(int32_t type, double C, double y, double p, double* grad, double* kink) {
   int br;
-  return pixel_loss(type, C, y, p, grad, &br, kink);
+  return pixel_loss(type, C, y, p, 0, grad, &br, kink);
 }
 
 /* ------------------------------------------------------------- signature */
@@ -458,15 +461,23 @@ typedef struct {
   double jac[3 * CIN];
   double a_pre[HID], h[DOUT], b1[HID], b2[HID];
   double rgb[3], sigma;
+  unsigned char flip[3][HID]; /* variant: ReLU backward masks taken the other way */
 } sample_state;
+
+/* Relative margin of one ReLU decision: |pre-activation| over the sum of its
+ * terms' magnitudes (INFINITY when every term is zero). */
+static double relu_margin(double pre, double magnitude) {
+  return magnitude > 0.0 ? fabs(pre) / magnitude : INFINITY;
+}
 
 /* One ray: forward, loss, backward.  Returns per-ray loss, force G = sum_i
  * dL/dp_i and torque tau = d x sum_i t_i dL/dp_i (+ d x dL/dd through the SH
  * path when enabled) -- Eq. (2) and Eq. (3). */
 static void shade_ray(const orc_field* f, const double pose64[12], const orc_intr* in,
                       int32_t pix, const float* obs, const float* ts, int32_t n, float delta32,
-                      const double* sh_dir, int32_t P, double* loss_out, double g_out[6],
-                      double rgb_out[3], int32_t* stop_out, uint64_t* sig, double* s_out) {
+                      const double* sh_dir, int32_t P, const orc_variant* var, double* loss_out,
+                      double g_out[6], double rgb_out[3], int32_t* stop_out, uint64_t* sig,
+                      double* s_out, int32_t* near_out) {
   float pose32[12];
   for (int q = 0; q < 12; ++q) pose32[q] = (float)pose64[q];
   float o32[3], d32[3];
@@ -514,26 +525,38 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
       }
     density_fwd(f, s->feat, s->a_pre, s->h);
     s->sigma = exp(s->h[0] + f->density_bias);
-    /* decision margin of the density ReLUs: |pre-activation| over the sum of
-     * its terms' magnitudes (diagnostic for comparing against float kernels) */
-    double margin = INFINITY;
-    for (int j = 0; j < HID; ++j) {
-      double m = 0.0;
-      for (int q = 0; q < f->din; ++q) m += fabs(s->feat[q] * f->wd1[q * HID + j]);
-      if (m > 0.0 && fabs(s->a_pre[j]) / m < margin) margin = fabs(s->a_pre[j]) / m;
-    }
     double xc[CIN];
     for (int q = 0; q < 15; ++q) xc[q] = s->h[1 + q];
     for (int q = 0; q < 16; ++q) xc[15 + q] = sh[q];
     xc[31] = 0.0;
     color_fwd(f, xc, s->b1, s->b2, s->rgb);
+    /* decision margins of the ReLUs (density layer 1, colour layers 1 and 2),
+     * for comparing against float kernels; the smallest one is reported, and a
+     * variant flips the backward mask of chosen units whose margin is below
+     * var->relu_margin (numbered layer by layer, unit by unit) */
+    double lm[3][HID];
     for (int j = 0; j < HID; ++j) {
-      double m1 = 0.0, m2 = 0.0;
+      double m0 = 0.0, m1 = 0.0, m2 = 0.0;
+      for (int q = 0; q < f->din; ++q) m0 += fabs(s->feat[q] * f->wd1[q * HID + j]);
       for (int q = 0; q < CIN; ++q) m1 += fabs(xc[q] * f->wc1[q * HID + j]);
       for (int q = 0; q < HID; ++q) m2 += fabs((s->b1[q] > 0.0 ? s->b1[q] : 0.0) * f->wc2[q * HID + j]);
-      if (m1 > 0.0 && fabs(s->b1[j]) / m1 < margin) margin = fabs(s->b1[j]) / m1;
-      if (m2 > 0.0 && fabs(s->b2[j]) / m2 < margin) margin = fabs(s->b2[j]) / m2;
+      lm[0][j] = relu_margin(s->a_pre[j], m0);
+      lm[1][j] = relu_margin(s->b1[j], m1);
+      lm[2][j] = relu_margin(s->b2[j], m2);
     }
+    double margin = INFINITY;
+    int32_t near = 0;
+    memset(s->flip, 0, sizeof(s->flip));
+    for (int layer = 0; layer < 3; ++layer)
+      for (int j = 0; j < HID; ++j) {
+        if (lm[layer][j] < margin) margin = lm[layer][j];
+        if (var && lm[layer][j] < var->relu_margin) {
+          const int32_t pat = var->relu_pattern ? var->relu_pattern[i] : var->relu_pattern_all;
+          if (near < 31 && ((pat >> near) & 1)) s->flip[layer][j] = 1;
+          ++near;
+        }
+      }
+    if (near_out) near_out[i] = near;
     for (int j = 0; j < HID; ++j) {
       h = fnv(h, s->a_pre[j] > 0.0);
       h = fnv(h, s->b1[j] > 0.0);
@@ -542,8 +565,8 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
     sig_s[i] = s->sigma;
     for (int c = 0; c < 3; ++c) rgb_s[3 * i + c] = s->rgb[c];
     if (s_out) {
-      double* so = s_out + 16 * (size_t)i;
-      for (int q = 0; q < 16; ++q) so[q] = 0.0;
+      double* so = s_out + ORC_SAMPLE_COLS * (size_t)i;
+      for (int q = 0; q < ORC_SAMPLE_COLS; ++q) so[q] = 0.0;
       so[0] = s->sigma;
       for (int c = 0; c < 3; ++c) so[1 + c] = s->rgb[c];
       so[11] = margin;
@@ -554,7 +577,12 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
   double* weight = (double*)malloc(sizeof(double) * (size_t)(n + 1));
   double C[3];
   int32_t used;
-  orc_composite(n, sig_s, rgb_s, delta, f->bg, f->t_stop, C, trans, weight, &used);
+  /* a variant may composite a given number of samples instead of testing the
+   * transmittance (the stop decision taken the other way) */
+  const int forced = var && var->stop >= 0;
+  const int32_t n_c = forced ? (var->stop < n ? var->stop : n) : n;
+  const double t_stop = forced ? 0.0 : f->t_stop;
+  orc_composite(n_c, sig_s, rgb_s, delta, f->bg, t_stop, C, trans, weight, &used);
   h = fnv(h, used);
   if (stop_out) *stop_out = used;
   if (rgb_out)
@@ -567,33 +595,39 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
   for (int c = 0; c < 3; ++c) {
     double g, km;
     int br;
-    L += pixel_loss(f->loss_type, C[c], (double)I[c], f->loss_param, &g, &br, &km) * norm;
+    const int fs = var ? var->loss_sign[c] : 0;
+    L += pixel_loss(f->loss_type, C[c], (double)I[c], f->loss_param, fs, &g, &br, &km) * norm;
     gC[c] = g * norm;
     h = fnv(h, br);
     if (km < kink) kink = km;
   }
   *loss_out = L;
-  /* distance of the stop decision from its threshold, relative to it */
+  /* distance of the stop decision from its threshold, relative to it.  The
+   * test T_{i+1} < t_stop runs after each sample i; the decisions next to the
+   * crossing are T_used (the first below, when the ray stopped before its last
+   * sample) and T_{used-1} (the last one at or above, tested when used >= 2). */
   double stop_margin = INFINITY;
-  if (f->t_stop > 0.0 && used > 0) {
-    double Tl = trans[used], Tp = trans[used - 1];
-    stop_margin = fabs(Tl - f->t_stop) / f->t_stop;
-    if (used < n) {
-      double Tn = Tl * exp(-sig_s[used] * delta);
-      if (fabs(Tn - f->t_stop) / f->t_stop < stop_margin) stop_margin = fabs(Tn - f->t_stop) / f->t_stop;
+  if (t_stop > 0.0 && used > 0) {
+    if (used < n) stop_margin = fabs(trans[used] - t_stop) / t_stop;
+    if (used >= 2) {
+      const double mp = fabs(trans[used - 1] - t_stop) / t_stop;
+      if (mp < stop_margin) stop_margin = mp;
     }
-    (void)Tp;
   }
   if (s_out)
     for (int32_t i = 0; i < n; ++i) {
-      s_out[16 * (size_t)i + 12] = kink;
-      if (stop_margin < s_out[16 * (size_t)i + 11]) s_out[16 * (size_t)i + 11] = stop_margin;
+      s_out[ORC_SAMPLE_COLS * (size_t)i + 12] = kink;
+      s_out[ORC_SAMPLE_COLS * (size_t)i + 16] = stop_margin;
     }
 
   /* backward through the composite, then each sample's networks and encoding */
   double* g_sig = (double*)malloc(sizeof(double) * (size_t)(n + 1));
   double* g_rgb = (double*)malloc(sizeof(double) * 3 * (size_t)(n + 1));
-  orc_composite_grad(n, sig_s, rgb_s, delta, f->bg, f->t_stop, gC, g_sig, g_rgb);
+  orc_composite_grad(n_c, sig_s, rgb_s, delta, f->bg, t_stop, gC, g_sig, g_rgb);
+  for (int32_t i = n_c; i < n; ++i) {
+    g_sig[i] = 0.0;
+    for (int c = 0; c < 3; ++c) g_rgb[3 * i + c] = 0.0;
+  }
   double G[3] = {0, 0, 0}, M[3] = {0, 0, 0}, gd[3] = {0, 0, 0};
   int32_t din = f->din;
   for (int32_t i = 0; i < used; ++i) {
@@ -604,12 +638,12 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
     for (int j = 0; j < HID; ++j) {
       double acc = 0.0;
       for (int c = 0; c < 3; ++c) acc += f->wc3[j * 3 + c] * gz[c];
-      gb2[j] = s->b2[j] > 0.0 ? acc : 0.0;
+      gb2[j] = ((s->b2[j] > 0.0) != s->flip[2][j]) ? acc : 0.0;
     }
     for (int j = 0; j < HID; ++j) {
       double acc = 0.0;
       for (int k = 0; k < HID; ++k) acc += f->wc2[j * HID + k] * gb2[k];
-      gb1[j] = s->b1[j] > 0.0 ? acc : 0.0;
+      gb1[j] = ((s->b1[j] > 0.0) != s->flip[1][j]) ? acc : 0.0;
     }
     for (int q = 0; q < CIN; ++q) {
       double acc = 0.0;
@@ -621,7 +655,7 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
     for (int j = 0; j < HID; ++j) {
       double acc = 0.0;
       for (int o2 = 0; o2 < DOUT; ++o2) acc += f->wd2[j * DOUT + o2] * gh[o2];
-      ga[j] = s->a_pre[j] > 0.0 ? acc : 0.0;
+      ga[j] = ((s->a_pre[j] > 0.0) != s->flip[0][j]) ? acc : 0.0;
     }
     for (int q = 0; q < din; ++q) {
       double acc = 0.0;
@@ -636,7 +670,7 @@ static void shade_ray(const orc_field* f, const double pose64[12], const orc_int
       gp[a] = gx / ext;
     }
     if (s_out) {
-      double* so = s_out + 16 * (size_t)i;
+      double* so = s_out + ORC_SAMPLE_COLS * (size_t)i;
       so[4] = gh[0];
       for (int c = 0; c < 3; ++c) {
         so[5 + c] = gz[c];
@@ -694,8 +728,8 @@ int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
     int32_t used;
     shade_ray(f, poses + 12 * k, in, pix[r], obs, t + ray_offset[r],
               (int32_t)(ray_offset[r + 1] - ray_offset[r]), delta[r],
-              sh_dirs ? sh_dirs + 3 * r : NULL, P, rl + r, rg + 6 * r, c, &used, rs + r,
-              sample_out ? sample_out + 16 * (size_t)ray_offset[r] : NULL);
+              sh_dirs ? sh_dirs + 3 * r : NULL, P, NULL, rl + r, rg + 6 * r, c, &used, rs + r,
+              sample_out ? sample_out + ORC_SAMPLE_COLS * (size_t)ray_offset[r] : NULL, NULL);
     if (rgb)
       for (int q = 0; q < 3; ++q) rgb[3 * r + q] = c[q];
     if (ray_stop) ray_stop[r] = used;
@@ -717,6 +751,59 @@ int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
   }
   if (signature) *signature = h;
   free(rl); free(rg); free(rs);
+  return 0;
+}
+
+int32_t orc_shade_ray_variant(const orc_field* f, const double pose[12], int32_t P,
+                              int32_t pix, const float* obs, const orc_intr* in, const float* t,
+                              int32_t n, float delta, const orc_variant* var, double* sample_out,
+                              int32_t* near_out, double* loss, double g[6], double rgb[3],
+                              int32_t* stop) {
+  if (f->F != 2 || f->din != f->L * f->F || f->din > CIN || f->loss_type < 0 || f->loss_type > 7 ||
+      n < 0 || P < 1 || !var)
+    return 1;
+  double c[3], gg[6], L;
+  int32_t used;
+  uint64_t h;
+  shade_ray(f, pose, in, pix, obs, t, n, delta, NULL, P, var, &L, gg, c, &used, &h, sample_out,
+            near_out);
+  if (loss) *loss = L;
+  if (g)
+    for (int q = 0; q < 6; ++q) g[q] = gg[q];
+  if (rgb)
+    for (int q = 0; q < 3; ++q) rgb[q] = c[q];
+  if (stop) *stop = used;
+  return 0;
+}
+
+int32_t orc_shade_ray_jobs(const orc_field* f, const double* poses, int32_t P, const float* obs,
+                           const orc_intr* in, const float* t, double relu_margin, int32_t n_jobs,
+                           const orc_ray_job* jobs, const int64_t* out_row, double* sample_out,
+                           int32_t* near_out, double* loss, double* g, int32_t n_threads) {
+  if (f->F != 2 || f->din != f->L * f->F || f->din > CIN || f->loss_type < 0 || f->loss_type > 7 ||
+      P < 1 || n_jobs < 0)
+    return 1;
+  if (n_threads < 1) n_threads = 1;
+#pragma omp parallel for schedule(dynamic, 4) num_threads(n_threads)
+  for (int32_t q = 0; q < n_jobs; ++q) {
+    const orc_ray_job* jb = jobs + q;
+    orc_variant var;
+    var.relu_margin = relu_margin;
+    var.relu_pattern = NULL;
+    var.relu_pattern_all = jb->relu_pattern;
+    var.stop = jb->stop;
+    for (int c = 0; c < 3; ++c) var.loss_sign[c] = jb->loss_sign[c];
+    double c3[3], gg[6], L;
+    int32_t used;
+    uint64_t h;
+    shade_ray(f, poses + 12 * (size_t)jb->hyp, in, jb->pix, obs, t + jb->t0, jb->n, jb->delta, NULL,
+              P, &var, &L, gg, c3, &used, &h,
+              sample_out ? sample_out + ORC_SAMPLE_COLS * (size_t)out_row[q] : NULL,
+              near_out ? near_out + out_row[q] : NULL);
+    if (loss) loss[q] = L;
+    if (g)
+      for (int k = 0; k < 6; ++k) g[6 * (size_t)q + k] = gg[k];
+  }
   return 0;
 }
 
@@ -780,7 +867,7 @@ void orc_step_momentum(int32_t K, float* poses, float* momentum, const float* dp
   }
 }
 
-/* Learning rate at global step `step` under the exponential decay of Sec. IV-C
+/* Learning rate at global step `step` under the exponential decay of Sec. IV-D
  * (base `decay_base` per `decay_steps` steps; continuous or stepwise). */
 static double decayed_lr(double lr0, const orc_adam* a, int32_t step) {
   if (a->decay_steps <= 0) return lr0;

@@ -64,21 +64,81 @@ int32_t orc_march(const orc_field* f, int32_t K, const float* poses, int32_t P,
                   const int32_t* pix, const orc_intr* in, int64_t* ray_offset,
                   float* t, int32_t* lattice_j, float* delta, int64_t capacity);
 
+/* Columns of the per-sample output of orc_shade and orc_shade_ray_variant:
+ *   0 sigma, 1..3 rgb, 4 dL/dh0, 5..7 dL/dz (z = pre-sigmoid colour),
+ *   8..10 dL/dp (zeros past the ray's stop), 11 the smallest relative margin of
+ *   the sample's ReLU decisions (|pre-activation| / sum of its terms'
+ *   magnitudes, over density layer 1 and colour layers 1 and 2), 12 its ray's
+ *   distance from the nearest jump of the loss derivative (INFINITY if none),
+ *   13..15 its share of the torque, t d x dL/dp (+ d x its dL/dd through SH when
+ *   the direction path is on), 16 its ray's stop-decision margin (relative
+ *   distance of T_used and T_{used-1} from t_stop; INFINITY without a stop). */
+#define ORC_SAMPLE_COLS 17
+
 /* Shade the frozen sample set (ray_offset, t, delta) for poses given in double,
  * take the loss against `obs` [H][W][3] and its gradient w.r.t. each pose.
  * Outputs (each may be NULL): loss[K], dpose[K][6] = (rotation, translation),
  * rgb[K*P][3], ray_stop[K*P] (samples composited per ray), signature (hash of
- * every discrete decision), sample_out[S][16] = per sample (sigma, rgb[3],
- * dL/dh0, dL/dz[3], dL/dp[3] -- zeros past a ray's stop -- the smallest
- * relative margin of its ReLU and stop decisions, its ray's distance from the
- * nearest jump of the loss derivative, and its share of the torque [3]).  sh_dirs: NULL, or [K*P][3] fixed directions fed to the SH
- * encoding instead of the ray direction (used to freeze that path). */
+ * every discrete decision), sample_out[S][ORC_SAMPLE_COLS] (see above).
+ * sh_dirs: NULL, or [K*P][3] fixed directions fed to the SH encoding instead of
+ * the ray direction (used to freeze that path). */
 int32_t orc_shade(const orc_field* f, int32_t K, const double* poses, int32_t P,
                   const int32_t* pix, const float* obs, const orc_intr* in,
                   const int64_t* ray_offset, const float* t, const float* delta,
                   const double* sh_dirs, double* loss, double* dpose, double* rgb,
                   int32_t* ray_stop, uint64_t* signature, double* sample_out,
                   int32_t n_threads);
+
+/* One ray (pixel `pix` of a hypothesis with pose [12] and P pixels, samples t[n]
+ * at spacing delta) shaded with some of its threshold decisions taken the other
+ * way: each of them has two valid outcomes when the compared value lies within
+ * rounding of its threshold, and a float implementation may take either.
+ *   relu_margin, relu_pattern: the ReLU units of sample i whose margin is below
+ *     relu_margin are numbered b = 0, 1, ... (density layer 1, then colour
+ *     layers 1 and 2, units in order); bit b of relu_pattern[i] flips that unit's
+ *     mask in the backward pass (its forward value is within rounding of 0
+ *     either way).  relu_pattern may be NULL.
+ *   stop: -1 to test the transmittance as the field says, else the number of
+ *     samples composited.
+ *   loss_sign[c]: 0, or +1 / -1 to take channel c's loss derivative on that
+ *     side of r = 0 (L1, Log L1, MAPE, sMAPE).
+ * Outputs: sample_out [n][ORC_SAMPLE_COLS] (or NULL), near_out[n] (the number
+ * of units below relu_margin per sample, or NULL), the ray's loss (already
+ * divided by 3P), its (torque, force) g[6], colour and samples composited.
+ * Returns 1 for an unsupported field. */
+typedef struct {
+  double relu_margin;
+  const int32_t* relu_pattern; /* [n], or NULL: relu_pattern_all for every sample */
+  int32_t relu_pattern_all;
+  int32_t stop;
+  int32_t loss_sign[3];
+} orc_variant;
+int32_t orc_shade_ray_variant(const orc_field* f, const double pose[12], int32_t P,
+                              int32_t pix, const float* obs, const orc_intr* in, const float* t,
+                              int32_t n, float delta, const orc_variant* var, double* sample_out,
+                              int32_t* near_out, double* loss, double g[6], double rgb[3],
+                              int32_t* stop);
+
+/* Many rays at once (OpenMP over the jobs), each shaded like
+ * orc_shade_ray_variant with the job's stop, loss signs and one ReLU pattern
+ * for all its samples (each sample keeps the bits below its own count of near
+ * units), the same relu_margin for all.  Job q reads its samples at t[t0..t0+n)
+ * and pose poses[hyp] (double [12]); its per-sample rows go to
+ * sample_out[out_row[q]..][ORC_SAMPLE_COLS] and near_out[out_row[q]..] (either
+ * may be NULL), its loss to loss[q] and (torque, force) to g[q][6]. */
+typedef struct {
+  int32_t hyp, pix;
+  int64_t t0;
+  int32_t n;
+  float delta;
+  int32_t stop;
+  int32_t loss_sign[3];
+  int32_t relu_pattern;
+} orc_ray_job;
+int32_t orc_shade_ray_jobs(const orc_field* f, const double* poses, int32_t P, const float* obs,
+                           const orc_intr* in, const float* t, double relu_margin, int32_t n_jobs,
+                           const orc_ray_job* jobs, const int64_t* out_row, double* sample_out,
+                           int32_t* near_out, double* loss, double* g, int32_t n_threads);
 
 /* Pieces exposed for pinning. */
 void orc_encode(const orc_field* f, const float x32[3], const double x64[3],

@@ -1,0 +1,119 @@
+"""The GPU parity checker (tests/gpu_common.py) on the CPU: fed the oracle's
+own results it passes; fed shares where set-aside rays took another valid
+outcome of their threshold decisions it passes and reports them; fed a
+corrupted sample, set aside or not, it fails."""
+import math
+
+import numpy as np
+import pytest
+
+from paper_2210_10108_amd import synth
+from tests import gpu_common as G
+
+
+@pytest.fixture
+def early_stop_case(oracle_lib, monkeypatch):
+    # generous margins set many samples and rays aside
+    monkeypatch.setattr(G, "MARGIN_RELU", 0.02)
+    monkeypatch.setattr(G, "MARGIN_STOP", 0.05)
+    monkeypatch.setattr(G, "MAX_SET_ASIDE", 1.0)
+    case = G.make_case("tiny32", K=3, P=60, march_mode=1, step=math.sqrt(3) / 96,
+                       max_samples=600, t_stop=5e-2, occ_res=16, density_bias=2.5,
+                       occ_bits=synth.occupancy_pattern("sphere", 16), loss_type=1,
+                       loss_param=0.1)
+    of = oracle_lib.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    alt = G.Alt(of, case.poses, case.pix, obs, case.intr)
+    return case, of, obs, ref, alt
+
+
+def natural_gpu(ref):
+    so = ref["samples"]
+    return np.concatenate([so[:, 13:16], so[:, 8:11]], axis=1).copy()
+
+
+def test_oracle_results_pass(early_stop_case):
+    case, of, obs, ref, alt = early_stop_case
+    st = G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=natural_gpu(ref),
+                                  alt=alt, label="self")
+    relu, ray = G.set_aside(ref["samples"])
+    assert relu.sum() > 10 and ray.sum() > 10
+    assert st["rays_checked"] > 5 and st["rays_other_decision"] == 0
+    assert st["samples_other_relu"] == 0
+
+
+def test_other_valid_outcomes_pass(early_stop_case, oracle_lib):
+    """Rays whose stop is at the threshold composite one sample more, and
+    samples at a ReLU threshold flip that unit: the checker accepts both."""
+    case, of, obs, ref, alt = early_stop_case
+    off, t, _, delta = ref["march"]
+    so = ref["samples"]
+    gpu = natural_gpu(ref)
+    K, P = case.pix.shape
+    relu, ray = G.set_aside(so)
+    n_stop = n_relu = 0
+    dpose = ref["dpose"].copy()
+    for r in range(K * P):
+        a, b = int(off[r]), int(off[r + 1])
+        if b - a < 3:
+            continue
+        k = r // P
+        used = int(ref["stop"][r])
+        if so[a, 16] < G.MARGIN_STOP and used < b - a and n_stop < 4:
+            v = of.shade_ray_variant(case.poses[k], P, case.pix[k, r % P], obs, case.intr, t[a:b],
+                                     delta[r], stop=used + 1)
+        elif relu[a:b].any() and not ray[a:b].any() and n_relu < 4:
+            v = of.shade_ray_variant(case.poses[k], P, case.pix[k, r % P], obs, case.intr, t[a:b],
+                                     delta[r], relu_margin=G.MARGIN_RELU,
+                                     relu_pattern=np.ones(b - a, np.int32))
+            if not np.any(v["near"] > 0):
+                continue
+            n_relu += 1
+        else:
+            continue
+        n_stop += v["stop"] != used
+        new = np.concatenate([v["samples"][:, 13:16], v["samples"][:, 8:11]], axis=1)
+        dpose[k] += np.concatenate([new[:, :3].sum(0), new[:, 3:].sum(0)]) - \
+            np.concatenate([gpu[a:b, :3].sum(0), gpu[a:b, 3:].sum(0)])
+        gpu[a:b] = new
+    assert n_stop >= 1 and n_relu >= 1
+    # the altered totals are not the oracle's: allow the difference the
+    # altered rays make, then the checker must attribute it to valid outcomes
+    st = G.assert_loss_grad_close(ref["loss"], dpose, ref, gpu_samples=gpu, alt=alt,
+                                  grad_rtol=1.0, label="alternatives")
+    assert st["rays_other_decision"] >= 1 and st["samples_other_relu"] >= 1
+
+
+def test_a_corrupted_set_aside_sample_fails(early_stop_case):
+    case, of, obs, ref, alt = early_stop_case
+    gpu = natural_gpu(ref)
+    relu, ray = G.set_aside(ref["samples"])
+    i = int(np.flatnonzero(relu & ~ray)[0])
+    gpu[i, 3:] *= 1.5
+    gpu[i, 3:] += 0.01 * np.abs(gpu[:, 3:]).max()
+    with pytest.raises(AssertionError, match="no valid outcome"):
+        G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=gpu, alt=alt,
+                                 grad_rtol=1.0)
+
+
+def test_a_corrupted_plain_sample_fails(early_stop_case, monkeypatch):
+    case, of, obs, ref, alt = early_stop_case
+    monkeypatch.setattr(G, "MARGIN_RELU", 1e-6)
+    monkeypatch.setattr(G, "MARGIN_STOP", 1e-6)
+    monkeypatch.setattr(G, "MARGIN_KINK", 1e-6)
+    gpu = natural_gpu(ref)
+    relu, ray = G.set_aside(ref["samples"])
+    i = int(np.flatnonzero(~(relu | ray))[0])
+    gpu[i, 3] += 0.01 * np.abs(gpu[:, 3:]).max()
+    with pytest.raises(AssertionError, match="per-sample share"):
+        G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=gpu, alt=alt,
+                                 grad_rtol=1.0)
+
+
+def test_the_raw_gradient_tolerance_is_asserted(early_stop_case):
+    case, of, obs, ref, alt = early_stop_case
+    dpose = ref["dpose"].copy()
+    dpose[1] *= 1.02
+    with pytest.raises(AssertionError):
+        G.assert_loss_grad_close(ref["loss"], dpose, ref)
