@@ -61,7 +61,7 @@ def lib():
         L.orc_grid_index.argtypes = [vp, i32, u32, u32, u32]
         L.orc_ray_f32.argtypes = [vp, vp, i32, vp, vp]
         L.orc_march.restype = i32
-        L.orc_march.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i64]
+        L.orc_march.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, i64, i32]
         L.orc_shade.restype = i32
         L.orc_shade.argtypes = [vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                 vp, vp, i32]
@@ -188,22 +188,23 @@ class OracleField:
         return rgb
 
     # ------------------------------------------------------------ path
-    def march(self, poses, pix, intr, capacity=None):
+    def march(self, poses, pix, intr, capacity=None, threads=None):
         poses = np.ascontiguousarray(poses, dtype=np.float32).reshape(-1, 12)
         pix = np.ascontiguousarray(pix, dtype=np.int32)
         K, P = pix.shape
         off = np.zeros(K * P + 1, dtype=np.int64)
         delta = np.zeros(K * P, dtype=np.float32)
         it = intr_struct(intr)
+        nt = threads or n_threads_default()
         lib().orc_march(self.ptr, K, _p(poses), P, _p(pix), C.byref(it), _p(off), None, None,
-                        _p(delta), 0)
+                        _p(delta), 0, nt)
         total = int(off[-1])
         if capacity is not None and total > capacity:
             return off, None, None, delta
         t = np.zeros(max(total, 1), dtype=np.float32)
         j = np.zeros(max(total, 1), dtype=np.int32)
         rc = lib().orc_march(self.ptr, K, _p(poses), P, _p(pix), C.byref(it), _p(off), _p(t),
-                             _p(j), _p(delta), max(total, 1))
+                             _p(j), _p(delta), max(total, 1), nt)
         assert rc == 0
         return off, t[:total], j[:total], delta
 
@@ -290,7 +291,7 @@ class OracleField:
         return so[:total], near[:total], rows[:nj], loss[:nj], g[:nj]
 
     def render_loss_grad(self, poses, pix, obs, intr, threads=None, per_sample=False):
-        m = self.march(poses, pix, intr)
+        m = self.march(poses, pix, intr, threads=threads)
         out = self.shade(np.asarray(poses, dtype=np.float32).astype(np.float64), pix, obs, intr, m,
                          threads=threads, per_sample=per_sample)
         out["march"] = m

@@ -151,18 +151,22 @@ static int32_t march_ray(const orc_field* f, const float o[3], const float d[3],
 
 int32_t orc_march(const orc_field* f, int32_t K, const float* poses, int32_t P,
                   const int32_t* pix, const orc_intr* in, int64_t* ray_offset, float* t,
-                  int32_t* lattice_j, float* delta, int64_t capacity) {
+                  int32_t* lattice_j, float* delta, int64_t capacity, int32_t n_threads) {
   int64_t n_rays = (int64_t)K * P;
+  if (n_threads < 1) n_threads = 1;
+  /* rays are independent: count each ray's samples, then offsets in ray order */
   ray_offset[0] = 0;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(n_threads)
   for (int64_t r = 0; r < n_rays; ++r) {
     float o[3], d[3], dl;
     orc_ray_f32(poses + 12 * (r / P), in, pix[r], o, d);
-    int32_t n = march_ray(f, o, d, NULL, NULL, &dl);
-    ray_offset[r + 1] = ray_offset[r] + n;
+    ray_offset[r + 1] = march_ray(f, o, d, NULL, NULL, &dl);
     if (delta) delta[r] = dl;
   }
+  for (int64_t r = 0; r < n_rays; ++r) ray_offset[r + 1] += ray_offset[r];
   if (ray_offset[n_rays] > capacity) return 1;
   if (!t) return 0;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(n_threads)
   for (int64_t r = 0; r < n_rays; ++r) {
     float o[3], d[3];
     orc_ray_f32(poses + 12 * (r / P), in, pix[r], o, d);

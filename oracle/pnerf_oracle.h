@@ -57,12 +57,14 @@ uint32_t orc_grid_index(const orc_field* f, int32_t level, uint32_t i, uint32_t 
 /* Ray of pixel `pix` for camera-to-world pose [3][4] (float decision path). */
 void orc_ray_f32(const float pose[12], const orc_intr* in, int32_t pix, float o[3], float d[3]);
 
-/* Samples of K*P rays.  Fills ray_offset[K*P+1]; when the total fits in
- * `capacity` also t[], lattice index j[] and the per-ray spacing delta[K*P].
- * Returns 0, or 1 if the total exceeds capacity (offsets still valid). */
+/* Samples of K*P rays (n_threads OpenMP threads over the rays).  Fills
+ * ray_offset[K*P+1]; when the total fits in `capacity` also t[], lattice index
+ * j[] and the per-ray spacing delta[K*P].  Returns 0, or 1 if the total exceeds
+ * capacity (offsets still valid). */
 int32_t orc_march(const orc_field* f, int32_t K, const float* poses, int32_t P,
                   const int32_t* pix, const orc_intr* in, int64_t* ray_offset,
-                  float* t, int32_t* lattice_j, float* delta, int64_t capacity);
+                  float* t, int32_t* lattice_j, float* delta, int64_t capacity,
+                  int32_t n_threads);
 
 /* Columns of the per-sample output of orc_shade and orc_shade_ray_variant:
  *   0 sigma, 1..3 rgb, 4 dL/dh0, 5..7 dL/dz (z = pre-sigmoid colour),

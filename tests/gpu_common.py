@@ -81,7 +81,8 @@ def rel_l2(a, b):
 MARGIN_RELU = 1e-4     # |pre-activation| / sum of its terms' magnitudes
 MARGIN_STOP = 1e-3     # |T - t_stop| / t_stop
 MARGIN_KINK = 1e-4     # |r| at a jump of the loss derivative
-MAX_SET_ASIDE = 0.10   # at most this share of a test's samples may be set aside
+MAX_SET_ASIDE = 0.10   # at most this share of a test's samples (ReLU) or rays (stop,
+                       # loss derivative) may be set aside
 SAMPLE_TOL = 2e-3      # per-sample shares, relative to the hypothesis's largest
 MAX_FLIP_BITS = 4      # ReLU units per sample whose both outcomes are tried
 
@@ -104,8 +105,14 @@ class Alt:
     intr: dict
 
 
-def _shares(so):
-    return np.concatenate([so[:, 13:16], so[:, 8:11]], axis=1)
+STAGE_TOL = 1e-3       # dL/dh0 and dL/dz per sample, relative to the hypothesis's largest
+
+
+def _shares(so, stage=False):
+    """Oracle per-sample vector in the GPU's layout: torque share [3], force [3],
+    and with `stage` also dL/dh0 and dL/dz [3]."""
+    cols = [so[:, 13:16], so[:, 8:11]] + ([so[:, 4:5], so[:, 5:8]] if stage else [])
+    return np.concatenate(cols, axis=1)
 
 
 def _ray_variants(ref, r, n, alt, loss_type):
@@ -140,14 +147,14 @@ def _ray_variants(ref, r, n, alt, loss_type):
     return [(st, sg) for st in stops for sg in signs]
 
 
-def _check_set_aside(ref, i, P, sg_all, g0, tol, relu, rayamb, alt, stats):
+def _check_set_aside(ref, i, P, sg_all, g0, tol, relu, rayamb, alt, stats, stage):
     """Match every set-aside sample of hypothesis i; returns the oracle shares
     under the decisions the GPU took, for all samples of the hypothesis."""
     from oracle import oracle as O
     off = ref["march"][0]
     s0 = int(off[i * P])
     so_h = ref["samples"][s0:int(off[(i + 1) * P])]
-    matched = _shares(so_h).copy()
+    matched = _shares(so_h, stage).copy()
     flag = relu | rayamb
     if not flag.any():
         return matched
@@ -190,7 +197,8 @@ def _check_set_aside(ref, i, P, sg_all, g0, tol, relu, rayamb, alt, stats):
             if rr != r or pat != 0:
                 continue
             # per sample: the candidates of this ray-level decision set
-            cand = np.stack([_shares(out[(r, st, sgn, p)]) for p in range(1 << int(m_i.max()))])
+            cand = np.stack([_shares(out[(r, st, sgn, p)], stage)
+                             for p in range(1 << int(m_i.max()))])
             valid = np.arange(len(cand))[:, None] < (1 << m_i)[None, :]       # [patterns][samples]
             err = np.abs(cand - sg[None]) - tol[None, None, :]
             fits = np.all(err <= 0, axis=2) & valid
@@ -199,7 +207,7 @@ def _check_set_aside(ref, i, P, sg_all, g0, tol, relu, rayamb, alt, stats):
                 best = (st, sgn, cand[pick, np.arange(b - a)], pick)
                 break
         if best is None:
-            nat = _shares(out[(r, -1, (0, 0, 0), 0)])
+            nat = _shares(out[(r, -1, (0, 0, 0), 0)], stage)
             worst = int(np.argmax(np.abs(nat - sg).max(1)))
             raise AssertionError(
                 f"ray {r}: no valid outcome of its threshold decisions matches the GPU; "
@@ -219,18 +227,21 @@ def assert_loss_grad_close(loss_gpu, dpose_gpu, ref, hyps=None, gpu_samples=None
                            gpu_ranges=None, alt=None, loss_rtol=LOSS_RTOL, grad_rtol=GRAD_RTOL,
                            label=""):
     """Per-hypothesis parity: loss within loss_rtol and the pose gradient within
-    grad_rtol relative L2 of the oracle's.  With the GPU's per-sample shares
-    (pnerf_field_inspect what=3: torque and force of every sample) also: the
-    same sample count per hypothesis, every sample's shares element by element,
-    where a sample's decisions are next to a threshold the shares of one of its
-    valid outcomes (needs `alt`), and the gradient within grad_rtol of the
-    oracle's under the outcomes the GPU took."""
+    grad_rtol relative L2 of the oracle's.  With the GPU's per-sample values
+    (pnerf_field_inspect what=3: torque and force share of every sample, [n][6];
+    or [n][10] with dL/dh0 and dL/dz appended, what=1 and 2) also: the same
+    sample count per hypothesis, every sample's values element by element, where
+    a sample's decisions are next to a threshold the values of one of its valid
+    outcomes (needs `alt`), and the gradient within grad_rtol of the oracle's
+    under the outcomes the GPU took."""
     hyps = list(range(len(ref["loss"])) if hyps is None else hyps)
     K_sub = len(ref["loss"])
     off = ref["march"][0]
     P = (len(off) - 1) // K_sub
-    stats = dict(samples=0, relu_set_aside=0, ray_set_aside=0, rays_checked=0,
-                 rays_other_decision=0, samples_other_relu=0, max_grad_err=0.0)
+    stats = dict(samples=0, rays=0, relu_set_aside=0, ray_set_aside=0, rays_set_aside=0,
+                 rays_checked=0,
+                 rays_other_decision=0, samples_other_relu=0, max_grad_err=0.0,
+                 raw_over_tol=[])
     for i, k in enumerate(hyps):
         lo, lg = ref["loss"][i], float(loss_gpu[k])
         assert abs(lg - lo) <= loss_rtol * abs(lo) + 1e-12, (k, lg, lo)
@@ -238,9 +249,13 @@ def assert_loss_grad_close(loss_gpu, dpose_gpu, ref, hyps=None, gpu_samples=None
         g_gpu = np.asarray(dpose_gpu[k], np.float64)
         e = rel_l2(g_gpu, g_orc)
         stats["max_grad_err"] = max(stats["max_grad_err"], e)
-        assert e <= grad_rtol, (k, e, g_gpu, g_orc)
+        # the oracle's gradient is one of several valid values when decisions sit
+        # at a threshold: beyond the tolerance only if the per-sample check below
+        # shows the GPU took another valid outcome and matches that gradient
+        assert e <= grad_rtol or gpu_samples is not None, (k, e, g_gpu, g_orc)
         if gpu_samples is None:
             continue
+        other_before = stats["rays_other_decision"] + stats["samples_other_relu"]
         s0, s1 = int(off[i * P]), int(off[(i + 1) * P])
         g0, g1 = gpu_ranges[i] if gpu_ranges is not None else (s0, s1)
         assert g1 - g0 == s1 - s0, (k, g1 - g0, s1 - s0)
@@ -250,22 +265,40 @@ def assert_loss_grad_close(loss_gpu, dpose_gpu, ref, hyps=None, gpu_samples=None
         stats["samples"] += s1 - s0
         stats["relu_set_aside"] += int((relu & ~rayamb).sum())
         stats["ray_set_aside"] += int(rayamb.sum())
-        orc = _shares(so)
-        tol = SAMPLE_TOL * np.concatenate([np.full(3, np.abs(orc[:, :3]).max(initial=0.0)),
-                                           np.full(3, np.abs(orc[:, 3:]).max(initial=0.0))])
+        ray_first = (off[i * P:(i + 1) * P] - s0).astype(np.int64)
+        has = off[i * P + 1:(i + 1) * P + 1] > off[i * P:(i + 1) * P]
+        stats["rays"] += int(has.sum())
+        stats["rays_set_aside"] += int(rayamb[ray_first[has]].sum()) if has.any() else 0
+        stage = sg.shape[1] == 10
+        orc = _shares(so, stage)
+        big = lambda a: np.abs(a).max(initial=0.0)
+        # the torque share t d x dL/dp inherits the force's error times t:
+        # |t d x e| <= t |e| (it can be far smaller than t |dL/dp| where dL/dp
+        # runs along the ray, so its own largest value does not bound it)
+        t_max = big(ref["march"][1][s0:s1]) if s1 > s0 else 0.0
+        f_tol = SAMPLE_TOL * big(orc[:, 3:6])
+        tol = np.concatenate([np.full(3, t_max * f_tol), np.full(3, f_tol)])
+        if stage:
+            tol = np.concatenate([tol, [STAGE_TOL * big(orc[:, 6])],
+                                  np.full(3, STAGE_TOL * big(orc[:, 7:10]))])
         ok = ~(relu | rayamb)
         bad = np.abs(sg[ok] - orc[ok]) > tol[None, :]
         assert not bad.any(), (k, "per-sample share", np.argwhere(bad)[:3], tol)
         if (relu | rayamb).any():
             assert alt is not None, "set-aside samples need the oracle's alternatives"
             matched = _check_set_aside(ref, i, P, np.asarray(gpu_samples, np.float64), g0, tol,
-                                       relu, rayamb, alt, stats)
-            g_m = np.concatenate([matched[:, :3].sum(0), matched[:, 3:].sum(0)])
+                                       relu, rayamb, alt, stats, stage)
+            g_m = np.concatenate([matched[:, :3].sum(0), matched[:, 3:6].sum(0)])
             em = rel_l2(g_gpu, g_m)
             assert em <= grad_rtol, (k, "under the GPU's decisions", em, g_gpu, g_m)
+        if e > grad_rtol:
+            took_other = stats["rays_other_decision"] + stats["samples_other_relu"] > other_before
+            assert took_other, (k, "gradient off with every decision as the oracle's", e, g_gpu,
+                                g_orc)
+            stats["raw_over_tol"].append((int(k), round(float(e), 5), round(float(em), 5)))
     if stats["samples"]:
-        aside = stats["relu_set_aside"] + stats["ray_set_aside"]
-        assert aside <= MAX_SET_ASIDE * stats["samples"], stats
+        assert stats["relu_set_aside"] <= MAX_SET_ASIDE * stats["samples"], stats
+        assert stats["rays_set_aside"] <= MAX_SET_ASIDE * stats["rays"], stats
     import sys
     sys.stderr.write(f"[parity] {label}: {stats}\n")
     sys.stderr.flush()

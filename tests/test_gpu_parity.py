@@ -148,7 +148,8 @@ def check_full(pn, case, obs, ref, of, hyps=None):
     ranges = [(int(ex["off"][k * P]), int(ex["off"][(k + 1) * P])) for k in hyps]
     alt = G.Alt(of, case.poses[hyps], case.pix[hyps], obs, case.intr)
     label = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
-    return G.assert_loss_grad_close(loss, dpose, ref, hyps=hyps, gpu_samples=ex["out6"],
+    per_sample = np.concatenate([ex["out6"], ex["gh0"][:, None], ex["gz"].reshape(-1, 3)], axis=1)
+    return G.assert_loss_grad_close(loss, dpose, ref, hyps=hyps, gpu_samples=per_sample,
                                     gpu_ranges=ranges, alt=alt, label=label), ex
 
 
@@ -163,14 +164,10 @@ def test_loss_grad_tiny(pn, overrides):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    # per sample: torque and force shares, and the stage values d loss / d h0
+    # and d loss / d z, element by element (check_full)
     stats, ex = check_full(pn, case, obs, ref, of)
     assert stats["samples"] == int(ref["march"][0][-1])
-    # stage parity element by element: d loss / d h0 and d loss / d z of every sample
-    so = ref["samples"]
-    relu, ray = G.set_aside(so)
-    ok = ~(relu | ray)
-    assert np.abs(ex["gh0"][ok] - so[ok, 4]).max() <= 1e-3 * np.abs(so[:, 4]).max()
-    assert np.abs(ex["gz"][ok] - so[ok, 5:8]).max() <= 1e-3 * np.abs(so[:, 5:8]).max()
 
 
 @pytest.mark.parametrize("n_levels,dense,sh_dir", [(8, 0, 0), (12, 1, 0), (16, 1, 0), (16, 1, 1),
@@ -484,10 +481,18 @@ def test_loss_grad_tiny_fp16_storage(pn, overrides):
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
+_OCC_CACHE = {}
+
+
 def with_oracle_occupancy(case, R, thr):
-    of0 = O.OracleField(dataclasses.replace(case.spec, occ_res=0, occ_bits=None))
-    bits = of0.build_occupancy(R, thr)
-    return dataclasses.replace(case, spec=dataclasses.replace(case.spec, occ_bits=bits))
+    """The case with the occupancy grid the oracle builds from the field's
+    density (cached per field: the 256^3 grid takes seconds)."""
+    key = (case.w.name, case.spec.log2_table, case.spec.param_dtype, R, thr,
+           float(np.asarray(case.spec.table).ravel()[:8].astype(np.float64).sum()))
+    if key not in _OCC_CACHE:
+        of0 = O.OracleField(dataclasses.replace(case.spec, occ_res=0, occ_bits=None))
+        _OCC_CACHE[key] = of0.build_occupancy(R, thr)
+    return dataclasses.replace(case, spec=dataclasses.replace(case.spec, occ_bits=_OCC_CACHE[key]))
 
 
 def check_sampled_hypotheses(pn, case, hyps):
@@ -564,3 +569,61 @@ def test_loss_grad_ngp800_bump_full_batch_sampled_hypotheses(pn):
     case = with_oracle_occupancy(G.make_case("ngp800_bump_occ128"), w.occ_res, w.occ_threshold)
     n = check_sampled_hypotheses(pn, case, [0, 31, 63])
     assert n > 0
+
+
+# ------------------------------------- full-size workloads: colour, per sample
+def workload_case(name):
+    """The workload's full batch (fp16 storage where the workload says so) with
+    the oracle's density-built occupancy grid."""
+    w = synth.WORKLOADS[name]
+    case = f16_case(name) if w.param_dtype == "f16" else G.make_case(name)
+    return with_oracle_occupancy(case, w.occ_res, w.occ_threshold)
+
+
+@pytest.mark.parametrize("name,hyps", [("ngp800_occ128", [0, 37, 63]),
+                                       ("cam640_f16_occ128", [0, 129, 255]),
+                                       ("large4m_occ256", [0, 600, 1023])])
+def test_render_colour_full_batch_sampled_hypotheses(pn, name, hyps):
+    """pnerf_render over the whole batch (chunked as the library decides); the
+    oracle renders the sampled hypotheses: colour within 2e-3 absolute
+    (Sec. III, volume rendering), on lattice marching with occupancy and early
+    stop, the fp16-stored field and the 2^21-entry [-2,2]^3 field."""
+    import torch
+    case = workload_case(name)
+    f = pn.Field(case.spec)
+    rgb = f.render(G.to_dev(case.poses), G.to_dev(case.pix), case.intr)
+    torch.cuda.synchronize()
+    got = rgb.cpu().numpy()
+    f.close()
+    of = O.OracleField(case.spec)
+    ref = of.render(case.poses[hyps], case.pix[hyps], case.intr)
+    err = np.abs(got[hyps] - ref).max()
+    sys.stderr.write(f"[parity] {name} colour: max abs error {err:.3g}\n")
+    assert err <= G.COLOR_ATOL
+    assert ref.max() > 0.05
+
+
+@pytest.mark.parametrize("name,hyps", [("cam640_f16_occ128", [3, 200]),
+                                       ("large4m_occ256", [5, 700])])
+def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps):
+    """The sampled hypotheses of a full-size workload as a batch of their own
+    (one chunk, so every sample can be inspected): per-hypothesis sample counts
+    exactly, per-sample torque and force shares and the stage values d loss /
+    d h0 and d loss / d z, loss and pose gradient (Eq. 2, Eq. 3)."""
+    full = workload_case(name)
+    case = dataclasses.replace(full, poses=full.poses[hyps], pix=full.pix[hyps])
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, _ = check_full(pn, case, obs, ref, of)
+    assert stats["samples"] == int(ref["march"][0][-1]) > 100_000
+
+
+def test_march_large_scene_density_grid_bitexact(pn):
+    """200 hypotheses of the [-2,2]^3 workload on its density-built 256^3 grid
+    (the random field sets every cell): ray offsets, sample distances and
+    lattice indices bit-exact."""
+    w = synth.WORKLOADS["large4m_occ256"]
+    case = with_oracle_occupancy(G.make_case("large4m_occ256"), w.occ_res, w.occ_threshold)
+    case = dataclasses.replace(case, poses=case.poses[:200], pix=case.pix[:200])
+    assert check_march(pn, case) > 50_000_000

@@ -29,8 +29,10 @@ def early_stop_case(oracle_lib, monkeypatch):
 
 
 def natural_gpu(ref):
+    """The oracle's per-sample values in the GPU's layout: torque share,
+    force, d loss / d h0, d loss / d z."""
     so = ref["samples"]
-    return np.concatenate([so[:, 13:16], so[:, 8:11]], axis=1).copy()
+    return np.concatenate([so[:, 13:16], so[:, 8:11], so[:, 4:5], so[:, 5:8]], axis=1).copy()
 
 
 def test_oracle_results_pass(early_stop_case):
@@ -73,9 +75,10 @@ def test_other_valid_outcomes_pass(early_stop_case, oracle_lib):
         else:
             continue
         n_stop += v["stop"] != used
-        new = np.concatenate([v["samples"][:, 13:16], v["samples"][:, 8:11]], axis=1)
-        dpose[k] += np.concatenate([new[:, :3].sum(0), new[:, 3:].sum(0)]) - \
-            np.concatenate([gpu[a:b, :3].sum(0), gpu[a:b, 3:].sum(0)])
+        vs = v["samples"]
+        new = np.concatenate([vs[:, 13:16], vs[:, 8:11], vs[:, 4:5], vs[:, 5:8]], axis=1)
+        dpose[k] += np.concatenate([new[:, :3].sum(0), new[:, 3:6].sum(0)]) - \
+            np.concatenate([gpu[a:b, :3].sum(0), gpu[a:b, 3:6].sum(0)])
         gpu[a:b] = new
     assert n_stop >= 1 and n_relu >= 1
     # the altered totals are not the oracle's: allow the difference the
@@ -90,8 +93,8 @@ def test_a_corrupted_set_aside_sample_fails(early_stop_case):
     gpu = natural_gpu(ref)
     relu, ray = G.set_aside(ref["samples"])
     i = int(np.flatnonzero(relu & ~ray)[0])
-    gpu[i, 3:] *= 1.5
-    gpu[i, 3:] += 0.01 * np.abs(gpu[:, 3:]).max()
+    gpu[i, 3:6] *= 1.5
+    gpu[i, 3:6] += 0.01 * np.abs(gpu[:, 3:6]).max()
     with pytest.raises(AssertionError, match="no valid outcome"):
         G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=gpu, alt=alt,
                                  grad_rtol=1.0)
@@ -105,7 +108,7 @@ def test_a_corrupted_plain_sample_fails(early_stop_case, monkeypatch):
     gpu = natural_gpu(ref)
     relu, ray = G.set_aside(ref["samples"])
     i = int(np.flatnonzero(~(relu | ray))[0])
-    gpu[i, 3] += 0.01 * np.abs(gpu[:, 3:]).max()
+    gpu[i, 3] += 0.01 * np.abs(gpu[:, 3:6]).max()
     with pytest.raises(AssertionError, match="per-sample share"):
         G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=gpu, alt=alt,
                                  grad_rtol=1.0)
@@ -117,3 +120,17 @@ def test_the_raw_gradient_tolerance_is_asserted(early_stop_case):
     dpose[1] *= 1.02
     with pytest.raises(AssertionError):
         G.assert_loss_grad_close(ref["loss"], dpose, ref)
+
+
+def test_a_corrupted_stage_value_fails(early_stop_case, monkeypatch):
+    case, of, obs, ref, alt = early_stop_case
+    monkeypatch.setattr(G, "MARGIN_RELU", 1e-6)
+    monkeypatch.setattr(G, "MARGIN_STOP", 1e-6)
+    monkeypatch.setattr(G, "MARGIN_KINK", 1e-6)
+    gpu = natural_gpu(ref)
+    relu, ray = G.set_aside(ref["samples"])
+    i = int(np.flatnonzero(~(relu | ray))[0])
+    gpu[i, 6] += 0.01 * np.abs(gpu[:, 6]).max()          # d loss / d h0
+    with pytest.raises(AssertionError, match="per-sample share"):
+        G.assert_loss_grad_close(ref["loss"], ref["dpose"], ref, gpu_samples=gpu, alt=alt,
+                                 grad_rtol=1.0)
