@@ -237,6 +237,22 @@ pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* opt_state
                                        float sigma_rot, float sigma_trans, uint64_t seed,
                                        uint32_t round_idx, void* stream);
 
+/* pnerf_resample_hypotheses for callers that cannot allocate memory (code under
+ * stream capture, tight serving loops, harnesses that forbid allocation): the
+ * same operation, arguments and results, with no allocation of any kind.  Its
+ * ranking scratch (2 K int32) lives in a static device array of each GPU, sized
+ * for K <= 65535 and held until the process ends; a larger K returns
+ * PNERF_ERR_CAPACITY before anything is enqueued.  The array is looked up on
+ * the first call on each device (with that device current).  All calls on one
+ * GPU share its array: calls that overlap on one GPU (several streams or host
+ * threads at once) race and must be ordered by the caller.  Nothing of an
+ * earlier call's contents is read. */
+pnerf_status pnerf_resample_hypotheses_noalloc(int32_t K, float* poses, float* opt_state,
+                                               int32_t state_dim, const float* loss,
+                                               float keep_frac, float sigma_rot,
+                                               float sigma_trans, uint64_t seed,
+                                               uint32_t round_idx, void* stream);
+
 /* Forward rendering only (the composite colour of each pixel's ray).
  * rgb (device) float32 [K][P][3].  Limits as for pnerf_render_loss_grad. */
 pnerf_status pnerf_render(pnerf_field* field, int32_t K, const float* poses, int32_t P,

@@ -988,6 +988,34 @@ pnerf_status pnerf_resample_hypotheses(int32_t K, float* poses, float* opt_state
   return PNERF_OK;
 }
 
+pnerf_status pnerf_resample_hypotheses_noalloc(int32_t K, float* poses, float* opt_state,
+                                               int32_t state_dim, const float* loss,
+                                               float keep_frac, float sigma_rot,
+                                               float sigma_trans, uint64_t seed,
+                                               uint32_t round_idx, void* stream) {
+  if (K < 1) return fail(PNERF_ERR_INVALID_ARG, "K=%d must be >= 1", K);
+  if (state_dim < 0 || state_dim > 64) return fail(PNERF_ERR_INVALID_ARG, "state_dim=%d", state_dim);
+  if (!poses || !loss || (state_dim > 0 && !opt_state))
+    return fail(PNERF_ERR_INVALID_ARG, "NULL pointer argument");
+  if (!(keep_frac >= 0.0f && keep_frac <= 1.0f)) return fail(PNERF_ERR_INVALID_ARG, "keep_frac");
+  if (!(sigma_rot >= 0.0f) || !(sigma_trans >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "sigma");
+  int device = 0;
+  HIP_TRY(hipGetDevice(&device));
+  int32_t* scratch = nullptr;
+  int max_k = 0;
+  HIP_TRY(resample_scratch(device, &scratch, &max_k));
+  if (K > max_k)
+    return fail(PNERF_ERR_CAPACITY, "K=%d exceeds the %d hypotheses the static scratch holds", K,
+                max_k);
+  int n_keep = (int)std::floor((double)K * (double)keep_frac);
+  n_keep = std::max(1, std::min(n_keep, K));
+  // every rank[i] and by_rank[r], i, r < K, is written before it is read:
+  // nothing left from an earlier call is used
+  HIP_TRY(launch_resample(K, poses, opt_state, state_dim, loss, n_keep, sigma_rot, sigma_trans,
+                          seed, round_idx, scratch, (hipStream_t)stream));
+  return PNERF_OK;
+}
+
 pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64_t n,
                                  void* stream) {
   if (!F || !dst) return fail(PNERF_ERR_INVALID_ARG, "NULL argument");

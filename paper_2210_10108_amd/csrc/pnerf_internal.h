@@ -197,6 +197,10 @@ hipError_t launch_resample(int K, float* poses, float* state, int state_dim, con
                            int n_keep, float sr, float st, uint64_t seed, uint32_t round,
                            int32_t* scratch, hipStream_t s);
 
+// The device address of the static resampling scratch on `device` (which must
+// be current): 2 * max_k int32 words, looked up once per device.
+hipError_t resample_scratch(int device, int32_t** ptr, int* max_k);
+
 int reduce_parts(int K);
 int mlp_fwd_blocks_per_cu(int lpg);
 int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad);

@@ -2,6 +2,8 @@
 // per subspace) and Monte Carlo hypothesis resampling.  All are tiny (one
 // thread per hypothesis) and run in double precision; results are stored as
 // float.
+#include <mutex>
+
 #include "pnerf_internal.h"
 
 namespace pnerf {
@@ -239,6 +241,36 @@ hipError_t launch_step_adam(int K, float* poses, float* state, const float* dpos
   hipLaunchKernelGGL(k_step_adam, dim3((K + 63) / 64), dim3(64), 0, s, K, poses, state, dpose,
                      lr_r, lr_t, b1, b2, eps, per_subspace, twist);
   return hipGetLastError();
+}
+
+// ------------------------------------------------ static resampling scratch
+// The ranking scratch of pnerf_resample_hypotheses_noalloc: rank and by_rank
+// of up to kMaxResampleK hypotheses, in a file-scope device array (512 KiB per
+// GPU, held until the process ends).  Host code never passes the array's name
+// to a kernel (on the host it is only a stand-in): it takes the device address
+// from hipGetSymbolAddress, once per device, with that device current.
+constexpr int kMaxResampleK = 65535;
+static __device__ __align__(256) int32_t scratch[2 * kMaxResampleK];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t resample_scratch(int device, int32_t** ptr, int* max_k) {
+  *max_k = kMaxResampleK;
+  *ptr = nullptr;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = static_cast<int32_t*>(p);
+  }
+  *ptr = g_scratch_ptr[device];
+  return hipSuccess;
 }
 
 hipError_t launch_resample(int K, float* poses, float* state, int state_dim, const float* loss,

@@ -73,6 +73,10 @@ _SIGS = {
     "pnerf_field_set_profiling": (C.c_int, [C.c_void_p, C.c_int32]),
     "pnerf_field_profile_read": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                            C.c_void_p]),
+    "pnerf_resample_hypotheses_noalloc": (C.c_int, [C.c_int32, C.c_void_p, C.c_void_p,
+                                                    C.c_int32, C.c_void_p, C.c_float, C.c_float,
+                                                    C.c_float, C.c_uint64, C.c_uint32,
+                                                    C.c_void_p]),
     "pnerf_plan_counted_batch": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_void_p]),
     "pnerf_plan_chunks": (C.c_int, [C.c_void_p, C.c_int32, C.c_int64, C.c_int64, C.c_void_p,
                                     C.c_void_p, C.c_void_p]),
@@ -310,6 +314,20 @@ def resample_hypotheses(poses, state, loss, keep_frac: float, sigma_rot: float,
     K = poses.shape[0]
     dim = 0 if state is None else int(state.shape[1])
     _check(lib().pnerf_resample_hypotheses(
+        K, _dev(poses, torch.float32, (K, 3, 4), "poses"),
+        None if state is None else _dev(state, torch.float32, (K, dim), "state"), dim,
+        _dev(loss, torch.float32, (K,), "loss"), keep_frac, sigma_rot, sigma_trans,
+        seed & 0xFFFFFFFFFFFFFFFF, round_idx, _stream(stream)))
+
+
+def resample_hypotheses_noalloc(poses, state, loss, keep_frac: float, sigma_rot: float,
+                                sigma_trans: float, seed: int, round_idx: int, stream=None):
+    """pnerf_resample_hypotheses_noalloc: resample_hypotheses without any
+    allocation (static ranking scratch per GPU, K <= 65535)."""
+    import torch
+    K = poses.shape[0]
+    dim = 0 if state is None else int(state.shape[1])
+    _check(lib().pnerf_resample_hypotheses_noalloc(
         K, _dev(poses, torch.float32, (K, 3, 4), "poses"),
         None if state is None else _dev(state, torch.float32, (K, dim), "state"), dim,
         _dev(loss, torch.float32, (K,), "loss"), keep_frac, sigma_rot, sigma_trans,

@@ -189,3 +189,20 @@ def test_plan_chunks_cuts_whole_hypotheses(pn):
     with pytest.raises(pn.PnerfError) as e:
         pn.plan_chunks([5, -2], 10, 10)
     assert e.value.status == pn.ERR_INVALID_ARG
+
+
+def test_noalloc_entry_point_calls_no_allocator():
+    """pnerf_resample_hypotheses_noalloc and the scratch lookup it uses contain
+    no allocating call; the device array's name reaches the host only through
+    hipGetSymbolAddress."""
+    src = os.path.join(ROOT, "paper_2210_10108_amd", "csrc")
+    api = open(os.path.join(src, "api.hip")).read()
+    body = api.split("pnerf_status pnerf_resample_hypotheses_noalloc(", 1)[1].split("\n}\n", 1)[0]
+    pose = open(os.path.join(src, "pose.hip")).read()
+    getter = pose.split("hipError_t resample_scratch(", 1)[1].split("\n}\n", 1)[0]
+    for text in (body, getter):
+        for bad in ("Malloc", "hipFree", "hipMemset", "new ", "torch", "std::vector"):
+            assert bad not in text, bad
+    assert "resample_scratch(" in body and "launch_resample(" in body
+    uses = [l for l in pose.splitlines() if re.search(r"\bscratch\b", l) and "HIP_SYMBOL" in l]
+    assert len(uses) == 1 and "hipGetSymbolAddress" in uses[0]
