@@ -13,7 +13,8 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "pnerf_oracle.c")
-LIB = os.path.join(HERE, "liboracle.so")
+# PNERF_ORACLE_LIB: load another build of the same source (the sanitizer test's)
+LIB = os.environ.get("PNERF_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 
 
 def build(force: bool = True) -> str:
