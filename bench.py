@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--no-calibration", action="store_true",
                     help="skip the on-box copy and bf16 GEMM reference rates")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--backward", type=int, default=0, choices=(0, 1),
+                    help="0: separate composite, network backward and reduction kernels; "
+                         "1: the fused per-ray backward kernel")
     ap.add_argument("--overlap-chunks", type=int, default=0,
                     help="field option: loss-gradient chunks pipelined over two streams "
                          "(0 = library default, 1 = off)")
@@ -188,7 +191,8 @@ def paper_run(args):
     sched = driver.PAPER_SCHEDULE
     K = sched.n_hypotheses
     fa = synth.make_field(w, args.seed)
-    field = pnerf.Field(synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad))
+    field = pnerf.Field(synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad),
+                        backward=args.backward)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
     poses0 = synth.perturb_poses(gt, K, w.max_rot_deg, w.max_trans, args.seed)
@@ -250,7 +254,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     fa = synth.make_field(w, args.seed)
     spec = synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad)  # occupancy built on the device
-    field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks)
+    field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks, backward=args.backward)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
     poses0 = synth.perturb_poses(gt, w.K, w.max_rot_deg, w.max_trans, args.seed)
@@ -326,7 +330,8 @@ def main():
     # three bf16 products per fp32 product, priced against the bf16 peak
     units = {"encode": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
              "mlp_fwd": ("mfma", 2 * mac_fwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
-             "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12)}
+             "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
+             "ray_bwd": ("mfma", 2 * mac_bwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12)}
     rooflines = {}
     for kname, (bound, per, peak, unit, scale) in units.items():
         if kname not in prof:
@@ -344,7 +349,8 @@ def main():
     lpg = w.n_levels // 4
     keys = {"encode": f"k_encode<{'true' if w.param_dtype == 'f16' else 'false'}, true>",
             "mlp_fwd": f"k_mlp_fwd<{lpg}, true>",
-            "mlp_bwd": f"k_mlp_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}>"}
+            "mlp_bwd": f"k_mlp_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}>",
+            "ray_bwd": f"k_ray_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}, false>"}
     for kname, r in rooflines.items():
         tr = measured_traffic(w.name, keys[kname])
         # HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE), same units as achieved
@@ -384,6 +390,7 @@ def main():
                    "table": f"2^{w.log2_table}", "image": f"{w.width}x{w.height}",
                    "sampling": "uniform" if w.march_mode == 0 else "lattice+occupancy",
                    "optimizer": args.optimizer, "sh_dir_grad": args.sh_dir_grad,
+                   "backward": "separate-kernels" if args.backward == 0 else "fused-per-ray",
                    "parallelism": "single-gpu"},
         "hypothesis_iters_per_sec": K * S / elapsed,
         "samples_per_step": samples_per_step,

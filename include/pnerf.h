@@ -143,6 +143,20 @@ typedef struct {
                                    loads through the same L1 address path, and
                                    on the 16 x 1024-ray workload the overlapped
                                    chunks ran slower than one chunk. */
+  int32_t backward;             /* the backward pass of render_loss_grad:
+                                   0 = separate kernels: composite and loss,
+                                   network backward per 16-sample tile, then
+                                   the per-hypothesis reduction (default; the
+                                   faster on the measured workloads);
+                                   1 = one fused kernel, a wavefront per ray:
+                                   composite, loss, composite backward, both
+                                   networks' backward and the encoding's
+                                   Jacobian, the ray's torque and force summed
+                                   in registers (no per-sample gradient in
+                                   memory);
+                                   2 = the fused kernel, also storing every
+                                   sample's intermediates as 0 does
+                                   (pnerf_field_inspect). */
 } pnerf_field_params;
 
 /* Create a field: validates `params`, copies every array to the device (builds
@@ -280,7 +294,8 @@ pnerf_status pnerf_march(pnerf_field* field, int32_t K, const float* poses, int3
  *   what 2: after pnerf_render rgb [n][3]; after pnerf_render_loss_grad dL/dz [n][3]
  *           (z = pre-sigmoid colour)
  *   what 3: after pnerf_render_loss_grad (t d x dL/dp, dL/dp) [n][6]
- * PNERF_ERR_INVALID_ARG if n exceeds the workspace or `what` is unknown. */
+ * PNERF_ERR_INVALID_ARG if n exceeds the workspace, `what` is unknown, or
+ * `what` > 0 after a pnerf_render_loss_grad with backward = 1. */
 pnerf_status pnerf_field_inspect(pnerf_field* field, int32_t what, float* dst, int64_t n,
                                  void* stream);
 

@@ -84,6 +84,8 @@ struct pnerf_field {
   int64_t samp_cap = 0;
   int n_slots = 0;              // sample buffers allocated (1 or 2)
   int overlap_chunks = 0;       // chunks a loss-gradient batch is cut into for overlap
+  int backward = 0;             // pnerf_field_params::backward
+  bool last_keeps_samples = false;  // the last call left per-sample intermediates
   // internal streams of the pipelined loss gradient: encoding | networks
   hipStream_t s_enc = nullptr, s_mlp = nullptr;
   hipEvent_t ev_start = nullptr, ev_enc[2] = {nullptr, nullptr}, ev_mlp[2] = {nullptr, nullptr};
@@ -97,7 +99,8 @@ struct pnerf_field {
   int64_t last_total = 0;
   const int32_t* last_total_dev = nullptr;  // the last call's total, when only the device holds it
   int64_t budget = 0;
-  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, enc_blocks = 0, enc_blocks_overlap = 0;
+  int n_cu = 0, fwd_blocks = 0, bwd_blocks = 0, ray_blocks = 0, enc_blocks = 0,
+      enc_blocks_overlap = 0;
   // profiling
   bool profiling = false;
   std::vector<KernelStat> stats;
@@ -223,6 +226,7 @@ struct RayWs {
   int32_t *count, *off, *blocksum, *hyp_total;
   int32_t* offc[2];             // per sample buffer: the chunk's own offsets,
   float *ray_loss[2], *partial[2];  // per-ray losses and reduction partials
+  float* ray_terms[2];          // fused backward: [n_rays][7] per-ray torque, force, loss
 };
 
 size_t carve_rays(int n_rays, int n_hyp, RayWs* r, char* base) {
@@ -248,6 +252,7 @@ size_t carve_rays(int n_rays, int n_hyp, RayWs* r, char* base) {
     x.offc[q] = c.take<int32_t>(R + 1);
     x.ray_loss[q] = c.take<float>(R);
     x.partial[q] = c.take<float>((size_t)n_hyp * kReduceParts * 7);
+    x.ray_terms[q] = c.take<float>(R * 7);
   }
   return c.off;
 }
@@ -304,6 +309,7 @@ DevWork chunk_work(pnerf_field* F, int ray_base, int chunk_id, int slot) {
   w.hyp_total = nullptr;
   w.ray_loss = r.ray_loss[slot];
   w.partial = r.partial[slot];
+  w.ray_terms = r.ray_terms[slot];
   w.total = F->d_totals + chunk_id;
   w.queue = F->d_queue;
   return w;
@@ -486,6 +492,7 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
                  int64_t capacity, hipStream_t s) {
   HIP_TRY(hipSetDevice(F->device));
   F->last_total_dev = nullptr;
+  F->last_keeps_samples = mode != kLossGrad || F->backward != 1;
   const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
   int32_t kr = 0;
   pnerf_status st = pnerf_plan_counted_batch(K, P, F->dev.max_per_ray, &kr);
@@ -600,11 +607,20 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
           HIP_TRY(hipStreamWaitEvent(sm, F->ev_enc[slot], 0));
         }
         HIP_TRY(timed(F, "mlp_fwd", sm, [&] { return launch_mlp_fwd(F->dev, b, w, F->fwd_blocks, 1, sm); }));
-        HIP_TRY(timed(F, "composite", sm, [&] { return launch_composite(F->dev, b, w, 1, nullptr, sm); }));
-        HIP_TRY(timed(F, "mlp_bwd", sm, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, sm); }));
-        HIP_TRY(timed(F, "reduce", sm, [&] {
-          return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, sm);
-        }));
+        if (F->backward == 0) {
+          HIP_TRY(timed(F, "composite", sm, [&] { return launch_composite(F->dev, b, w, 1, nullptr, sm); }));
+          HIP_TRY(timed(F, "mlp_bwd", sm, [&] { return launch_mlp_bwd(F->dev, b, w, F->bwd_blocks, sm); }));
+          HIP_TRY(timed(F, "reduce", sm, [&] {
+            return launch_reduce(F->dev, b, w, loss + k0, dpose + (size_t)6 * k0, sm);
+          }));
+        } else {
+          HIP_TRY(timed(F, "ray_bwd", sm, [&] {
+            return launch_ray_bwd(F->dev, b, w, F->ray_blocks, F->backward == 2, sm);
+          }));
+          HIP_TRY(timed(F, "reduce", sm, [&] {
+            return launch_reduce_rays(b, w, loss + k0, dpose + (size_t)6 * k0, sm);
+          }));
+        }
         if (overlap) HIP_TRY(hipEventRecord(F->ev_mlp[slot], sm));
       }
       base += device_sized ? 0 : sums[c];
@@ -726,6 +742,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   if (!(p->t_stop >= 0.0f)) return fail(PNERF_ERR_INVALID_ARG, "t_stop must be >= 0");
   if (p->overlap_chunks < 0 || p->overlap_chunks > 64)
     return fail(PNERF_ERR_INVALID_ARG, "overlap_chunks=%d outside 0..64", p->overlap_chunks);
+  if (p->backward < 0 || p->backward > 2)
+    return fail(PNERF_ERR_INVALID_ARG, "backward=%d outside 0..2", p->backward);
 
   pnerf_field* F = new pnerf_field();
   auto cleanup_fail = [&](pnerf_status st) {
@@ -851,6 +869,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   F->n_cu = prop.multiProcessorCount;
   F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
   F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad);
+  F->ray_blocks = F->n_cu * ray_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad);
+  F->backward = p->backward;
   CF_TRY(hipMalloc(&F->d_queue, sizeof(uint32_t) * kMaxLevels * kQueueStride));
   F->enc_blocks = encode_blocks(d, F->n_cu, 8);
   F->enc_blocks_overlap = encode_blocks(d, F->n_cu, 4);  // leave room for the networks
@@ -1022,6 +1042,9 @@ pnerf_status pnerf_field_inspect(pnerf_field* F, int32_t what, float* dst, int64
   if (what < 0 || what > 3) return fail(PNERF_ERR_INVALID_ARG, "what=%d", what);
   if (!F->d_samp[0] || n < 0 || n > F->samp_cap) return fail(PNERF_ERR_INVALID_ARG, "n=%lld", (long long)n);
   if (F->last_chunks != 1) return fail(PNERF_ERR_INVALID_ARG, "last call used %d chunks", F->last_chunks);
+  if (what > 0 && !F->last_keeps_samples)
+    return fail(PNERF_ERR_INVALID_ARG,
+                "the last loss gradient kept no per-sample intermediates (backward = 1)");
   DevWork w{};
   carve_samples(F->dev, F->samp_cap, &w, (char*)F->d_samp[0]);
   w.total = F->d_totals;  // the single chunk of the last call

@@ -23,7 +23,10 @@
 // Lane group g reads the features of levels g, g+4, g+8, g+12 of its column's
 // sample (rows 2 LPG g .. of the SoA feature array): the first layer's B
 // operand.
+#include <algorithm>
+
 #include "pnerf_internal.h"
+#include "render_common.h"
 
 namespace pnerf {
 namespace {
@@ -339,12 +342,123 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 }
 
 // ----------------------------------------------------------------- backward
-// DIR: the SH direction path (sh_dir_grad) is on; without it the SH rows of
-// colour layer 1 are not staged, and four blocks fit a CU's LDS.
+// The backward networks for one 16-sample column tile: lane (g, col) holds
+// the sample of column col.  In: z = d loss / d z of that sample (zero when it
+// has none), gh0 = d loss / d h_0 on lane group 0 (zero elsewhere), the
+// sample's two ReLU mask words as the forward kernel stored them for this lane
+// group, and sc = the sample whose Jacobian records are read (any valid sample
+// when the column is empty).  Out: d loss / d p of the sample, gx (in every
+// lane group, after the sums over the groups), and on the direction path the
+// term d loss / d d through the SH input, gd (likewise summed).
+template <int LPG, bool DIR>
+__device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
+                                         const WeightUnit* lds, const float* s_c3,
+                                         const SplitK& sk, int lane, const float z[3], float gh0,
+                                         uint32_t mw0, uint32_t mw1, int sc, const float d[3],
+                                         float gx[3], float gd[3]) {
+  constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
+  const int g = lane >> 4;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
+  // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
+  floatx4 gb2[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float* c3 = s_c3 + 3 * (16 * m + 4 * g + i);
+      gb2[m][i] = c3[0] * z[0] + c3[1] * z[1] + c3[2] * z[2];
+    }
+  apply_mask(gb2, mw1, 0);
+  // colour layer 2 transposed
+  floatx4 gb1[4] = {zero, zero, zero, zero};
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const Split x = pack2(gb2[2 * s2], gb2[2 * s2 + 1], sk);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) gb1[m] = mfma3(load_unit(lds, kBC2 + 2 * m + s2, lane), x, gb1[m]);
+  }
+  apply_mask(gb1, mw0, 8);
+  // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
+  floatx4 gh = zero, gsh = zero;
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const Split x = pack2(gb1[2 * s2], gb1[2 * s2 + 1], sk);
+    gh = mfma3(load_unit(lds, kBC1 + s2, lane), x, gh);
+    if (DIR) gsh = mfma3(load_unit(lds, kBSH + s2, lane), x, gsh);
+  }
+  gh[0] += gh0;  // d loss / d h_0 (zero off group 0)
+  // density layer 2 transposed: ga = W_d2 gh (one K step, upper half zero), masked
+  floatx4 ga[4];
+  {
+    const Split x = pack2(gh, zero, sk);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) ga[m] = mfma3(load_unit(lds, kBD2 + m, lane), x, zero);
+  }
+  apply_mask(ga, mw0, 0);
+  // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
+  // level 4 (2 mm + i / 2) + g, so lane group g gets its own levels
+  floatx4 gf[MD];
+#pragma unroll
+  for (int mm = 0; mm < MD; ++mm) gf[mm] = zero;
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const Split x = pack2(ga[2 * s2], ga[2 * s2 + 1], sk);
+#pragma unroll
+    for (int mm = 0; mm < MD; ++mm) gf[mm] = mfma3(load_unit(lds, kBD1 + 2 * mm + s2, lane), x, gf[mm]);
+  }
+  // d loss / d p = sum over the lane group's levels 4j + g of d loss / d
+  // feature times the stored Jacobian, then over the 4 groups.  This lane
+  // group's Jacobian records of the sample (level 4j + g at record j): six
+  // fp16 values d feature_q / d pos_a at 3 q + a
+  const uint32_t* jp = reinterpret_cast<const uint32_t*>(w.jac) +
+                       (((int64_t)(sc >> 5) * 4 + g) * (6 * LPG * 32) + (sc & 31) * 6) / 2;
+  gx[0] = gx[1] = gx[2] = 0.f;
+#pragma unroll
+  for (int j = 0; j < LPG; ++j) {
+    // level 4j + g: d loss / d pos_l = sum_q gf * J, then times N_l
+    const uint32_t* rec = jp + j * (32 * 6 / 2);
+    // read once: non-temporal, so that they do not displace cached data
+    const uint32_t r[3] = {__builtin_nontemporal_load(rec), __builtin_nontemporal_load(rec + 1),
+                           __builtin_nontemporal_load(rec + 2)};
+    float J[6];
+#pragma unroll
+    for (int k = 0; k < 6; ++k)
+      J[k] = __half2float(__ushort_as_half((unsigned short)(r[k / 2] >> (16 * (k % 2)))));
+    float gl[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float gq = gf[j / 2][2 * (j % 2) + q];
+#pragma unroll
+      for (int a = 0; a < 3; ++a) gl[a] += gq * J[3 * q + a];
+    }
+    const float N = (float)f.res[4 * j + g];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) gx[a] += N * gl[a];
+  }
+  gd[0] = gd[1] = gd[2] = 0.f;
+  if (DIR) {
+    const float gs[4] = {gsh[0], gsh[1], gsh[2], gsh[3]};
+    sh4_vjp(d, g, gs, gd);
+  }
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    gx[a] += __shfl_xor(gx[a], 16);
+    gx[a] += __shfl_xor(gx[a], 32);
+    gx[a] *= f.inv_ext[a];  // d pos / d p = N_l / extent (N_l applied above)
+    gd[a] += __shfl_xor(gd[a], 16);
+    gd[a] += __shfl_xor(gd[a], 32);
+  }
+}
+
+// The backward kernel of the separate-kernel path: one 16-sample column tile
+// per wavefront, reading d loss / d h_0 and d loss / d z from the composite
+// kernel, and storing each sample's torque and force terms for the
+// reduction.  DIR: the SH direction path (sh_dir_grad) is on; without it the
+// SH rows of colour layer 1 are not staged, and four blocks fit a CU's LDS.
 template <int LPG, bool DIR>
 __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevWork w) {
-  constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
-  constexpr int NT = kBwdNT, TS = 16 * NT;
+  static_assert(kBwdNT == 1, "one column tile per wavefront");
   constexpr int NU = DIR ? kBwdUnits : kBSH;  // staged weight units
   __shared__ WeightUnit lds[NU];
   __shared__ float s_c3[64 * 3];
@@ -353,191 +467,207 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
   __syncthreads();
 
   const int S = *w.total;
-  const int n_tiles = (S + TS - 1) / TS;
+  const int n_tiles = (S + 15) / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
   const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
   const int n_waves = gridDim.x * (kBlock / 64);
-  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   const SplitK sk = split_k(f);
 
   for (int tile = wave; tile < n_tiles; tile += n_waves) {
     // the weight units are re-read from LDS every tile: hoisted out of the
     // loop they would pin ~150 registers and cap occupancy at 1 wave/SIMD
     asm volatile("" ::: "memory");
-    const uint32_t* mw = w.masks + (size_t)tile * NT * 2 * 64 + lane;
+    const uint32_t* mw = w.masks + (size_t)tile * 2 * 64 + lane;
     // word 0: density layer 1 (base 0) and colour layer 1 (base 8); word 1:
     // colour layer 2 (base 0)
-    uint32_t mw0[NT], mw1[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      mw0[nt] = mw[(2 * nt) * 64];
-      mw1[nt] = mw[(2 * nt + 1) * 64];
-    }
-    // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
-    // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
-    floatx4 gb2[NT][4];
-    float gh0[NT];
-    int sidx[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int s = tile * TS + nt * 16 + col;
-      sidx[nt] = s;
-      const int sc = s < S ? s : S - 1;
-      const bool ok = s < S;
-      const float z0 = ok ? w.cr[sc] : 0.0f, z1 = ok ? w.cg[sc] : 0.0f, z2 = ok ? w.cb[sc] : 0.0f;
-      gh0[nt] = g == 0 && ok ? w.sig[sc] : 0.0f;
-#pragma unroll
-      for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float* c3 = s_c3 + 3 * (16 * m + 4 * g + i);
-          gb2[nt][m][i] = c3[0] * z0 + c3[1] * z1 + c3[2] * z2;
-        }
-      apply_mask(gb2[nt], mw1[nt], 0);
-    }
-    // colour layer 2 transposed
-    floatx4 gb1[NT][4];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int m = 0; m < 4; ++m) gb1[nt][m] = zero;
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb2[nt][2 * s2], gb2[nt][2 * s2 + 1], sk);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const Split a = load_unit(lds, kBC2 + 2 * m + s2, lane);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) gb1[nt][m] = mfma3(a, x[nt], gb1[nt][m]);
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) apply_mask(gb1[nt], mw0[nt], 8);
-    // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
-    floatx4 gh[NT], gsh[NT];
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) gh[nt] = gsh[nt] = zero;
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gb1[nt][2 * s2], gb1[nt][2 * s2 + 1], sk);
-      const Split a = load_unit(lds, kBC1 + s2, lane);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) gh[nt] = mfma3(a, x[nt], gh[nt]);
-      if (DIR) {
-        const Split a2 = load_unit(lds, kBSH + s2, lane);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) gsh[nt] = mfma3(a2, x[nt], gsh[nt]);
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) gh[nt][0] += gh0[nt];  // d loss / d h_0 (zero off group 0)
-    // density layer 2 transposed: ga = W_d2 gh (one K step, upper half zero), masked
-    floatx4 ga[NT][4];
-    {
-      Split x[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(gh[nt], zero, sk);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const Split a = load_unit(lds, kBD2 + m, lane);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) ga[nt][m] = mfma3(a, x[nt], zero);
-      }
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) apply_mask(ga[nt], mw0[nt], 0);
-    // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
-    // level 4 (2 mm + i / 2) + g, so lane group g gets its own levels
-    floatx4 gf[MD][NT];
-#pragma unroll
-    for (int mm = 0; mm < MD; ++mm)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) gf[mm][nt] = zero;
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) x[nt] = pack2(ga[nt][2 * s2], ga[nt][2 * s2 + 1], sk);
-#pragma unroll
-      for (int mm = 0; mm < MD; ++mm) {
-        const Split a = load_unit(lds, kBD1 + 2 * mm + s2, lane);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) gf[mm][nt] = mfma3(a, x[nt], gf[mm][nt]);
-      }
-    }
-    // d loss / d p = sum over the lane group's levels 4j + g of
-    // d loss / d feature times the stored Jacobian, then over the 4 groups;
+    const uint32_t mw0 = mw[0], mw1 = mw[64];
+    const int s = tile * 16 + col;
+    const int sc = s < S ? s : S - 1;
+    const bool ok = s < S;
+    const float z[3] = {ok ? w.cr[sc] : 0.0f, ok ? w.cg[sc] : 0.0f, ok ? w.cb[sc] : 0.0f};
+    const float gh0 = g == 0 && ok ? w.sig[sc] : 0.0f;
+    float d[3];
+    sample_dir(w, sc, d);
+    float gx[3], gd[3];
+    bwd_tile<LPG, DIR>(f, w, lds, s_c3, sk, lane, z, gh0, mw0, mw1, sc, d, gx, gd);
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int s = sidx[nt];
-      const int sc = s < S ? s : S - 1;
-      // this lane group's Jacobian records of the sample (level 4j + g at
-      // record j): six fp16 values d feature_q / d pos_a at 3 q + a
-      const uint32_t* jp = reinterpret_cast<const uint32_t*>(w.jac) +
-                           (((int64_t)(sc >> 5) * 4 + g) * (6 * LPG * 32) + (sc & 31) * 6) / 2;
-      float gx[3] = {0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < LPG; ++j) {
-        // level 4j + g: d loss / d pos_l = sum_q gf * J, then times N_l
-        const uint32_t* rec = jp + j * (32 * 6 / 2);
-        // read once: non-temporal, so that they do not displace cached data
-        const uint32_t r[3] = {__builtin_nontemporal_load(rec), __builtin_nontemporal_load(rec + 1),
-                               __builtin_nontemporal_load(rec + 2)};
-        float J[6];
-#pragma unroll
-        for (int k = 0; k < 6; ++k)
-          J[k] = __half2float(__ushort_as_half((unsigned short)(r[k / 2] >> (16 * (k % 2)))));
-        float gl[3] = {0.f, 0.f, 0.f};
-#pragma unroll
-        for (int q = 0; q < 2; ++q) {
-          const float gq = gf[j / 2][nt][2 * (j % 2) + q];
-#pragma unroll
-          for (int a = 0; a < 3; ++a) gl[a] += gq * J[3 * q + a];
-        }
-        const float N = (float)f.res[4 * j + g];
-#pragma unroll
-        for (int a = 0; a < 3; ++a) gx[a] += N * gl[a];
+    if (ok && g < 2) {
+      const float t = w.t[s];
+      const float m[3] = {t * gx[0] + gd[0], t * gx[1] + gd[1], t * gx[2] + gd[2]};
+      // lane group 0 stores the torque, group 1 the force
+      float o0, o1, o2;
+      if (g == 0) {
+        o0 = d[1] * m[2] - d[2] * m[1];
+        o1 = d[2] * m[0] - d[0] * m[2];
+        o2 = d[0] * m[1] - d[1] * m[0];
+      } else {
+        o0 = gx[0];
+        o1 = gx[1];
+        o2 = gx[2];
       }
-      float gd[3] = {0.f, 0.f, 0.f};
-      float d[3];
-      sample_dir(w, sc, d);
-      if (DIR) {
-        float gs[4] = {gsh[nt][0], gsh[nt][1], gsh[nt][2], gsh[nt][3]};
-        sh4_vjp(d, g, gs, gd);
+      float* out = w.feat + (int64_t)(3 * g) * w.cap;  // feature rows are free by now
+      out[s] = o0;
+      out[w.cap + s] = o1;
+      out[2 * w.cap + s] = o2;
+    }
+  }
+}
+
+// The fused backward kernel: one wavefront per ray, persistent over rays.
+// It composites the ray front to back and takes the loss on its pixel
+// (classic volume rendering), sweeps the composite backward in 64-sample
+// steps, and runs every step's samples, 16 at a time, through the backward
+// networks and the encoding's Jacobian: d loss / d h_0 and d loss / d z pass
+// from the composite lanes to the network columns by cross-lane reads, and the
+// ray's sums M = sum_i (t_i d loss / d p_i + d loss / d d_i) and
+// G = sum_i d loss / d p_i stay in registers, so that the ray's torque
+// (Eq. 3) is one cross product d x M.  Each ray leaves 7 floats -- torque,
+// force (Eq. 2), loss -- for the per-hypothesis reduction; no per-sample
+// gradient goes to memory.  KEEP also stores every sample's d loss / d h_0,
+// d loss / d z and (torque, force) terms as the separate kernels do
+// (inspection).
+template <int LPG, bool DIR, bool KEEP>
+__global__ __launch_bounds__(kBlock) void k_ray_bwd(DevField f, DevBatch b, DevWork w) {
+  constexpr int NU = DIR ? kBwdUnits : kBSH;
+  __shared__ WeightUnit lds[NU];
+  __shared__ float s_c3[64 * 3];
+  stage(lds, f.wbwd, NU);
+  for (int i = threadIdx.x; i < 64 * 3; i += kBlock) s_c3[i] = f.wc3[i];
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63, g = lane >> 4, col = lane & 15;
+  const int wave = blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  const int n_waves = gridDim.x * (kBlock / 64);
+  const SplitK sk = split_k(f);
+  const float norm = 1.0f / (3.0f * (float)b.P);
+  const int n_pix = b.W * b.H;
+
+  for (int ray = wave; ray < b.n_rays; ray += n_waves) {
+    const int base = w.off[ray];
+    const int n = w.off[ray + 1] - base;
+    const float delta = w.rdelta[ray];
+    int pix = b.pix[ray];
+    pix = pix < 0 ? 0 : (pix >= n_pix ? n_pix - 1 : pix);
+    const float* I = b.obs + 3 * (size_t)pix;
+    const float y[3] = {I[0], I[1], I[2]};
+
+    // pass 1: colour and stop index
+    float C[3] = {0.f, 0.f, 0.f};
+    float carry = 0.0f;
+    int n_used = n;
+    for (int i0 = 0; i0 < n_used; i0 += 64) {
+      float incl;
+      const Chunk ch = step_chunk(f, w, base, n, i0, delta, carry, lane, incl);
+      const uint64_t st = __ballot(ch.stop_here);
+      int last = 63;
+      if (st) {
+        last = __ffsll((unsigned long long)st) - 1;
+        n_used = i0 + last + 1;
       }
+      const bool use = ch.live && lane <= last;
 #pragma unroll
-      for (int a = 0; a < 3; ++a) {
-        gx[a] += __shfl_xor(gx[a], 16);
-        gx[a] += __shfl_xor(gx[a], 32);
-        gx[a] *= f.inv_ext[a];  // d pos / d p = N_l / extent (N_l applied above)
-        gd[a] += __shfl_xor(gd[a], 16);
-        gd[a] += __shfl_xor(gd[a], 32);
+      for (int q = 0; q < 3; ++q) C[q] += wave_sum(use ? ch.w * ch.c[q] : 0.0f);
+      carry = lane_value(incl, last);
+      if (st) break;
+    }
+    const float T_end = __expf(-carry);
+    float gC[3], L = 0.0f;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      C[q] += T_end * f.bg[q];
+      float gq;
+      L += pixel_loss(f.loss_type, C[q], y[q], f.loss_param, gq);
+      gC[q] = gq * norm;
+    }
+
+    // pass 2: the composite backward, step by step, and the networks
+    const float d[3] = {w.rdx[ray], w.rdy[ray], w.rdz[ray]};
+    float R[3] = {C[0], C[1], C[2]};  // colour behind the step (background included)
+    float carry2 = 0.0f;
+    float M[3] = {0.f, 0.f, 0.f}, G[3] = {0.f, 0.f, 0.f};  // this column's share of the sums
+    for (int i0 = 0; i0 < n_used; i0 += 64) {
+      float incl;
+      const Chunk ch = step_chunk(f, w, base, n, i0, delta, carry2, lane, incl);
+      const int i = i0 + lane;
+      const bool use = ch.live && i < n_used;
+      float gs = 0.0f, gz[3];
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const float wc = use ? ch.w * ch.c[q] : 0.0f;
+        const float p = wave_incl_scan(wc);
+        const float S = R[q] - p;  // colour behind sample i
+        R[q] -= lane_value(p, 63);
+        gs += gC[q] * (ch.T_out * ch.c[q] - S);
+        gz[q] = use ? ch.w * gC[q] * ch.c[q] * (1.0f - ch.c[q]) : 0.0f;
       }
-      if (s < S && g < 2) {
+      carry2 = lane_value(incl, 63);
+      const float gh0 = use ? delta * gs * ch.sig : 0.0f;
+      if (KEEP && i < n) {
+        w.sig[base + i] = gh0;
+        w.cr[base + i] = gz[0];
+        w.cg[base + i] = gz[1];
+        w.cb[base + i] = gz[2];
+      }
+      // the step's samples through the networks, 16 columns at a time
+      const int n_step = min(64, n_used - i0);
+      for (int c0 = 0; c0 < n_step; c0 += 16) {
+        // the weight units are re-read from LDS every tile (see k_mlp_bwd)
+        asm volatile("" ::: "memory");
+        const int src = c0 + col;  // composite lane of this column's sample
+        const bool ok = src < n_step;
+        const int s = base + i0 + (ok ? src : 0);
+        // lanes past the ray's used samples hold zero gradients
+        const float z[3] = {__shfl(gz[0], src), __shfl(gz[1], src), __shfl(gz[2], src)};
+        const float gh = __shfl(gh0, src);
+        // the sample's mask words, where the forward kernel's column tile of
+        // 16 compacted samples left them for this lane group
+        const uint32_t* mw = w.masks + (size_t)(s >> 4) * 2 * 64 + 16 * g + (s & 15);
+        float gx[3], gd[3];
+        bwd_tile<LPG, DIR>(f, w, lds, s_c3, sk, lane, z, g == 0 ? gh : 0.0f, mw[0], mw[64], s,
+                           d, gx, gd);
         const float t = w.t[s];
-        const float m[3] = {t * gx[0] + gd[0], t * gx[1] + gd[1], t * gx[2] + gd[2]};
-        // lane group 0 stores the torque, group 1 the force
-        float o0, o1, o2;
-        if (g == 0) {
-          o0 = d[1] * m[2] - d[2] * m[1];
-          o1 = d[2] * m[0] - d[0] * m[2];
-          o2 = d[0] * m[1] - d[1] * m[0];
-        } else {
-          o0 = gx[0];
-          o1 = gx[1];
-          o2 = gx[2];
+        if (ok) {
+#pragma unroll
+          for (int a = 0; a < 3; ++a) {
+            M[a] += t * gx[a] + gd[a];
+            G[a] += gx[a];
+          }
         }
-        float* out = w.feat + (int64_t)(3 * g) * w.cap;  // feature rows are free by now
-        out[s] = o0;
-        out[w.cap + s] = o1;
-        out[2 * w.cap + s] = o2;
+        if (KEEP && ok && g < 2) {
+          const float m[3] = {t * gx[0] + gd[0], t * gx[1] + gd[1], t * gx[2] + gd[2]};
+          const float o[3] = {g == 0 ? d[1] * m[2] - d[2] * m[1] : gx[0],
+                              g == 0 ? d[2] * m[0] - d[0] * m[2] : gx[1],
+                              g == 0 ? d[0] * m[1] - d[1] * m[0] : gx[2]};
+          float* out = w.feat + (int64_t)(3 * g) * w.cap;
+#pragma unroll
+          for (int a = 0; a < 3; ++a) out[a * w.cap + s] = o[a];
+        }
       }
     }
+    if (KEEP) {  // samples after the stop: zero gradient
+      for (int i = n_used + lane; i < n; i += 64) {
+        w.sig[base + i] = 0.0f;
+        w.cr[base + i] = 0.0f;
+        w.cg[base + i] = 0.0f;
+        w.cb[base + i] = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 6; ++q) w.feat[(int64_t)q * w.cap + base + i] = 0.0f;
+      }
+    }
+    // the ray's sums over the 16 columns (fixed butterfly), then the torque
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        M[a] += __shfl_xor(M[a], o);
+        G[a] += __shfl_xor(G[a], o);
+      }
+    }
+    const float tq[3] = {d[1] * M[2] - d[2] * M[1], d[2] * M[0] - d[0] * M[2],
+                         d[0] * M[1] - d[1] * M[0]};
+    const float v = lane == 0 ? tq[0] : lane == 1 ? tq[1] : lane == 2 ? tq[2]
+                  : lane == 3 ? G[0]  : lane == 4 ? G[1]  : lane == 5 ? G[2] : L * norm;
+    if (lane < 7) w.ray_terms[(int64_t)7 * ray + lane] = v;
   }
 }
 
@@ -564,6 +694,19 @@ int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad) {
     case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<2, true> : k_mlp_bwd<2, false>, kBlock, 0); break;
     case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<3, true> : k_mlp_bwd<3, false>, kBlock, 0); break;
     case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<4, true> : k_mlp_bwd<4, false>, kBlock, 0); break;
+  }
+  return e == hipSuccess && n > 0 ? n : 1;
+}
+
+int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad) {
+  int n = 0;
+  hipError_t e = hipErrorInvalidValue;
+  const bool dir = sh_dir_grad != 0;
+  switch (lpg) {
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<1, true, false> : k_ray_bwd<1, false, false>, kBlock, 0); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<2, true, false> : k_ray_bwd<2, false, false>, kBlock, 0); break;
+    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<3, true, false> : k_ray_bwd<3, false, false>, kBlock, 0); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<4, true, false> : k_ray_bwd<4, false, false>, kBlock, 0); break;
   }
   return e == hipSuccess && n > 0 ? n : 1;
 }
@@ -611,6 +754,31 @@ hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w
   if (f.sh_dir_grad)
     return launch_bwd<true>(f, b, w, n_blocks, s);
   return launch_bwd<false>(f, b, w, n_blocks, s);
+}
+
+namespace {
+template <bool DIR, bool KEEP>
+hipError_t launch_ray(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                      hipStream_t s) {
+  switch (f.lpg) {
+    case 1: hipLaunchKernelGGL((k_ray_bwd<1, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_ray_bwd<2, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_ray_bwd<3, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_ray_bwd<4, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_ray_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                          int keep, hipStream_t s) {
+  // no more workgroups than the rays need (8 rays each)
+  const int need = (b.n_rays + kBlock / 64 - 1) / (kBlock / 64);
+  n_blocks = std::max(1, std::min(n_blocks, need));
+  if (f.sh_dir_grad)
+    return keep ? launch_ray<true, true>(f, b, w, n_blocks, s) : launch_ray<true, false>(f, b, w, n_blocks, s);
+  return keep ? launch_ray<false, true>(f, b, w, n_blocks, s) : launch_ray<false, false>(f, b, w, n_blocks, s);
 }
 
 }  // namespace pnerf

@@ -149,6 +149,7 @@ struct DevWork {
   int32_t* total;               // device scalar: samples of the counted batch / the chunk
   float* ray_loss;              // [n_rays]
   float* partial;               // [K][parts][7] per-hypothesis partial sums
+  float* ray_terms;             // [n_rays][7] fused backward: each ray's torque, force, loss
   // per sample
   float* t;
   int32_t* sray;                // ray of each sample
@@ -182,6 +183,13 @@ hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w
                           hipStream_t s);
 hipError_t launch_reduce(const DevField& f, const DevBatch& b, const DevWork& w, float* loss,
                          float* dpose, hipStream_t s);
+// The fused per-ray backward (composite, loss, network backward, each ray's
+// torque and force) and the per-hypothesis sums of its per-ray terms.  keep:
+// also store the per-sample intermediates the separate kernels leave.
+hipError_t launch_ray_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                          int keep, hipStream_t s);
+hipError_t launch_reduce_rays(const DevBatch& b, const DevWork& w, float* loss, float* dpose,
+                              hipStream_t s);
 hipError_t launch_occupancy(const DevField& f, uint32_t* bits, int R, float thr, hipStream_t s);
 hipError_t launch_copy_samples(const float* t, const int32_t* j, float* t_out, int32_t* j_out,
                                int64_t n, hipStream_t s);
@@ -204,6 +212,7 @@ hipError_t resample_scratch(int device, int32_t** ptr, int* max_k);
 int reduce_parts(int K);
 int mlp_fwd_blocks_per_cu(int lpg);
 int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad);
+int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad);
 int encode_blocks(const DevField& f, int n_cu, int per_cu);
 
 }  // namespace pnerf

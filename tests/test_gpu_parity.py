@@ -111,11 +111,15 @@ def test_render_colour_ngp800(pn):
 
 
 # -------------------------------------------------------- loss and gradient
-def run_loss_grad(pn, case, obs, max_ws=0, per_sample=False):
+def run_loss_grad(pn, case, obs, max_ws=0, per_sample=False, backward=None):
     """GPU loss and gradient; with per_sample also each sample's (torque, force)
-    share and each hypothesis's sample range (from the GPU's own ray offsets)."""
+    share and each hypothesis's sample range (from the GPU's own ray offsets).
+    backward: the field's backward pass (0: separate kernels, the default)."""
     import torch
-    f = pn.Field(case.spec, max_workspace_bytes=max_ws, overlap_chunks=1 if per_sample else 0)
+    if backward is None:
+        backward = 0
+    f = pn.Field(case.spec, max_workspace_bytes=max_ws, overlap_chunks=1 if per_sample else 0,
+                 backward=backward)
     poses, pix = G.to_dev(case.poses), G.to_dev(case.pix)
     loss, dpose = f.render_loss_grad(poses, pix, G.to_dev(obs), case.intr)
     torch.cuda.synchronize()
@@ -138,11 +142,11 @@ def oracle_subset(of, case, obs, hyps):
     return of.render_loss_grad(case.poses[hyps], case.pix[hyps], obs, case.intr, per_sample=True)
 
 
-def check_full(pn, case, obs, ref, of, hyps=None):
+def check_full(pn, case, obs, ref, of, hyps=None, backward=0):
     """The whole batch on the GPU as one chunk; `ref` is the oracle's per-sample
     result for hypotheses `hyps` (all by default), computed by `of`."""
     import os
-    loss, dpose, n, ex = run_loss_grad(pn, case, obs, per_sample=True)
+    loss, dpose, n, ex = run_loss_grad(pn, case, obs, per_sample=True, backward=backward)
     P = case.pix.shape[1]
     hyps = list(range(case.pix.shape[0])) if hyps is None else list(hyps)
     ranges = [(int(ex["off"][k * P]), int(ex["off"][(k + 1) * P])) for k in hyps]
@@ -159,20 +163,22 @@ def check_full(pn, case, obs, ref, of, hyps=None):
     dict(sh_dir_grad=1),
     dict(dense_coarse_levels=0),
 ])
-def test_loss_grad_tiny(pn, overrides):
+@pytest.mark.parametrize("backward", [0, 2])
+def test_loss_grad_tiny(pn, overrides, backward):
     case = G.make_case("tiny32", **overrides)
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
     # per sample: torque and force shares, and the stage values d loss / d h0
     # and d loss / d z, element by element (check_full)
-    stats, ex = check_full(pn, case, obs, ref, of)
+    stats, ex = check_full(pn, case, obs, ref, of, backward=backward)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
 @pytest.mark.parametrize("n_levels,dense,sh_dir", [(8, 0, 0), (12, 1, 0), (16, 1, 0), (16, 1, 1),
                                                     (12, 1, 1)])
-def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense, sh_dir):
+@pytest.mark.parametrize("backward", [0, 2])
+def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense, sh_dir, backward):
     """8, 12 and 16 levels: as many encoding work queues, fewer than, as many
     as and more than the 8 XCDs, with and without dense coarse levels; and
     the backward kernel built with the SH direction path at 12 and 16 levels."""
@@ -184,7 +190,7 @@ def test_loss_grad_level_counts(pn, monkeypatch, n_levels, dense, sh_dir):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref, of)
+    stats, _ = check_full(pn, case, obs, ref, of, backward=backward)
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
@@ -207,7 +213,8 @@ def test_loss_grad_pixel_losses(pn, loss_type, param):
 # in the second, and later (with longer rays that never stop beside them)
 @pytest.mark.parametrize("div,bias,stops", [(96, 3.0, (0, 64)), (384, 2.5, (64, 128)),
                                             (768, 2.5, (128, 10**9))])
-def test_loss_grad_early_stop_and_occupancy(pn, div, bias, stops):
+@pytest.mark.parametrize("backward", [0, 2])
+def test_loss_grad_early_stop_and_occupancy(pn, div, bias, stops, backward):
     R = 16
     case = G.make_case("tiny32", K=3, P=200, march_mode=1, step=math.sqrt(3) / div,
                        max_samples=600, t_stop=1e-2, occ_res=R, density_bias=bias,
@@ -220,7 +227,7 @@ def test_loss_grad_early_stop_and_occupancy(pn, div, bias, stops):
     assert np.sum(stopped & (ref["stop"] >= stops[0]) & (ref["stop"] < stops[1])) >= 5
     if stops[0] >= 128:
         assert np.sum(~stopped & (cnt > 128)) >= 5
-    check_full(pn, case, obs, ref, of)
+    check_full(pn, case, obs, ref, of, backward=backward)
 
 
 def test_loss_grad_empty_grid_is_background_only(pn):
@@ -237,12 +244,51 @@ def test_loss_grad_empty_grid_is_background_only(pn):
 
 
 @pytest.mark.parametrize("K,P", [(1, 1), (1, 257), (5, 63), (7, 1)])
-def test_loss_grad_ragged_shapes(pn, K, P):
+@pytest.mark.parametrize("backward", [0, 2])
+def test_loss_grad_ragged_shapes(pn, K, P, backward):
     case = G.make_case("tiny32", K=K, P=P, pix_seed=K * 100 + P)
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    check_full(pn, case, obs, ref, of)
+    check_full(pn, case, obs, ref, of, backward=backward)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("tiny32", dict(K=5, P=63)),
+    ("tiny32", dict(K=3, P=200, march_mode=1, step=math.sqrt(3) / 384, max_samples=600,
+                    t_stop=1e-2, occ_res=16, density_bias=2.5, sh_dir_grad=1,
+                    occ_bits=synth.occupancy_pattern("sphere", 16))),
+    ("ngp800_uniform", dict(K=4)),
+])
+def test_backward_paths_agree(pn, name, kw):
+    """The fused per-ray kernel with and without its per-sample stores, and the
+    separate kernels: the same loss and gradient up to summation order (the
+    fused kernel sums each ray first), and the fused kernel's stores change
+    nothing."""
+    case = G.make_case(name, **kw)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    res = {bw: run_loss_grad(pn, case, obs, backward=bw) for bw in (0, 1, 2)}
+    assert res[0][2] == res[1][2] == res[2][2]
+    for bw, ref_bw, tol in ((2, 1, 1e-6), (1, 0, 1e-4)):
+        assert np.allclose(res[bw][0], res[ref_bw][0], rtol=tol, atol=0), bw
+        err = np.linalg.norm(res[bw][1] - res[ref_bw][1]) / np.linalg.norm(res[ref_bw][1])
+        assert err <= tol, (bw, err)
+
+
+def test_inspect_needs_a_backward_that_keeps_samples(pn):
+    import torch
+    case = G.make_case("tiny32", K=2, P=40)
+    obs = np.random.default_rng(0).uniform(0, 1, (32, 32, 3)).astype(np.float32)
+    f = pn.Field(case.spec, overlap_chunks=1, backward=1)
+    f.render_loss_grad(G.to_dev(case.poses), G.to_dev(case.pix), G.to_dev(obs), case.intr)
+    torch.cuda.synchronize()
+    n = f.last_sample_count()
+    assert n > 0
+    f.inspect(0, n)  # the sample positions are there
+    with pytest.raises(RuntimeError, match="per-sample intermediates"):
+        f.inspect(3, n)
+    f.close()
 
 
 def test_loss_grad_uniform_scanned_offsets(pn):
@@ -359,8 +405,8 @@ def test_loss_grad_device_sized_matches_host_planned(pn):
     assert np.array_equal(l1, l2) and np.array_equal(g1, g2)
 
 
-@pytest.mark.parametrize("chunks", [2, 4, 7])
-def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks):
+@pytest.mark.parametrize("chunks,backward", [(2, 0), (4, 0), (7, 0), (3, 1)])
+def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks, backward):
     # the pipelined loss gradient (encoding of one chunk alongside the networks
     # of the previous, two streams and sample buffers) gives the same bits as
     # one chunk on the caller's stream: per-sample work does not depend on the
@@ -371,7 +417,7 @@ def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks):
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     out = []
     for oc in (1, chunks):
-        f = pn.Field(case.spec, overlap_chunks=oc)
+        f = pn.Field(case.spec, overlap_chunks=oc, backward=backward)
         loss, dpose = f.render_loss_grad(G.to_dev(case.poses), G.to_dev(case.pix), G.to_dev(obs),
                                          case.intr)
         torch.cuda.synchronize()
@@ -603,9 +649,10 @@ def test_render_colour_full_batch_sampled_hypotheses(pn, name, hyps):
     assert ref.max() > 0.05
 
 
-@pytest.mark.parametrize("name,hyps", [("cam640_f16_occ128", [3, 200]),
-                                       ("large4m_occ256", [5, 700])])
-def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps):
+@pytest.mark.parametrize("name,hyps,backward", [("cam640_f16_occ128", [3, 200], 0),
+                                                ("large4m_occ256", [5, 700], 0),
+                                                ("large4m_occ256", [5, 700], 2)])
+def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps, backward):
     """The sampled hypotheses of a full-size workload as a batch of their own
     (one chunk, so every sample can be inspected): per-hypothesis sample counts
     exactly, per-sample torque and force shares and the stage values d loss /
@@ -615,7 +662,7 @@ def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps):
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
-    stats, _ = check_full(pn, case, obs, ref, of)
+    stats, _ = check_full(pn, case, obs, ref, of, backward=backward)
     assert stats["samples"] == int(ref["march"][0][-1]) > 100_000
 
 
