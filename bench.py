@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--backward", type=int, default=0, choices=(0, 1),
                     help="0: separate composite, network backward and reduction kernels; "
                          "1: the fused per-ray backward kernel")
+    ap.add_argument("--mlp-precision", type=int, default=0, choices=(0, 1),
+                    help="0: split-bf16 MFMA (three products, fp32-equivalent); "
+                         "1: fp16 MFMA (one product, fp32 accumulation)")
     ap.add_argument("--overlap-chunks", type=int, default=0,
                     help="field option: loss-gradient chunks pipelined over two streams "
                          "(0 = library default, 1 = off)")
@@ -78,6 +81,13 @@ def render_observation(field, w, gt, dev):
         ids = torch.arange(s, e, dtype=torch.int32, device=dev)[None]
         out[s:e] = field.render(pose, ids, intr)[0]
     return out.reshape(w.height, w.width, 3)
+
+
+def dtype_label(w, args):
+    """The path's arithmetic: fp32 (or fp16-stored) table and weights, fp32
+    encoding and compositing, and the networks' MFMA arithmetic."""
+    storage = "f16-storage" if w.param_dtype == "f16" else "f32"
+    return storage + ("+f16-mfma" if args.mlp_precision else "+split-bf16x3-mfma")
 
 
 def measured_traffic(workload, kernel_key):
@@ -192,7 +202,7 @@ def paper_run(args):
     K = sched.n_hypotheses
     fa = synth.make_field(w, args.seed)
     field = pnerf.Field(synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad),
-                        backward=args.backward)
+                        backward=args.backward, mlp_precision=args.mlp_precision)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
     poses0 = synth.perturb_poses(gt, K, w.max_rot_deg, w.max_trans, args.seed)
@@ -220,7 +230,7 @@ def paper_run(args):
     print(json.dumps({
         "metric": "seconds per pose estimate (paper schedule)", "value": elapsed, "unit": "s",
         "n_gpus": 1, "higher_is_better": False, "data": "synthetic",
-        "dtype": ("f16-storage" if w.param_dtype == "f16" else "f32") + "+split-bf16x3-mfma",
+        "dtype": dtype_label(w, args),
         "steps": sched.total_steps, "hypotheses": K,
         "hypothesis_iters_per_sec": K * sched.total_steps / elapsed,
         "config": {"workload": w.name, "P": w.P, "rays_per_step": K * w.P,
@@ -254,7 +264,8 @@ def main():
     w = synth.WORKLOADS[args.workload]
     fa = synth.make_field(w, args.seed)
     spec = synth.field_spec(w, fa, sh_dir_grad=args.sh_dir_grad)  # occupancy built on the device
-    field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks, backward=args.backward)
+    field = pnerf.Field(spec, overlap_chunks=args.overlap_chunks, backward=args.backward,
+                        mlp_precision=args.mlp_precision)
     gt = synth.ground_truth_pose(w, args.seed)
     obs = render_observation(field, w, gt, dev)
     poses0 = synth.perturb_poses(gt, w.K, w.max_rot_deg, w.max_trans, args.seed)
@@ -326,8 +337,9 @@ def main():
     # 3*64 + 64*64 + 64*15, density 16*64 + 64*din
     mac_fwd = din * 64 + 64 * 16 + 16 * 64 + 64 * 64 + 64 * 3
     mac_bwd = 3 * 64 + 64 * 64 + 64 * 15 + 16 * 64 + 64 * din
-    # the MLP kernels run v_mfma_f32_16x16x32_bf16 on split (hi + lo) operands:
-    # three bf16 products per fp32 product, priced against the bf16 peak
+    # the MLP kernels run v_mfma_f32_16x16x32_bf16 on split (hi + lo) operands
+    # (three bf16 products per fp32 product), or v_mfma_f32_16x16x32_f16 (one
+    # product); both priced against the 16-bit peak
     units = {"encode": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
              "mlp_fwd": ("mfma", 2 * mac_fwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
              "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
@@ -344,13 +356,16 @@ def main():
                             "avg_ms": prof[kname]["avg_ms"], "per_sample": per,
                             "_scale_bytes": 1e9 if bound == "hbm" else None}
         if bound == "mfma":
-            rooflines[kname]["executed_frac"] = 3 * ach / peak  # bf16 products issued
+            # 16-bit products issued
+            rooflines[kname]["executed_frac"] = (1 if args.mlp_precision else 3) * ach / peak
     dom_name = max(rooflines, key=lambda k: prof[k]["avg_ms"] * prof[k]["launches"])
     lpg = w.n_levels // 4
+    tf = {0: "false", 1: "true"}
+    h, dr = tf[args.mlp_precision], tf[args.sh_dir_grad]
     keys = {"encode": f"k_encode<{'true' if w.param_dtype == 'f16' else 'false'}, true>",
-            "mlp_fwd": f"k_mlp_fwd<{lpg}, true>",
-            "mlp_bwd": f"k_mlp_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}>",
-            "ray_bwd": f"k_ray_bwd<{lpg}, {'true' if args.sh_dir_grad else 'false'}, false>"}
+            "mlp_fwd": f"k_mlp_fwd<{lpg}, true, {h}>",
+            "mlp_bwd": f"k_mlp_bwd<{lpg}, {dr}, {h}>",
+            "ray_bwd": f"k_ray_bwd<{lpg}, {dr}, false, {h}>"}
     for kname, r in rooflines.items():
         tr = measured_traffic(w.name, keys[kname])
         # HBM bytes per launch (calibrated FETCH_SIZE + WRITE_SIZE), same units as achieved
@@ -381,8 +396,10 @@ def main():
         # the path's arithmetic: fp32 (or fp16-stored) table and weights, fp32
         # encoding and compositing; the MLPs as three bf16 MFMA products per fp32
         # product (hi*hi + hi*lo + lo*hi), accumulated in fp32
-        "dtype": ("f16-storage" if w.param_dtype == "f16" else "f32") + "+split-bf16x3-mfma",
-        "mlp_arithmetic": "bf16 MFMA on split hi/lo operands (3 products), fp32 accumulation",
+        "dtype": dtype_label(w, args),
+        "mlp_arithmetic": ("fp16 MFMA (weights and activations rounded to fp16, one product), "
+                           "fp32 accumulation" if args.mlp_precision else
+                           "bf16 MFMA on split hi/lo operands (3 products), fp32 accumulation"),
         "data": ("synthetic (seeded random frozen field" +
                  ("" if w.density == "random" else ", density shaped as one object in empty space") +
                  "; observation rendered at a seeded ground-truth pose)"),

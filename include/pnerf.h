@@ -157,6 +157,20 @@ typedef struct {
                                    2 = the fused kernel, also storing every
                                    sample's intermediates as 0 does
                                    (pnerf_field_inspect). */
+  int32_t mlp_precision;        /* arithmetic of both networks (forward and
+                                   backward):
+                                   0 = fp32-equivalent: each fp32 operand split
+                                   into two bf16 parts, three bf16 MFMA
+                                   products per fp32 product, fp32
+                                   accumulation (default);
+                                   1 = fp16 MFMA: each weight as two fp16
+                                   parts, each activation rounded to fp16, two
+                                   products, fp32 accumulation; the backward
+                                   scales each sample's incoming gradient by a
+                                   power of two (exact) to keep its fp16
+                                   operands normal.  Faster; results differ
+                                   from 0 by the activations' fp16 rounding
+                                   (2^-12 relative each). */
 } pnerf_field_params;
 
 /* Create a field: validates `params`, copies every array to the device (builds

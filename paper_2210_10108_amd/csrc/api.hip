@@ -70,6 +70,8 @@ struct pnerf_field {
   void* d_table = nullptr;
   void* d_wfwd = nullptr;
   void* d_wbwd = nullptr;
+  void* d_hfwd = nullptr;       // fp16 tiles (mlp_precision 1)
+  void* d_hbwd = nullptr;
   float* d_wc3 = nullptr;
   float* d_wd1 = nullptr;
   float* d_wd2 = nullptr;
@@ -151,11 +153,43 @@ struct Units {
   }
 };
 
+// fp32 -> fp16, round to nearest even (IEEE binary16, subnormals kept).
+uint16_t f16_rn(float x) {
+  uint32_t u;
+  std::memcpy(&u, &x, 4);
+  const uint16_t sign = (uint16_t)((u >> 16) & 0x8000u);
+  const uint32_t a = u & 0x7FFFFFFFu;
+  if (a > 0x7F800000u) return sign | 0x7E00u;   // NaN
+  if (a >= 0x477FF000u) return sign | 0x7C00u;  // from 65520 up: infinity
+  if (a < 0x38800000u) {                        // below 2^-14: multiples of 2^-24
+    float m;
+    std::memcpy(&m, &a, 4);
+    return sign | (uint16_t)std::nearbyint(m * 16777216.0f);  // exact product, ties to even
+  }
+  uint32_t r = a - 0x38000000u;                 // exponent bias 127 -> 15
+  r += 0xFFFu + ((r >> 13) & 1u);
+  return sign | (uint16_t)(r >> 13);
+}
+
+// The weight units of v_mfma_f32_16x16x32_f16: each fp32 weight as fp16
+// hi = rn(w) and lo = rn(w - hi) (w - hi is exact in fp32).
+struct HalfUnits {
+  std::vector<uint16_t> v;  // [unit][hi, lo][lane][8]
+  explicit HalfUnits(int n) : v((size_t)n * 2 * 64 * 8, 0) {}
+  void put(int unit, int lane, int j, float w) {
+    const uint16_t hi = f16_rn(w);
+    const uint16_t lo = f16_rn(w - half_to_float(hi));
+    v[(((size_t)unit * 2 + 0) * 64 + lane) * 8 + j] = hi;
+    v[(((size_t)unit * 2 + 1) * 64 + lane) * 8 + j] = lo;
+  }
+};
+
 // hidden unit at K position j of lane group g in K step s
 inline int kpos(int s, int g, int j) { return 16 * (2 * s + j / 4) + 4 * g + j % 4; }
 
-Units build_fwd_units(const Weights& W, int lpg) {
-  Units U(kFwdUnits);
+template <class U_t>
+U_t build_fwd_units(const Weights& W, int lpg) {
+  U_t U(kFwdUnits);
   for (int lane = 0; lane < 64; ++lane) {
     const int g = lane / 16, r = lane % 16;
     for (int j = 0; j < 8; ++j) {
@@ -181,8 +215,9 @@ Units build_fwd_units(const Weights& W, int lpg) {
   return U;
 }
 
-Units build_bwd_units(const Weights& W, int lpg) {
-  Units U(kBwdUnits);
+template <class U_t>
+U_t build_bwd_units(const Weights& W, int lpg) {
+  U_t U(kBwdUnits);
   const int MD = (lpg + 1) / 2;
   for (int lane = 0; lane < 64; ++lane) {
     const int g = lane / 16, r = lane % 16;
@@ -744,6 +779,8 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
     return fail(PNERF_ERR_INVALID_ARG, "overlap_chunks=%d outside 0..64", p->overlap_chunks);
   if (p->backward < 0 || p->backward > 2)
     return fail(PNERF_ERR_INVALID_ARG, "backward=%d outside 0..2", p->backward);
+  if (p->mlp_precision != 0 && p->mlp_precision != 1)
+    return fail(PNERF_ERR_INVALID_ARG, "mlp_precision=%d outside 0..1", p->mlp_precision);
 
   pnerf_field* F = new pnerf_field();
   auto cleanup_fail = [&](pnerf_status st) {
@@ -821,8 +858,9 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   load(p->w_color1, 32 * 64, W.c1);
   load(p->w_color2, 64 * 64, W.c2);
   load(p->w_color3, 64 * 3, W.c3);
-  Units uf = build_fwd_units(W, d.lpg);
-  Units ub = build_bwd_units(W, d.lpg);
+  Units uf = build_fwd_units<Units>(W, d.lpg);
+  Units ub = build_bwd_units<Units>(W, d.lpg);
+  d.mlp_f16 = p->mlp_precision;
 
   size_t table_elems = (size_t)L * d.T * 2;
   size_t table_bytes = table_elems * (p->param_dtype == 0 ? 4 : 2);
@@ -851,6 +889,20 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   d.wfwd = (const WeightUnit*)F->d_wfwd;
   d.wbwd = (const WeightUnit*)F->d_wbwd;
   d.wc3 = F->d_wc3;
+  d.hfwd = nullptr;
+  d.hbwd = nullptr;
+  if (d.mlp_f16) {
+    HalfUnits hf = build_fwd_units<HalfUnits>(W, d.lpg);
+    HalfUnits hb = build_bwd_units<HalfUnits>(W, d.lpg);
+    CF_TRY(hipMalloc(&F->d_hfwd, hf.v.size() * 2));
+    CF_TRY(hipMemcpyAsync(F->d_hfwd, hf.v.data(), hf.v.size() * 2, hipMemcpyHostToDevice, s));
+    CF_TRY(hipMalloc(&F->d_hbwd, hb.v.size() * 2));
+    CF_TRY(hipMemcpyAsync(F->d_hbwd, hb.v.data(), hb.v.size() * 2, hipMemcpyHostToDevice, s));
+    // the staging copies are synchronised before create returns
+    CF_TRY(hipStreamSynchronize(s));
+    d.hfwd = (const WeightUnit*)F->d_hfwd;
+    d.hbwd = (const WeightUnit*)F->d_hbwd;
+  }
   d.wd1 = F->d_wd1;
   d.wd2 = F->d_wd2;
   d.occ = nullptr;
@@ -867,9 +919,9 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   hipDeviceProp_t prop;
   CF_TRY(hipGetDeviceProperties(&prop, F->device));
   F->n_cu = prop.multiProcessorCount;
-  F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg);
-  F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad);
-  F->ray_blocks = F->n_cu * ray_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad);
+  F->fwd_blocks = F->n_cu * mlp_fwd_blocks_per_cu(d.lpg, d.mlp_f16);
+  F->bwd_blocks = F->n_cu * mlp_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad, d.mlp_f16);
+  F->ray_blocks = F->n_cu * ray_bwd_blocks_per_cu(d.lpg, d.sh_dir_grad, d.mlp_f16);
   F->backward = p->backward;
   CF_TRY(hipMalloc(&F->d_queue, sizeof(uint32_t) * kMaxLevels * kQueueStride));
   F->enc_blocks = encode_blocks(d, F->n_cu, 8);
@@ -892,6 +944,8 @@ void pnerf_destroy_field(pnerf_field* F) {
   (void)hipFree(F->d_table);
   (void)hipFree(F->d_wfwd);
   (void)hipFree(F->d_wbwd);
+  (void)hipFree(F->d_hfwd);
+  (void)hipFree(F->d_hbwd);
   (void)hipFree(F->d_wc3);
   (void)hipFree(F->d_wd1);
   (void)hipFree(F->d_wd2);

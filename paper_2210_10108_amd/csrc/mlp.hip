@@ -5,12 +5,20 @@
 // through the SH input to d loss / d direction), ending in each sample's force
 // and torque terms of Eq. 2 and Eq. 3.
 //
-// Arithmetic: every fp32 operand x is split into bf16 parts x = hi + lo + r
-// (|r| <= 2^-17 |x|), and each product is accumulated in fp32 as
-// hi*hi + hi*lo + lo*hi by v_mfma_f32_16x16x32_bf16 (the dropped lo*lo and r
-// terms are about 2^-16 of the product).  The weights are split once at field
-// creation; fp16-stored weights split exactly.  Activations are split two at a
-// time (split2): two packed converts and two bf16 dot products per pair.
+// Arithmetic (mlp_precision 0): every fp32 operand x is split into bf16 parts
+// x = hi + lo + r (|r| <= 2^-17 |x|), and each product is accumulated in fp32
+// as hi*hi + hi*lo + lo*hi by v_mfma_f32_16x16x32_bf16 (the dropped lo*lo and
+// r terms are about 2^-16 of the product).  The weights are split once at
+// field creation; fp16-stored weights split exactly.  Activations are split
+// two at a time (split2): two packed converts and two bf16 dot products per
+// pair.  mlp_precision 1: each weight as two fp16 parts w = hi + lo (split
+// once at field creation, |w - hi - lo| <= 2^-22 |w|), each activation
+// rounded to fp16, and two v_mfma_f32_16x16x32_f16 products hi*x + lo*x per
+// fp32 product, accumulated in fp32: the activation's rounding (2^-12) is the
+// only error of note, and one packed convert per pair replaces the split.  The
+// backward networks scale each sample's incoming gradient by a power of two
+// that puts its largest component in [16, 32), so that the fp16 operands stay
+// normal, and scale the result back (both exact).
 //
 // Work unit: one wavefront takes a tile of NT * 16 consecutive compacted
 // samples, as NT 16-sample column tiles.  The batch (sample) dimension is the MFMA N
@@ -35,6 +43,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBlock = 512;  // 8 wavefronts: one LDS copy of the weight units serves 8 waves
 constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
@@ -100,14 +110,8 @@ __device__ __forceinline__ Split load_unit(const WeightUnit* lds, int u, int lan
   return s;
 }
 
-// B operand of one K step from two accumulator tiles (rows of tile t0 at
-// positions 0..3, of tile t1 at 4..7).
-__device__ __forceinline__ Split pack2(const floatx4& t0, const floatx4& t1, const SplitK& k) {
-  const float v[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
-  return split8(v, k);
-}
-
-// The same for a ReLU layer: the B operand of relu(t0), relu(t1) and, when
+// The B operand of one K step from two accumulator tiles (rows of tile t0 at
+// positions 0..3, of tile t1 at 4..7) for a ReLU layer: relu(t0), relu(t1) and, when
 // MASK, its mask bits.  Position v of the K step is value pair p = v / 2:
 // the pair's bits are at shift + p (even v) and shift + p + 16 (odd v) of mk.
 // max(bits, 0) as a signed integer is the ReLU (every non-positive float, -0
@@ -140,11 +144,101 @@ __device__ __forceinline__ Split relu_pack2(const floatx4& t0, const floatx4& t1
   return s;
 }
 
-__device__ inline void stage(WeightUnit* lds, const WeightUnit* src, int n_units) {
+// Copy n_units weight units of `words` 16-byte words each to LDS.
+__device__ inline void stage(void* lds, const void* src, int n_units, int words) {
   const uint4* s = reinterpret_cast<const uint4*>(src);
   uint4* d = reinterpret_cast<uint4*>(lds);
-  for (int i = threadIdx.x; i < n_units * 128; i += kBlock) d[i] = s[i];
+  for (int i = threadIdx.x; i < n_units * words; i += kBlock) d[i] = s[i];
 }
+
+// An fp16 B operand of a K step (8 values per lane), and an fp16 A operand
+// as two parts.
+struct Half8 {
+  f16x8 v;
+};
+struct Half8x2 {
+  f16x8 hi, lo;
+};
+
+__device__ __forceinline__ uint32_t half2_rn(float x0, float x1) {
+  const f16x2 h = {(_Float16)x0, (_Float16)x1};
+  return __builtin_bit_cast(uint32_t, h);
+}
+
+// The two arithmetics behind one interface: the B operand type of a K step
+// (Op), the A operand (AOp, weights), and pack (8 values), relu_pack (relu of
+// two accumulator tiles, with their mask bits when MASK), mma (c += A B) and
+// load (A operand of a weight unit staged in LDS).
+template <bool H>
+struct Arith;
+
+template <>
+struct Arith<false> {
+  using Op = Split;
+  using AOp = Split;
+  using Unit = WeightUnit;
+  static constexpr int kWords = 128;  // 16-byte words per staged unit (hi and lo)
+  __device__ static __forceinline__ Op pack(const float v[8], const SplitK& k) {
+    return split8(v, k);
+  }
+  template <bool MASK>
+  __device__ static __forceinline__ Op relu_pack(const floatx4& t0, const floatx4& t1,
+                                                 const SplitK& k, uint32_t& mk, int shift) {
+    return relu_pack2<MASK>(t0, t1, k, mk, shift);
+  }
+  __device__ static __forceinline__ floatx4 mma(const AOp& a, const Op& b, floatx4 c) {
+    return mfma3(a, b, c);
+  }
+  __device__ static __forceinline__ AOp load(const Unit* lds, int u, int lane) {
+    return load_unit(lds, u, lane);
+  }
+  __device__ static __forceinline__ const Unit* fwd(const DevField& f) { return f.wfwd; }
+  __device__ static __forceinline__ const Unit* bwd(const DevField& f) { return f.wbwd; }
+};
+
+template <>
+struct Arith<true> {
+  using Op = Half8;
+  using AOp = Half8x2;
+  using Unit = WeightUnit;  // fp16 hi and lo parts
+  static constexpr int kWords = 128;
+  __device__ static __forceinline__ Op pack(const float v[8], const SplitK&) {
+    u32x4 w;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) w[p] = half2_rn(v[2 * p], v[2 * p + 1]);
+    return {__builtin_bit_cast(f16x8, w)};
+  }
+  // relu as in relu_pack2; a unit counts as active when its fp16 value is
+  // nonzero (positive values below 2^-25 round to zero and count as off),
+  // found by the same carry-free add: both halves are below 0x8000
+  template <bool MASK>
+  __device__ static __forceinline__ Op relu_pack(const floatx4& t0, const floatx4& t1,
+                                                 const SplitK&, uint32_t& mk, int shift) {
+    float v[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = __int_as_float(max(__float_as_int(v[i]), 0));
+    u32x4 w;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const uint32_t h = half2_rn(v[2 * p], v[2 * p + 1]);
+      w[p] = h;
+      if (MASK) {
+        const uint32_t top = h + 0x7FFF7FFFu;
+        mk |= (top >> (15 - shift - p)) & (0x00010001u << (shift + p));
+      }
+    }
+    return {__builtin_bit_cast(f16x8, w)};
+  }
+  __device__ static __forceinline__ floatx4 mma(const AOp& a, const Op& b, floatx4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.lo, b.v, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a.hi, b.v, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ AOp load(const Unit* lds, int u, int lane) {
+    return {__builtin_bit_cast(f16x8, lds[u].hi[lane]), __builtin_bit_cast(f16x8, lds[u].lo[lane])};
+  }
+  __device__ static __forceinline__ const Unit* fwd(const DevField& f) { return f.hfwd; }
+  __device__ static __forceinline__ const Unit* bwd(const DevField& f) { return f.hbwd; }
+};
 
 // Unit ray direction of sample s.
 __device__ __forceinline__ void sample_dir(const DevWork& w, int s, float d[3]) {
@@ -204,12 +298,14 @@ __device__ inline void sh4_vjp(const float d[3], int g, const float gs[4], float
 // ------------------------------------------------------------------ forward
 // GRAD = false (forward rendering only) skips the ReLU masks the backward
 // pass needs; it is a separate kernel so that profiles keep the two apart.
-template <int LPG, bool GRAD>
+template <int LPG, bool GRAD, bool H>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_mlp_fwd(DevField f, DevBatch b, DevWork w) {
+  using A = Arith<H>;
+  using Op = typename A::Op;
   constexpr int KD = 2 * LPG;  // features per lane group
   constexpr int NT = kFwdNT, TS = 16 * NT;
-  __shared__ WeightUnit lds[kFwdUnits];
-  stage(lds, f.wfwd, kFwdUnits);
+  __shared__ typename A::Unit lds[kFwdUnits];
+  stage(lds, A::fwd(f), kFwdUnits, A::kWords);
   __syncthreads();
 
   const int S = *w.total;
@@ -225,7 +321,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     // the weight units are re-read from LDS every tile (hoisted, they would
     // take ~160 registers and spill)
     asm volatile("" ::: "memory");
-    Split xf[NT];
+    Op xf[NT];
     float shv[NT][4];
     int sidx[NT];
 #pragma unroll
@@ -236,7 +332,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       float v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = j < KD ? frow[(int64_t)j * w.cap + sc] : 0.0f;
-      xf[nt] = split8(v, sk);
+      xf[nt] = A::pack(v, sk);
       // SH functions 4g..4g+3 of the sample's ray (sh16, stored per ray)
       const float4 sh = reinterpret_cast<const float4*>(w.rsh)[4 * w.sray[sc] + g];
       shv[nt][0] = sh.x;
@@ -248,9 +344,9 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     floatx4 acc[NT][4];
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
-      const Split a = load_unit(lds, kFD1 + m, lane);
+      const typename A::AOp a = A::load(lds, kFD1 + m, lane);
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[nt][m] = mfma3(a, xf[nt], zero);
+      for (int nt = 0; nt < NT; ++nt) acc[nt][m] = A::mma(a, xf[nt], zero);
     }
     // mask words: layer a at base 0 and colour layer 1 at base 8 of word 0,
     // colour layer 2 at base 0 of word 1 (bit layout: relu_pack2)
@@ -263,27 +359,28 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int nt = 0; nt < NT; ++nt) h[nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      const Split a = load_unit(lds, kFD2 + s2, lane);
+      const typename A::AOp a = A::load(lds, kFD2 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        h[nt] = mfma3(a, relu_pack2<GRAD>(acc[nt][2 * s2], acc[nt][2 * s2 + 1], sk, mw0[nt], 4 * s2),
-                      h[nt]);
+        h[nt] = A::mma(a, A::template relu_pack<GRAD>(acc[nt][2 * s2], acc[nt][2 * s2 + 1], sk,
+                                                      mw0[nt], 4 * s2),
+                       h[nt]);
     }
     // colour layer 1 on [h (h_0 has zero weights), SH_16]
     floatx4 b1[NT][4];
     {
-      Split xc[NT];
+      Op xc[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const float v[8] = {h[nt][0], h[nt][1], h[nt][2], h[nt][3],
                             shv[nt][0], shv[nt][1], shv[nt][2], shv[nt][3]};
-        xc[nt] = split8(v, sk);
+        xc[nt] = A::pack(v, sk);
       }
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
-        const Split a = load_unit(lds, kFC1 + m, lane);
+        const typename A::AOp a = A::load(lds, kFC1 + m, lane);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) b1[nt][m] = mfma3(a, xc[nt], zero);
+        for (int nt = 0; nt < NT; ++nt) b1[nt][m] = A::mma(a, xc[nt], zero);
       }
     }
     // colour layer 2 on relu(b1)
@@ -294,15 +391,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
       for (int m = 0; m < 4; ++m) b2[nt][m] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      Split x[NT];
+      Op x[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        x[nt] = relu_pack2<GRAD>(b1[nt][2 * s2], b1[nt][2 * s2 + 1], sk, mw0[nt], 8 + 4 * s2);
+        x[nt] = A::template relu_pack<GRAD>(b1[nt][2 * s2], b1[nt][2 * s2 + 1], sk, mw0[nt],
+                                            8 + 4 * s2);
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
-        const Split a = load_unit(lds, kFC2 + 2 * m + s2, lane);
+        const typename A::AOp a = A::load(lds, kFC2 + 2 * m + s2, lane);
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) b2[nt][m] = mfma3(a, x[nt], b2[nt][m]);
+        for (int nt = 0; nt < NT; ++nt) b2[nt][m] = A::mma(a, x[nt], b2[nt][m]);
       }
     }
     // colour layer 3 on relu(b2) (3 outputs in rows 0..2)
@@ -311,11 +409,12 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
     for (int nt = 0; nt < NT; ++nt) z[nt] = zero;
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
-      const Split a = load_unit(lds, kFC3 + s2, lane);
+      const typename A::AOp a = A::load(lds, kFC3 + s2, lane);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
-        z[nt] = mfma3(a, relu_pack2<GRAD>(b2[nt][2 * s2], b2[nt][2 * s2 + 1], sk, mw1[nt], 4 * s2),
-                      z[nt]);
+        z[nt] = A::mma(a, A::template relu_pack<GRAD>(b2[nt][2 * s2], b2[nt][2 * s2 + 1], sk,
+                                                      mw1[nt], 4 * s2),
+                       z[nt]);
     }
     // outputs: rows 0..3 live in lane group 0
 #pragma unroll
@@ -344,21 +443,35 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) voi
 // ----------------------------------------------------------------- backward
 // The backward networks for one 16-sample column tile: lane (g, col) holds
 // the sample of column col.  In: z = d loss / d z of that sample (zero when it
-// has none), gh0 = d loss / d h_0 on lane group 0 (zero elsewhere), the
+// has none), gh0 = d loss / d h_0 of that sample (in every lane group), the
 // sample's two ReLU mask words as the forward kernel stored them for this lane
 // group, and sc = the sample whose Jacobian records are read (any valid sample
 // when the column is empty).  Out: d loss / d p of the sample, gx (in every
 // lane group, after the sums over the groups), and on the direction path the
 // term d loss / d d through the SH input, gd (likewise summed).
-template <int LPG, bool DIR>
+template <int LPG, bool DIR, bool H>
 __device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
-                                         const WeightUnit* lds, const float* s_c3,
-                                         const SplitK& sk, int lane, const float z[3], float gh0,
-                                         uint32_t mw0, uint32_t mw1, int sc, const float d[3],
-                                         float gx[3], float gd[3]) {
+                                         const typename Arith<H>::Unit* lds, const float* s_c3,
+                                         const SplitK& sk, int lane, const float zin[3],
+                                         float gh0in, uint32_t mw0, uint32_t mw1, int sc,
+                                         const float d[3], float gx[3], float gd[3]) {
+  using A = Arith<H>;
+  using Op = typename A::Op;
   constexpr int MD = (LPG + 1) / 2;  // row tiles of d loss / d feature
   const int g = lane >> 4;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  // fp16 operands: the sample's gradient scaled by 2^k, its largest component
+  // (biased exponent ex) into [16, 32); k is kept within +-100
+  float scale = 1.0f, unscale = 1.0f;
+  if (H) {
+    const float m = fmaxf(fmaxf(fabsf(zin[0]), fabsf(zin[1])), fmaxf(fabsf(zin[2]), fabsf(gh0in)));
+    const int ex = (__float_as_int(m) >> 23) & 0xFF;
+    const int k = min(max(131 - ex, -100), 100);
+    scale = __int_as_float((127 + k) << 23);
+    unscale = __int_as_float((127 - k) << 23);
+  }
+  const float z[3] = {zin[0] * scale, zin[1] * scale, zin[2] * scale};
+  const float gh0 = g == 0 ? gh0in * scale : 0.0f;
   // colour layer 3 transposed, in fp32 on the vector ALUs: gb2 = W_c3 gz
   // (rows 16m + 4g + i of this lane), masked by layer 2's ReLU
   floatx4 gb2[4];
@@ -374,26 +487,31 @@ __device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
   floatx4 gb1[4] = {zero, zero, zero, zero};
 #pragma unroll
   for (int s2 = 0; s2 < 2; ++s2) {
-    const Split x = pack2(gb2[2 * s2], gb2[2 * s2 + 1], sk);
+    const float v[8] = {gb2[2 * s2][0], gb2[2 * s2][1], gb2[2 * s2][2], gb2[2 * s2][3],
+                        gb2[2 * s2 + 1][0], gb2[2 * s2 + 1][1], gb2[2 * s2 + 1][2], gb2[2 * s2 + 1][3]};
+    const Op x = A::pack(v, sk);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) gb1[m] = mfma3(load_unit(lds, kBC2 + 2 * m + s2, lane), x, gb1[m]);
+    for (int m = 0; m < 4; ++m) gb1[m] = A::mma(A::load(lds, kBC2 + 2 * m + s2, lane), x, gb1[m]);
   }
   apply_mask(gb1, mw0, 8);
   // colour layer 1 transposed: rows = h index (row 0 has zero weights); SH rows
   floatx4 gh = zero, gsh = zero;
 #pragma unroll
   for (int s2 = 0; s2 < 2; ++s2) {
-    const Split x = pack2(gb1[2 * s2], gb1[2 * s2 + 1], sk);
-    gh = mfma3(load_unit(lds, kBC1 + s2, lane), x, gh);
-    if (DIR) gsh = mfma3(load_unit(lds, kBSH + s2, lane), x, gsh);
+    const float v[8] = {gb1[2 * s2][0], gb1[2 * s2][1], gb1[2 * s2][2], gb1[2 * s2][3],
+                        gb1[2 * s2 + 1][0], gb1[2 * s2 + 1][1], gb1[2 * s2 + 1][2], gb1[2 * s2 + 1][3]};
+    const Op x = A::pack(v, sk);
+    gh = A::mma(A::load(lds, kBC1 + s2, lane), x, gh);
+    if (DIR) gsh = A::mma(A::load(lds, kBSH + s2, lane), x, gsh);
   }
   gh[0] += gh0;  // d loss / d h_0 (zero off group 0)
   // density layer 2 transposed: ga = W_d2 gh (one K step, upper half zero), masked
   floatx4 ga[4];
   {
-    const Split x = pack2(gh, zero, sk);
+    const float v[8] = {gh[0], gh[1], gh[2], gh[3], 0.f, 0.f, 0.f, 0.f};
+    const Op x = A::pack(v, sk);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) ga[m] = mfma3(load_unit(lds, kBD2 + m, lane), x, zero);
+    for (int m = 0; m < 4; ++m) ga[m] = A::mma(A::load(lds, kBD2 + m, lane), x, zero);
   }
   apply_mask(ga, mw0, 0);
   // density layer 1 transposed: row 4g + i of tile mm = feature i % 2 of
@@ -403,9 +521,12 @@ __device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
   for (int mm = 0; mm < MD; ++mm) gf[mm] = zero;
 #pragma unroll
   for (int s2 = 0; s2 < 2; ++s2) {
-    const Split x = pack2(ga[2 * s2], ga[2 * s2 + 1], sk);
+    const float v[8] = {ga[2 * s2][0], ga[2 * s2][1], ga[2 * s2][2], ga[2 * s2][3],
+                        ga[2 * s2 + 1][0], ga[2 * s2 + 1][1], ga[2 * s2 + 1][2], ga[2 * s2 + 1][3]};
+    const Op x = A::pack(v, sk);
 #pragma unroll
-    for (int mm = 0; mm < MD; ++mm) gf[mm] = mfma3(load_unit(lds, kBD1 + 2 * mm + s2, lane), x, gf[mm]);
+    for (int mm = 0; mm < MD; ++mm)
+      gf[mm] = A::mma(A::load(lds, kBD1 + 2 * mm + s2, lane), x, gf[mm]);
   }
   // d loss / d p = sum over the lane group's levels 4j + g of d loss / d
   // feature times the stored Jacobian, then over the 4 groups.  This lane
@@ -445,9 +566,10 @@ __device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
   for (int a = 0; a < 3; ++a) {
     gx[a] += __shfl_xor(gx[a], 16);
     gx[a] += __shfl_xor(gx[a], 32);
-    gx[a] *= f.inv_ext[a];  // d pos / d p = N_l / extent (N_l applied above)
+    gx[a] *= f.inv_ext[a] * unscale;  // d pos / d p = N_l / extent (N_l applied above)
     gd[a] += __shfl_xor(gd[a], 16);
     gd[a] += __shfl_xor(gd[a], 32);
+    gd[a] *= unscale;
   }
 }
 
@@ -456,13 +578,14 @@ __device__ __forceinline__ void bwd_tile(const DevField& f, const DevWork& w,
 // kernel, and storing each sample's torque and force terms for the
 // reduction.  DIR: the SH direction path (sh_dir_grad) is on; without it the
 // SH rows of colour layer 1 are not staged, and four blocks fit a CU's LDS.
-template <int LPG, bool DIR>
+template <int LPG, bool DIR, bool H>
 __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevWork w) {
   static_assert(kBwdNT == 1, "one column tile per wavefront");
+  using A = Arith<H>;
   constexpr int NU = DIR ? kBwdUnits : kBSH;  // staged weight units
-  __shared__ WeightUnit lds[NU];
+  __shared__ typename A::Unit lds[NU];
   __shared__ float s_c3[64 * 3];
-  stage(lds, f.wbwd, NU);
+  stage(lds, A::bwd(f), NU, A::kWords);
   for (int i = threadIdx.x; i < 64 * 3; i += kBlock) s_c3[i] = f.wc3[i];
   __syncthreads();
 
@@ -485,11 +608,11 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
     const int sc = s < S ? s : S - 1;
     const bool ok = s < S;
     const float z[3] = {ok ? w.cr[sc] : 0.0f, ok ? w.cg[sc] : 0.0f, ok ? w.cb[sc] : 0.0f};
-    const float gh0 = g == 0 && ok ? w.sig[sc] : 0.0f;
+    const float gh0 = ok ? w.sig[sc] : 0.0f;
     float d[3];
     sample_dir(w, sc, d);
     float gx[3], gd[3];
-    bwd_tile<LPG, DIR>(f, w, lds, s_c3, sk, lane, z, gh0, mw0, mw1, sc, d, gx, gd);
+    bwd_tile<LPG, DIR, H>(f, w, lds, s_c3, sk, lane, z, gh0, mw0, mw1, sc, d, gx, gd);
     // the sample's terms: force dL/dp, torque d x (t dL/dp + dL/dd)
     if (ok && g < 2) {
       const float t = w.t[s];
@@ -526,12 +649,13 @@ __global__ __launch_bounds__(kBlock) void k_mlp_bwd(DevField f, DevBatch b, DevW
 // gradient goes to memory.  KEEP also stores every sample's d loss / d h_0,
 // d loss / d z and (torque, force) terms as the separate kernels do
 // (inspection).
-template <int LPG, bool DIR, bool KEEP>
+template <int LPG, bool DIR, bool KEEP, bool H>
 __global__ __launch_bounds__(kBlock) void k_ray_bwd(DevField f, DevBatch b, DevWork w) {
+  using A = Arith<H>;
   constexpr int NU = DIR ? kBwdUnits : kBSH;
-  __shared__ WeightUnit lds[NU];
+  __shared__ typename A::Unit lds[NU];
   __shared__ float s_c3[64 * 3];
-  stage(lds, f.wbwd, NU);
+  stage(lds, A::bwd(f), NU, A::kWords);
   for (int i = threadIdx.x; i < 64 * 3; i += kBlock) s_c3[i] = f.wc3[i];
   __syncthreads();
 
@@ -623,8 +747,7 @@ __global__ __launch_bounds__(kBlock) void k_ray_bwd(DevField f, DevBatch b, DevW
         // 16 compacted samples left them for this lane group
         const uint32_t* mw = w.masks + (size_t)(s >> 4) * 2 * 64 + 16 * g + (s & 15);
         float gx[3], gd[3];
-        bwd_tile<LPG, DIR>(f, w, lds, s_c3, sk, lane, z, g == 0 ? gh : 0.0f, mw[0], mw[64], s,
-                           d, gx, gd);
+        bwd_tile<LPG, DIR, H>(f, w, lds, s_c3, sk, lane, z, gh, mw[0], mw[64], s, d, gx, gd);
         const float t = w.t[s];
         if (ok) {
 #pragma unroll
@@ -673,112 +796,142 @@ __global__ __launch_bounds__(kBlock) void k_ray_bwd(DevField f, DevBatch b, DevW
 
 }  // namespace
 
-int mlp_fwd_blocks_per_cu(int lpg) {
+namespace {
+// Resident blocks per CU of a kernel (1 if the query fails).
+template <class K>
+int blocks_per_cu(K kernel) {
   int n = 0;
-  hipError_t e = hipErrorInvalidValue;
-  switch (lpg) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_fwd<1, true>, kBlock, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_fwd<2, true>, kBlock, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_fwd<3, true>, kBlock, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k_mlp_fwd<4, true>, kBlock, 0); break;
-  }
+  const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kBlock, 0);
   return e == hipSuccess && n > 0 ? n : 1;
 }
 
-int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad) {
-  int n = 0;
-  hipError_t e = hipErrorInvalidValue;
-  const bool dir = sh_dir_grad != 0;
+template <bool H>
+int fwd_per_cu(int lpg) {
   switch (lpg) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<1, true> : k_mlp_bwd<1, false>, kBlock, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<2, true> : k_mlp_bwd<2, false>, kBlock, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<3, true> : k_mlp_bwd<3, false>, kBlock, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_mlp_bwd<4, true> : k_mlp_bwd<4, false>, kBlock, 0); break;
+    case 1: return blocks_per_cu(k_mlp_fwd<1, true, H>);
+    case 2: return blocks_per_cu(k_mlp_fwd<2, true, H>);
+    case 3: return blocks_per_cu(k_mlp_fwd<3, true, H>);
+    default: return blocks_per_cu(k_mlp_fwd<4, true, H>);
   }
-  return e == hipSuccess && n > 0 ? n : 1;
 }
 
-int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad) {
-  int n = 0;
-  hipError_t e = hipErrorInvalidValue;
-  const bool dir = sh_dir_grad != 0;
+template <bool DIR, bool H>
+int bwd_per_cu(int lpg) {
   switch (lpg) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<1, true, false> : k_ray_bwd<1, false, false>, kBlock, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<2, true, false> : k_ray_bwd<2, false, false>, kBlock, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<3, true, false> : k_ray_bwd<3, false, false>, kBlock, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, dir ? k_ray_bwd<4, true, false> : k_ray_bwd<4, false, false>, kBlock, 0); break;
+    case 1: return blocks_per_cu(k_mlp_bwd<1, DIR, H>);
+    case 2: return blocks_per_cu(k_mlp_bwd<2, DIR, H>);
+    case 3: return blocks_per_cu(k_mlp_bwd<3, DIR, H>);
+    default: return blocks_per_cu(k_mlp_bwd<4, DIR, H>);
   }
-  return e == hipSuccess && n > 0 ? n : 1;
+}
+
+template <bool DIR, bool H>
+int ray_per_cu(int lpg) {
+  switch (lpg) {
+    case 1: return blocks_per_cu(k_ray_bwd<1, DIR, false, H>);
+    case 2: return blocks_per_cu(k_ray_bwd<2, DIR, false, H>);
+    case 3: return blocks_per_cu(k_ray_bwd<3, DIR, false, H>);
+    default: return blocks_per_cu(k_ray_bwd<4, DIR, false, H>);
+  }
+}
+}  // namespace
+
+int mlp_fwd_blocks_per_cu(int lpg, int f16) {
+  return f16 ? fwd_per_cu<true>(lpg) : fwd_per_cu<false>(lpg);
+}
+
+int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad, int f16) {
+  if (sh_dir_grad) return f16 ? bwd_per_cu<true, true>(lpg) : bwd_per_cu<true, false>(lpg);
+  return f16 ? bwd_per_cu<false, true>(lpg) : bwd_per_cu<false, false>(lpg);
+}
+
+int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad, int f16) {
+  if (sh_dir_grad) return f16 ? ray_per_cu<true, true>(lpg) : ray_per_cu<true, false>(lpg);
+  return f16 ? ray_per_cu<false, true>(lpg) : ray_per_cu<false, false>(lpg);
 }
 
 namespace {
-template <bool GRAD>
+template <bool GRAD, bool H>
 void launch_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                 hipStream_t s) {
   switch (f.lpg) {
-    case 1: hipLaunchKernelGGL((k_mlp_fwd<1, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 2: hipLaunchKernelGGL((k_mlp_fwd<2, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 3: hipLaunchKernelGGL((k_mlp_fwd<3, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 4: hipLaunchKernelGGL((k_mlp_fwd<4, GRAD>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 1: hipLaunchKernelGGL((k_mlp_fwd<1, GRAD, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_mlp_fwd<2, GRAD, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_mlp_fwd<3, GRAD, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_mlp_fwd<4, GRAD, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
   }
+}
+
+template <bool DIR, bool H>
+hipError_t launch_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                      hipStream_t s) {
+  switch (f.lpg) {
+    case 1: hipLaunchKernelGGL((k_mlp_bwd<1, DIR, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_mlp_bwd<2, DIR, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_mlp_bwd<3, DIR, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_mlp_bwd<4, DIR, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <bool DIR, bool KEEP, bool H>
+hipError_t launch_ray(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                      hipStream_t s) {
+  switch (f.lpg) {
+    case 1: hipLaunchKernelGGL((k_ray_bwd<1, DIR, KEEP, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 2: hipLaunchKernelGGL((k_ray_bwd<2, DIR, KEEP, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 3: hipLaunchKernelGGL((k_ray_bwd<3, DIR, KEEP, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    case 4: hipLaunchKernelGGL((k_ray_bwd<4, DIR, KEEP, H>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <bool H>
+hipError_t launch_ray_h(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
+                        int keep, hipStream_t s) {
+  if (f.sh_dir_grad)
+    return keep ? launch_ray<true, true, H>(f, b, w, n_blocks, s)
+                : launch_ray<true, false, H>(f, b, w, n_blocks, s);
+  return keep ? launch_ray<false, true, H>(f, b, w, n_blocks, s)
+              : launch_ray<false, false, H>(f, b, w, n_blocks, s);
 }
 }  // namespace
 
 hipError_t launch_mlp_fwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                           int with_grad, hipStream_t s) {
   if (f.lpg < 1 || f.lpg > 4) return hipErrorInvalidValue;
-  if (with_grad)
-    launch_fwd<true>(f, b, w, n_blocks, s);
-  else
-    launch_fwd<false>(f, b, w, n_blocks, s);
-  return hipGetLastError();
-}
-
-namespace {
-template <bool DIR>
-hipError_t launch_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                      hipStream_t s) {
-  switch (f.lpg) {
-    case 1: hipLaunchKernelGGL((k_mlp_bwd<1, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 2: hipLaunchKernelGGL((k_mlp_bwd<2, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 3: hipLaunchKernelGGL((k_mlp_bwd<3, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 4: hipLaunchKernelGGL((k_mlp_bwd<4, DIR>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    default: return hipErrorInvalidValue;
+  if (f.mlp_f16) {
+    if (with_grad)
+      launch_fwd<true, true>(f, b, w, n_blocks, s);
+    else
+      launch_fwd<false, true>(f, b, w, n_blocks, s);
+  } else {
+    if (with_grad)
+      launch_fwd<true, false>(f, b, w, n_blocks, s);
+    else
+      launch_fwd<false, false>(f, b, w, n_blocks, s);
   }
   return hipGetLastError();
 }
-}  // namespace
 
 hipError_t launch_mlp_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                           hipStream_t s) {
-  if (f.sh_dir_grad)
-    return launch_bwd<true>(f, b, w, n_blocks, s);
-  return launch_bwd<false>(f, b, w, n_blocks, s);
+  if (f.mlp_f16)
+    return f.sh_dir_grad ? launch_bwd<true, true>(f, b, w, n_blocks, s)
+                         : launch_bwd<false, true>(f, b, w, n_blocks, s);
+  return f.sh_dir_grad ? launch_bwd<true, false>(f, b, w, n_blocks, s)
+                       : launch_bwd<false, false>(f, b, w, n_blocks, s);
 }
-
-namespace {
-template <bool DIR, bool KEEP>
-hipError_t launch_ray(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
-                      hipStream_t s) {
-  switch (f.lpg) {
-    case 1: hipLaunchKernelGGL((k_ray_bwd<1, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 2: hipLaunchKernelGGL((k_ray_bwd<2, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 3: hipLaunchKernelGGL((k_ray_bwd<3, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    case 4: hipLaunchKernelGGL((k_ray_bwd<4, DIR, KEEP>), dim3(n_blocks), dim3(kBlock), 0, s, f, b, w); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-}  // namespace
 
 hipError_t launch_ray_bwd(const DevField& f, const DevBatch& b, const DevWork& w, int n_blocks,
                           int keep, hipStream_t s) {
   // no more workgroups than the rays need (8 rays each)
   const int need = (b.n_rays + kBlock / 64 - 1) / (kBlock / 64);
   n_blocks = std::max(1, std::min(n_blocks, need));
-  if (f.sh_dir_grad)
-    return keep ? launch_ray<true, true>(f, b, w, n_blocks, s) : launch_ray<true, false>(f, b, w, n_blocks, s);
-  return keep ? launch_ray<false, true>(f, b, w, n_blocks, s) : launch_ray<false, false>(f, b, w, n_blocks, s);
+  return f.mlp_f16 ? launch_ray_h<true>(f, b, w, n_blocks, keep, s)
+                   : launch_ray_h<false>(f, b, w, n_blocks, keep, s);
 }
 
 }  // namespace pnerf

@@ -26,12 +26,14 @@ constexpr int kReduceParts = 64;      // parts per hypothesis of the reduction (
 constexpr int kAdamState = 16;        // Adam state floats per hypothesis: m[6], v[6], n, 3 pads
 
 // A operand of one (row tile, K step) of v_mfma_f32_16x16x32_bf16: 8 bf16
-// values per lane, as a high part and the low part of the fp32 weight.  Lane
+// values per lane, as a high part and the low part of the fp32 weight (for
+// v_mfma_f32_16x16x32_f16 the two parts are fp16).  Lane
 // l = 16 g + r supplies row r and K positions 8g .. 8g+7.
 struct alignas(16) WeightUnit {
   uint4 hi[64];
   uint4 lo[64];
 };
+
 // unit indices of the forward tiles: density layer 1 (4 row tiles), layer 2
 // (2 K steps), colour layer 1 (4 row tiles), layer 2 (4 x 2), layer 3 (2 K steps)
 constexpr int kFD1 = 0, kFD2 = 4, kFC1 = 6, kFC2 = 10, kFC3 = 18, kFwdUnits = 20;
@@ -106,6 +108,9 @@ struct DevField {
   const __half* table16;        // [L][T][2]
   const WeightUnit* wfwd;       // forward A-operand tiles [kFwdUnits]
   const WeightUnit* wbwd;       // backward A-operand tiles [kBwdUnits]
+  const WeightUnit* hfwd;       // the same tiles for v_mfma_f32_16x16x32_f16: fp16 hi
+  const WeightUnit* hbwd;       // and lo parts (mlp_precision 1)
+  int32_t mlp_f16;              // network arithmetic: 0 split bf16 (3 products), 1 fp16
   const float* wc3;             // W_c3 [64][3] (fp32, transposed colour layer 3)
   const float* wd1;             // plain W_d1 [2L][64] and W_d2 [64][16] (occupancy build)
   const float* wd2;
@@ -210,9 +215,9 @@ hipError_t launch_resample(int K, float* poses, float* state, int state_dim, con
 hipError_t resample_scratch(int device, int32_t** ptr, int* max_k);
 
 int reduce_parts(int K);
-int mlp_fwd_blocks_per_cu(int lpg);
-int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad);
-int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad);
+int mlp_fwd_blocks_per_cu(int lpg, int f16);
+int mlp_bwd_blocks_per_cu(int lpg, int sh_dir_grad, int f16);
+int ray_bwd_blocks_per_cu(int lpg, int sh_dir_grad, int f16);
 int encode_blocks(const DevField& f, int n_cu, int per_cu);
 
 }  // namespace pnerf

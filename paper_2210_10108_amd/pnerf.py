@@ -42,7 +42,8 @@ class FieldParams(C.Structure):
                 ("occ_threshold", C.c_float), ("background", C.c_float * 3),
                 ("loss_type", C.c_int32), ("loss_param", C.c_float),
                 ("sh_dir_grad", C.c_int32), ("max_workspace_bytes", C.c_int64),
-                ("overlap_chunks", C.c_int32), ("backward", C.c_int32)]
+                ("overlap_chunks", C.c_int32), ("backward", C.c_int32),
+                ("mlp_precision", C.c_int32)]
 
 
 _lib = None
@@ -136,7 +137,7 @@ class Field:
     """A frozen field on the current device (wraps pnerf_create_field)."""
 
     def __init__(self, spec, stream=None, max_workspace_bytes: int = 0, overlap_chunks: int = 0,
-                 backward: int = 0):
+                 backward: int = 0, mlp_precision: int = 0):
         self._h = C.c_void_p()
         f16 = spec.param_dtype == "f16"
         npdt = np.float16 if f16 else np.float32
@@ -171,6 +172,7 @@ class Field:
         p.max_workspace_bytes = int(max_workspace_bytes)
         p.overlap_chunks = int(overlap_chunks)
         p.backward = int(backward)
+        p.mlp_precision = int(mlp_precision)
         self.spec = spec
         self.occ_res = spec.occ_res
         _check(lib().pnerf_create_field(C.byref(p), _stream(stream), C.byref(self._h)))

@@ -58,7 +58,7 @@ int main(void) {{
   O(n_levels); O(level_res); O(table); O(w_color3); O(density_bias); O(aabb_max);
   O(march_mode); O(step); O(t_stop); O(occ_bits); O(occ_threshold); O(background);
   O(loss_type); O(loss_param); O(sh_dir_grad); O(max_workspace_bytes); O(overlap_chunks);
-  O(backward);
+  O(backward); O(mlp_precision);
   return 0;
 }}""")
     exe = tmp_path / "layout"
