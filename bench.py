@@ -338,8 +338,9 @@ def main():
     mac_fwd = din * 64 + 64 * 16 + 16 * 64 + 64 * 64 + 64 * 3
     mac_bwd = 3 * 64 + 64 * 64 + 64 * 15 + 16 * 64 + 64 * din
     # the MLP kernels run v_mfma_f32_16x16x32_bf16 on split (hi + lo) operands
-    # (three bf16 products per fp32 product), or v_mfma_f32_16x16x32_f16 (one
-    # product); both priced against the 16-bit peak
+    # (three bf16 products per fp32 product), or v_mfma_f32_16x16x32_f16 (two:
+    # the weight's two fp16 parts times the fp16 activation); both priced
+    # against the 16-bit peak
     units = {"encode": ("hbm", gather_bytes, PEAK_HBM, "GB/s", 1e9),
              "mlp_fwd": ("mfma", 2 * mac_fwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
              "mlp_bwd": ("mfma", 2 * mac_bwd, PEAK_BF16_MFMA, "TFLOP/s", 1e12),
@@ -356,8 +357,9 @@ def main():
                             "avg_ms": prof[kname]["avg_ms"], "per_sample": per,
                             "_scale_bytes": 1e9 if bound == "hbm" else None}
         if bound == "mfma":
-            # 16-bit products issued
-            rooflines[kname]["executed_frac"] = (1 if args.mlp_precision else 3) * ach / peak
+            # 16-bit products issued: three bf16 (split) or two fp16 (weights
+            # as two parts) per fp32 product
+            rooflines[kname]["executed_frac"] = (2 if args.mlp_precision else 3) * ach / peak
     dom_name = max(rooflines, key=lambda k: prof[k]["avg_ms"] * prof[k]["launches"])
     lpg = w.n_levels // 4
     tf = {0: "false", 1: "true"}
@@ -397,8 +399,8 @@ def main():
         # encoding and compositing; the MLPs as three bf16 MFMA products per fp32
         # product (hi*hi + hi*lo + lo*hi), accumulated in fp32
         "dtype": dtype_label(w, args),
-        "mlp_arithmetic": ("fp16 MFMA (weights and activations rounded to fp16, one product), "
-                           "fp32 accumulation" if args.mlp_precision else
+        "mlp_arithmetic": ("fp16 MFMA (weights as two fp16 parts, activations rounded to fp16, "
+                           "two products), fp32 accumulation" if args.mlp_precision else
                            "bf16 MFMA on split hi/lo operands (3 products), fp32 accumulation"),
         "data": ("synthetic (seeded random frozen field" +
                  ("" if w.density == "random" else ", density shaped as one object in empty space") +
