@@ -307,21 +307,17 @@ def main():
     run(W + S, 0, poses, mom, count=True, counts=counts)
     timed_samples = int(sum(counts[W:]))
 
-    # timed run
+    # timed run, with HIP events recorded around every kernel launch on the
+    # stream it runs on (read once the clock has stopped): the per-kernel
+    # times are those of the timed steps themselves
     poses, mom = fresh()
     run(W, 0, poses, mom)
     torch.cuda.synchronize()
+    field.set_profiling(True)
     t0 = time.perf_counter()
     run(S, W, poses, mom)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-
-    # per-kernel HIP-event timing over an identical pass
-    poses, mom = fresh()
-    run(W, 0, poses, mom)
-    field.set_profiling(True)
-    run(S, W, poses, mom)
-    torch.cuda.synchronize()
     prof = {name: {"launches": n, "avg_ms": ms / max(n, 1)} for name, n, ms in field.profile()}
     field.set_profiling(False)
 
