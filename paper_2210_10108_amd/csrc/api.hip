@@ -107,6 +107,7 @@ struct pnerf_field {
   bool profiling = false;
   std::vector<KernelStat> stats;
   std::vector<PendingEvent> pending;
+  std::vector<hipEvent_t> ev_pool;  // timing events made once, reused across launches
 };
 
 namespace {
@@ -451,10 +452,16 @@ hipError_t timed(pnerf_field* F, const char* name, hipStream_t s, Fn fn) {
     idx = (int)F->stats.size() - 1;
   }
   PendingEvent pe{idx, nullptr, nullptr};
-  hipError_t e = hipEventCreate(&pe.a);
-  if (e != hipSuccess) return e;
-  e = hipEventCreate(&pe.b);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
+  for (hipEvent_t* ev : {&pe.a, &pe.b}) {
+    if (F->ev_pool.empty()) {
+      e = hipEventCreate(ev);
+      if (e != hipSuccess) return e;
+    } else {
+      *ev = F->ev_pool.back();
+      F->ev_pool.pop_back();
+    }
+  }
   e = hipEventRecord(pe.a, s);
   if (e != hipSuccess) return e;
   e = fn();
@@ -471,8 +478,8 @@ pnerf_status resolve_profile(pnerf_field* F) {
     float ms = 0.0f;
     HIP_TRY(hipEventElapsedTime(&ms, pe.a, pe.b));
     F->stats[pe.idx].total_ms += ms;
-    (void)hipEventDestroy(pe.a);
-    (void)hipEventDestroy(pe.b);
+    F->ev_pool.push_back(pe.a);
+    F->ev_pool.push_back(pe.b);
   }
   F->pending.clear();
   return PNERF_OK;
@@ -941,6 +948,7 @@ void pnerf_destroy_field(pnerf_field* F) {
     (void)hipEventDestroy(pe.a);
     (void)hipEventDestroy(pe.b);
   }
+  for (hipEvent_t ev : F->ev_pool) (void)hipEventDestroy(ev);
   (void)hipFree(F->d_table);
   (void)hipFree(F->d_wfwd);
   (void)hipFree(F->d_wbwd);
@@ -1133,7 +1141,16 @@ pnerf_status pnerf_field_set_profiling(pnerf_field* F, int32_t enable) {
   if (!F) return fail(PNERF_ERR_INVALID_ARG, "NULL field");
   pnerf_status st = resolve_profile(F);
   if (st != PNERF_OK) return st;
-  if (enable) F->stats.clear();
+  if (enable) {
+    F->stats.clear();
+    // events for the first launches, made before any is timed
+    HIP_TRY(hipSetDevice(F->device));
+    while (F->ev_pool.size() < 512) {
+      hipEvent_t ev;
+      HIP_TRY(hipEventCreate(&ev));
+      F->ev_pool.push_back(ev);
+    }
+  }
   F->profiling = enable != 0;
   return PNERF_OK;
 }

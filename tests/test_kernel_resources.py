@@ -15,9 +15,9 @@ from paper_2210_10108_amd import build
 BUDGET = {
     "encode.hip": {"k_encodeILb0ELb1E": 7},
     # <levels per lane group, (SH direction path,) (keep,) fp16>
-    "mlp.hip": {"k_mlp_fwdILi4ELb1ELb0E": 8, "k_mlp_bwdILi4ELb0ELb0E": 8,
+    "mlp.hip": {"k_mlp_fwdILi4ELb1ELb0E": 8, "k_mlp_bwdILi4ELb0ELb0E": 7,
                 "k_mlp_bwdILi4ELb1ELb0E": 6, "k_ray_bwdILi4ELb0ELb0ELb0E": 4,
-                "k_mlp_fwdILi4ELb1ELb1E": 7, "k_mlp_bwdILi4ELb0ELb1E": 8,
+                "k_mlp_fwdILi4ELb1ELb1E": 8, "k_mlp_bwdILi4ELb0ELb1E": 8,
                 "k_mlp_bwdILi4ELb1ELb1E": 6},
 }
 
