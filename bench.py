@@ -320,6 +320,15 @@ def main():
     elapsed = time.perf_counter() - t0
     prof = {name: {"launches": n, "avg_ms": ms / max(n, 1)} for name, n, ms in field.profile()}
     field.set_profiling(False)
+    # the same steps again without the events: their cost on the device (a few
+    # microseconds per launch) shows on workloads whose launches are short
+    poses, mom = fresh()
+    run(W, 0, poses, mom)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    run(S, W, poses, mom)
+    torch.cuda.synchronize()
+    elapsed_plain = time.perf_counter() - t1
 
     samples_per_step = timed_samples / S
     # roofline of every per-sample kernel: algorithmic units per sample x samples
@@ -408,6 +417,8 @@ def main():
                    "backward": "separate-kernels" if args.backward == 0 else "fused-per-ray",
                    "parallelism": "single-gpu"},
         "hypothesis_iters_per_sec": K * S / elapsed,
+        "without_kernel_events": {"value": timed_samples / elapsed_plain,
+                                  "ms_per_step": elapsed_plain / S * 1e3},
         "samples_per_step": samples_per_step,
         "mean_samples_per_ray": samples_per_step / w.n_rays,
         "roofline": roof,
