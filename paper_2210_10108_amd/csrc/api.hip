@@ -868,6 +868,12 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   Units uf = build_fwd_units<Units>(W, d.lpg);
   Units ub = build_bwd_units<Units>(W, d.lpg);
   d.mlp_f16 = p->mlp_precision;
+  // the fp16 network's tiles, built on the host with the others
+  HalfUnits hf(d.mlp_f16 ? kFwdUnits : 0), hb(d.mlp_f16 ? kBwdUnits : 0);
+  if (d.mlp_f16) {
+    hf = build_fwd_units<HalfUnits>(W, d.lpg);
+    hb = build_bwd_units<HalfUnits>(W, d.lpg);
+  }
 
   size_t table_elems = (size_t)L * d.T * 2;
   size_t table_bytes = table_elems * (p->param_dtype == 0 ? 4 : 2);
@@ -899,14 +905,10 @@ pnerf_status pnerf_create_field(const pnerf_field_params* p, void* stream, pnerf
   d.hfwd = nullptr;
   d.hbwd = nullptr;
   if (d.mlp_f16) {
-    HalfUnits hf = build_fwd_units<HalfUnits>(W, d.lpg);
-    HalfUnits hb = build_bwd_units<HalfUnits>(W, d.lpg);
     CF_TRY(hipMalloc(&F->d_hfwd, hf.v.size() * 2));
     CF_TRY(hipMemcpyAsync(F->d_hfwd, hf.v.data(), hf.v.size() * 2, hipMemcpyHostToDevice, s));
     CF_TRY(hipMalloc(&F->d_hbwd, hb.v.size() * 2));
     CF_TRY(hipMemcpyAsync(F->d_hbwd, hb.v.data(), hb.v.size() * 2, hipMemcpyHostToDevice, s));
-    // the staging copies are synchronised before create returns
-    CF_TRY(hipStreamSynchronize(s));
     d.hfwd = (const WeightUnit*)F->d_hfwd;
     d.hbwd = (const WeightUnit*)F->d_hbwd;
   }

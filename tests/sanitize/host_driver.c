@@ -78,7 +78,7 @@ static void validation(void) {
 }
 
 /* A tiny field in float32 or float16 storage. */
-static void creation(int f16, int march_mode, int L) {
+static void creation(int f16, int march_mode, int L, int mlp_precision) {
   const int T = 1 << 10, din = 2 * L;
   int32_t res[16];
   for (int l = 0; l < L; ++l) res[l] = 4 + 3 * l;
@@ -120,6 +120,7 @@ static void creation(int f16, int march_mode, int L) {
   p.max_samples = 100;
   p.occ_res = march_mode ? 8 : 0;
   p.loss_param = 0.1f;
+  p.mlp_precision = mlp_precision;
   pnerf_field* F = NULL;
   pnerf_status st = pnerf_create_field(&p, NULL, &F);
   /* without a GPU the first device allocation fails after the host work */
@@ -133,6 +134,12 @@ static void creation(int f16, int march_mode, int L) {
   p.loss_type = 9;
   EXPECT(pnerf_create_field(&p, NULL, &F) == PNERF_ERR_INVALID_ARG);
   p.loss_type = 0;
+  p.backward = 3;
+  EXPECT(pnerf_create_field(&p, NULL, &F) == PNERF_ERR_INVALID_ARG);
+  p.backward = 0;
+  p.mlp_precision = 2;
+  EXPECT(pnerf_create_field(&p, NULL, &F) == PNERF_ERR_INVALID_ARG);
+  p.mlp_precision = mlp_precision;
   p.step = 1e-9f;
   p.march_mode = 1;
   EXPECT(pnerf_create_field(&p, NULL, &F) == PNERF_ERR_INVALID_ARG);
@@ -144,8 +151,10 @@ int main(void) {
   planning();
   validation();
   for (int L = 4; L <= 16; L += 4) {
-    creation(0, 0, L);
-    creation(1, 1, L);
+    for (int mlp = 0; mlp <= 1; ++mlp) {
+      creation(0, 0, L, mlp);
+      creation(1, 1, L, mlp);
+    }
   }
   if (failures) fprintf(stderr, "%d failures\n", failures);
   printf("host driver done\n");
