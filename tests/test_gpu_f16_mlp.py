@@ -112,24 +112,27 @@ def test_f16_loss_grad_tiny(pn, overrides):
     check_f16("tiny32 " + str(overrides), case, of, obs, ref, *gpu_loss_grad(pn, case, obs))
 
 
-@pytest.mark.parametrize("n_levels,sh_dir", [(8, 0), (12, 1), (16, 0)])
-def test_f16_loss_grad_level_counts(pn, monkeypatch, n_levels, sh_dir):
+@pytest.mark.parametrize("n_levels,sh_dir,backward", [(8, 0, 0), (12, 1, 0), (16, 0, 0), (12, 0, 2)])
+def test_f16_loss_grad_level_counts(pn, monkeypatch, n_levels, sh_dir, backward):
     name = f"tiny32_l{n_levels}"
     w = dataclasses.replace(synth.WORKLOADS["tiny32"], name=name, n_levels=n_levels, log2_table=14)
     monkeypatch.setitem(synth.WORKLOADS, name, w)
     case = G.make_case(name, K=8, P=256, dense_coarse_levels=1, sh_dir_grad=sh_dir)
     of, obs, ref = oracle_case(case)
-    check_f16(name, case, of, obs, ref, *gpu_loss_grad(pn, case, obs))
+    check_f16(name, case, of, obs, ref, *gpu_loss_grad(pn, case, obs, backward=backward))
 
 
-def test_f16_loss_grad_early_stop_and_occupancy(pn):
+@pytest.mark.parametrize("sh_dir,backward", [(0, 0), (1, 0), (1, 2)])
+def test_f16_loss_grad_early_stop_and_occupancy(pn, sh_dir, backward):
     R = 16
     case = G.make_case("tiny32", K=3, P=200, march_mode=1, step=math.sqrt(3) / 384,
                        max_samples=600, t_stop=1e-2, occ_res=R, density_bias=2.5,
-                       occ_bits=synth.occupancy_pattern("sphere", R), background=(0.5, 0.2, 0.9))
+                       occ_bits=synth.occupancy_pattern("sphere", R), background=(0.5, 0.2, 0.9),
+                       sh_dir_grad=sh_dir)
     of, obs, ref = oracle_case(case)
     assert np.sum(ref["stop"] < np.diff(ref["march"][0])) >= 5
-    check_f16("early stop", case, of, obs, ref, *gpu_loss_grad(pn, case, obs))
+    check_f16(f"early stop sh_dir={sh_dir} backward={backward}", case, of, obs, ref,
+              *gpu_loss_grad(pn, case, obs, backward=backward))
 
 
 def test_f16_loss_grad_tiny_gradients_are_scaled(pn):

@@ -366,7 +366,8 @@ def test_loss_grad_ngp800_uniform_full_batch(pn):
     assert stats["samples"] == int(ref["march"][0][-1])
 
 
-def test_loss_grad_ngp800_occ128_full_batch_sampled_hypotheses(pn):
+@pytest.mark.parametrize("backward", [0, 2])
+def test_loss_grad_ngp800_occ128_full_batch_sampled_hypotheses(pn, backward):
     # the full 64 x 4096 batch on the GPU; hypotheses are independent, so the
     # oracle recomputes a sample of them; occupancy grid built by the oracle
     w = synth.WORKLOADS["ngp800_occ128"]
@@ -378,7 +379,7 @@ def test_loss_grad_ngp800_occ128_full_batch_sampled_hypotheses(pn):
     hyps = [0, 31, 63]
     obs = G.oracle_observation(of, case.gt, case.pix[hyps], case.intr)
     ref = oracle_subset(of, case, obs, hyps)
-    check_full(pn, case, obs, ref, of, hyps=hyps)
+    check_full(pn, case, obs, ref, of, hyps=hyps, backward=backward)
 
 
 def test_loss_grad_chunked_matches_single_chunk(pn):
