@@ -56,6 +56,10 @@ def parse():
     ap.add_argument("--backward", type=int, default=0, choices=(0, 1),
                     help="0: separate composite, network backward and reduction kernels; "
                          "1: the fused per-ray backward kernel")
+    ap.add_argument("--graph", action="store_true",
+                    help="also record one step (loss gradient + optimizer step) into a HIP graph "
+                         "and time its replays (workloads without resampling whose batch fits "
+                         "one sample buffer)")
     ap.add_argument("--mlp-precision", type=int, default=0, choices=(0, 1),
                     help="0: split-bf16 MFMA (three products, fp32-equivalent); "
                          "1: fp16 MFMA (one product, fp32 accumulation)")
@@ -81,6 +85,40 @@ def render_observation(field, w, gt, dev):
         ids = torch.arange(s, e, dtype=torch.int32, device=dev)[None]
         out[s:e] = field.render(pose, ids, intr)[0]
     return out.reshape(w.height, w.width, 3)
+
+
+def graph_replay(field, w, obs, intr, pix, fresh, adam, loss, dpose, S, W):
+    """One step -- the loss gradient and the momentum step -- recorded into a
+    HIP graph by stream capture and replayed W + S times from the initial
+    poses (S timed), each replay's pixel ids copied into the recorded buffer
+    first: the eager steps' work without a host launch per kernel."""
+    import torch
+    from paper_2210_10108_amd import pnerf
+    if w.resample_every:
+        return {"unsupported": "the workload resamples between steps"}
+    if adam is not None:
+        return {"unsupported": "the Adam step takes its step number from the host"}
+    poses, mom = fresh()
+    pix_buf = pix[0].clone()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    try:
+        with torch.cuda.graph(g):
+            field.render_loss_grad(poses, pix_buf, obs, intr, loss, dpose)
+            pnerf.step_momentum(poses, mom, dpose, w.lr, w.beta)
+    except pnerf.PnerfError as e:
+        torch.cuda.synchronize()
+        return {"unsupported": str(e)}
+    for i in range(W):
+        pix_buf.copy_(pix[i % len(pix)])
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(W, W + S):
+        pix_buf.copy_(pix[i % len(pix)])
+        g.replay()
+    torch.cuda.synchronize()
+    return {"ms_per_step": (time.perf_counter() - t0) / S * 1e3}
 
 
 def dtype_label(w, args):
@@ -330,6 +368,12 @@ def main():
     torch.cuda.synchronize()
     elapsed_plain = time.perf_counter() - t1
 
+    graph = None
+    if args.graph:
+        graph = graph_replay(field, w, obs, intr, pix, fresh, adam, loss, dpose, S, W)
+        if "ms_per_step" in graph:
+            graph["value"] = timed_samples / (graph["ms_per_step"] * 1e-3 * S)
+
     samples_per_step = timed_samples / S
     # roofline of every per-sample kernel: algorithmic units per sample x samples
     # per launch / average launch time (HIP events on the call's stream)
@@ -417,6 +461,7 @@ def main():
                    "backward": "separate-kernels" if args.backward == 0 else "fused-per-ray",
                    "parallelism": "single-gpu"},
         "hypothesis_iters_per_sec": K * S / elapsed,
+        "graph_replay": graph,
         "without_kernel_events": {"value": timed_samples / elapsed_plain,
                                   "ms_per_step": elapsed_plain / S * 1e3},
         "samples_per_step": samples_per_step,

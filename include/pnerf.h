@@ -193,7 +193,13 @@ void pnerf_destroy_field(pnerf_field* field);
  * poses (device) [K][3][4]; pixel_ids (device) int32 [K][P], each in [0, W*H);
  * observed (device) float32 [H][W][3]; loss (device) [K]; dpose (device) [K][6].
  * Limits: 1 <= K <= 65535, P >= 1, K*P < 2^31, pixel ids in range (not checked on the
- * device: out-of-range ids are undefined behaviour). */
+ * device: out-of-range ids are undefined behaviour).
+ * Stream capture: the call can be recorded into a HIP graph (and replayed with
+ * new poses and pixel ids in the same buffers) when it only enqueues kernels:
+ * the field has already run a batch of this shape (no workspace growth), the
+ * batch's worst case (every ray at its sample cap) fits one sample buffer, so
+ * that no read of its sample totals is needed, and profiling is off.  Otherwise
+ * it returns PNERF_ERR_NOT_SUPPORTED under capture, having enqueued nothing. */
 pnerf_status pnerf_render_loss_grad(pnerf_field* field, int32_t K, const float* poses,
                                     int32_t P, const int32_t* pixel_ids,
                                     const float* observed, const pnerf_intrinsics* intr,

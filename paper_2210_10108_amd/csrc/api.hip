@@ -355,7 +355,20 @@ int64_t bytes_per_sample(const DevField& f) {
   return (int64_t)carve_samples(f, 64 * kTile, nullptr, nullptr) / (64 * kTile) + 1;
 }
 
-pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s) {
+// Under stream capture nothing may be allocated or waited for: a workspace
+// that would have to grow is refused instead.
+pnerf_status refuse_growth_in_capture(bool capturing, const char* what) {
+  if (!capturing) return PNERF_OK;
+  return fail(PNERF_ERR_NOT_SUPPORTED,
+              "the %s would grow under stream capture: run the same shape once outside the "
+              "capture first", what);
+}
+
+pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s, bool capturing) {
+  if (n_rays > F->rays_cap || n_hyp > F->rays_hyp || n_hyp > F->h_hyp_cap) {
+    pnerf_status st = refuse_growth_in_capture(capturing, "ray workspace");
+    if (st != PNERF_OK) return st;
+  }
   if (n_rays > F->rays_cap || n_hyp > F->rays_hyp) {
     n_rays = std::max(n_rays, F->rays_cap);
     n_hyp = std::max(n_hyp, F->rays_hyp);
@@ -391,7 +404,11 @@ pnerf_status ensure_rays(pnerf_field* F, int n_rays, int n_hyp, hipStream_t s) {
 // quarter more than asked when it grows, within `limit`), and the per-chunk
 // totals to n_chunks.
 pnerf_status ensure_samples(pnerf_field* F, int64_t need, int64_t limit, int n_chunks, int slots,
-                            hipStream_t s) {
+                            hipStream_t s, bool capturing) {
+  if (n_chunks > F->max_chunks || std::max<int64_t>(need, 1) > F->samp_cap || slots > F->n_slots) {
+    pnerf_status st = refuse_growth_in_capture(capturing, "sample workspace");
+    if (st != PNERF_OK) return st;
+  }
   if (n_chunks > F->max_chunks) {
     if (F->d_totals) {
       HIP_TRY(hipStreamSynchronize(s));
@@ -533,6 +550,14 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
                  float* dpose, float* rgb, int64_t* ray_offset, float* t_out, int32_t* j_out,
                  int64_t capacity, hipStream_t s) {
   HIP_TRY(hipSetDevice(F->device));
+  // under stream capture (a HIP graph being recorded) the call may only
+  // enqueue kernels: no allocation, no event timing, no read of the totals
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  HIP_TRY(hipStreamIsCapturing(s, &cs));
+  const bool capturing = cs != hipStreamCaptureStatusNone;
+  if (capturing && (mode != kLossGrad || F->profiling))
+    return fail(PNERF_ERR_NOT_SUPPORTED, "only render_loss_grad, without profiling, can be "
+                                         "recorded under stream capture");
   F->last_total_dev = nullptr;
   F->last_keeps_samples = mode != kLossGrad || F->backward != 1;
   const int64_t max_rays = (int64_t)kMaxScanBlocks * 256;
@@ -541,7 +566,7 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
   if (st != PNERF_OK) return st;
   if (mode == kMarch && kr < K)
     return fail(PNERF_ERR_CAPACITY, "march inspection needs K*P <= %lld rays", (long long)max_rays);
-  st = ensure_rays(F, kr * P, kr, s);
+  st = ensure_rays(F, kr * P, kr, s, capturing);
   if (st != PNERF_OK) return st;
   const int64_t per_sample = bytes_per_sample(F->dev);  // per buffer
   const int64_t limit = std::min<int64_t>(
@@ -567,8 +592,12 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
     const int64_t worst = (int64_t)hn * P * F->dev.max_per_ray;
     const bool device_sized = mode == kLossGrad && !pipe && hn == K && worst <= limit &&
                               worst * per_sample <= kDeviceSizedBytes;
+    if (capturing && !device_sized)
+      return fail(PNERF_ERR_NOT_SUPPORTED,
+                  "this batch needs the host's chunk plan (a read of its sample totals), which "
+                  "stream capture cannot record");
     // the totals array for the counted batch (and, device-sized, the whole buffer)
-    st = ensure_samples(F, device_sized ? worst : 0, slot_limit, chunk_id + 1, 1, s);
+    st = ensure_samples(F, device_sized ? worst : 0, slot_limit, chunk_id + 1, 1, s, capturing);
     if (st != PNERF_OK) return st;
     DevWork wb = counted_work(F);
     int raw_blocks = 0;  // device-sized: the write pass may finish the offset scan itself
@@ -601,7 +630,8 @@ pnerf_status run(pnerf_field* F, Mode mode, int32_t K, const float* poses, int32
       int64_t biggest = 0;
       for (int64_t v : sums) biggest = std::max(biggest, v);
       overlap = pipe_here && sums.size() > 1;
-      st = ensure_samples(F, biggest, cap_c, chunk_id + (int)sums.size(), overlap ? 2 : 1, s);
+      st = ensure_samples(F, biggest, cap_c, chunk_id + (int)sums.size(), overlap ? 2 : 1, s,
+                          false);
       if (st != PNERF_OK) return st;
       wb = counted_work(F);
     }
