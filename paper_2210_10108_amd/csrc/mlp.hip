@@ -48,7 +48,7 @@ typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kBlock = 512;  // 8 wavefronts: one LDS copy of the weight units serves 8 waves
 constexpr int kFwdNT = 1;    // 16-sample column tiles per wavefront, forward
-constexpr int kBwdNT = 1;    // and backward (62 registers without the SH direction path: 8 wavefronts per SIMD)
+constexpr int kBwdNT = 1;    // and backward (68 registers without the SH direction path: 7 wavefronts per SIMD)
 
 struct Split {
   bf16x8 hi, lo;
