@@ -291,6 +291,24 @@ def test_inspect_needs_a_backward_that_keeps_samples(pn):
     f.close()
 
 
+@pytest.mark.parametrize("seed", [1, 2, 3, 4])
+@pytest.mark.parametrize("lattice", [False, True])
+def test_loss_grad_other_seeds(pn, seed, lattice):
+    """Other fields, poses and pixel batches (seeds 1-4), uniform and lattice
+    marching with early stop: per-sample parity as above, the fused backward
+    keeping its per-sample values on odd seeds."""
+    kw = dict(K=3, P=300, pix_seed=seed)
+    if lattice:
+        kw.update(march_mode=1, step=math.sqrt(3) / 192, max_samples=400, t_stop=1e-2, occ_res=16,
+                  density_bias=2.0, occ_bits=synth.occupancy_pattern("sphere", 16))
+    case = G.make_case("tiny32", seed=seed, **kw)
+    of = O.OracleField(case.spec)
+    obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
+    ref = of.render_loss_grad(case.poses, case.pix, obs, case.intr, per_sample=True)
+    stats, _ = check_full(pn, case, obs, ref, of, backward=2 if seed % 2 else 0)
+    assert stats["samples"] == int(ref["march"][0][-1]) > 0
+
+
 def test_loss_grad_uniform_scanned_offsets(pn):
     """Uniform sampling over more rays than the write pass scans itself (96
     scan blocks of 256 rays, against 64): the counts known at ray set-up go
