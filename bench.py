@@ -195,8 +195,9 @@ def cpu_baseline(w, spec, gt, poses, pix_batches, budget_s):
 
 def calibrate(dev):
     """On-box reference rates, reported beside the published peaks: a 1 GiB
-    device-to-device copy (bytes read + written per second) and a large bf16
-    library GEMM (hipBLASLt through torch; 2 m n k flop per product)."""
+    device-to-device copy (bytes read + written per second), a large bf16
+    library GEMM (hipBLASLt through torch; 2 m n k flop per product), and
+    random 16-byte reads counted at the 128-byte line each one fetches."""
     import torch
     out = {}
     n = (1 << 30) // 4
@@ -223,6 +224,23 @@ def calibrate(dev):
     torch.cuda.synchronize()
     out["bf16_gemm_TFLOPs"] = 10 * 2 * m ** 3 / (time.perf_counter() - t0) / 1e12
     del a, b, c
+    # random 16-byte reads from a table of `mib` MiB (torch's indexing kernel):
+    # each touches its own 128-byte line, the encoding's pattern on its fine
+    # levels; reported as lines fetched per second x 128 B
+    n_idx = 1 << 24
+    for mib in (256, 1024):
+        table = torch.ones(mib * (1 << 20) // 16, 4, dtype=torch.float32, device=dev)
+        g = torch.Generator(device=dev).manual_seed(0)
+        idx = torch.randint(0, table.shape[0], (n_idx,), generator=g, device=dev)
+        for _ in range(2):
+            torch.index_select(table, 0, idx)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(10):
+            torch.index_select(table, 0, idx)
+        torch.cuda.synchronize()
+        out[f"random_line_read_{mib}MiB_TBps"] = 10 * n_idx * 128 / (time.perf_counter() - t0) / 1e12
+        del table, idx
     torch.cuda.empty_cache()
     return out
 
