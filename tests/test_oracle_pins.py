@@ -19,13 +19,19 @@ def tiny_spec(**kw):
 
 # ------------------------------------------------------------------ hashing
 # Vertex indices evaluated by hand from the spatial hash of the multiresolution
-# encoding: (i * 1) xor (j * 2654435761) xor (k * 805459861), uint32, mod T.
-HASH_PINS = {
-    12: {(0, 0, 0): 0, (1, 0, 0): 1, (0, 1, 0): 2481, (0, 0, 1): 1941, (1, 1, 1): 3621,
-         (3, 5, 7): 1381, (16, 16, 16): 592},
-    19: {(0, 1, 0): 489905, (0, 0, 1): 153493, (1, 1, 1): 339493, (3, 5, 7): 329061,
-         (16, 16, 16): 189008},
-}
+# encoding (tests/golden/hash_vertices.txt, which states the definition).
+def _hash_pins():
+    import os
+    pins = {}
+    path = os.path.join(os.path.dirname(__file__), "golden", "hash_vertices.txt")
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            log2T, i, j, k, h = (int(v) for v in line.split())
+            pins.setdefault(log2T, {})[(i, j, k)] = h
+    return pins
+
+
+HASH_PINS = _hash_pins()
 
 
 @pytest.mark.parametrize("log2T", [12, 19])

@@ -5,15 +5,40 @@ import pytest
 from paper_2210_10108_amd.driver import MCSchedule, PAPER_SCHEDULE
 
 
+def golden():
+    """tests/golden/schedule_sec4d.txt: name -> values."""
+    import os
+    out = {}
+    path = os.path.join(os.path.dirname(__file__), "golden", "schedule_sec4d.txt")
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            name, *vals = line.split()
+            out[name] = [float(v) for v in vals]
+    return out
+
+
 def test_paper_schedule_constants():
+    g = golden()
     s = PAPER_SCHEDULE
-    assert (s.n_hypotheses, s.s1, s.s2, s.rounds, s.keep_frac) == (64, 512, 512, 4, 0.25)
-    assert s.total_steps == 2560                      # s1 + S s2
+    assert (s.n_hypotheses, s.s1, s.s2, s.rounds, s.keep_frac) == (
+        g["hypotheses"][0], g["first_stage_steps"][0], g["stage_steps"][0],
+        g["resampling_rounds"][0], g["keep_fraction"][0])
+    assert s.total_steps == g["total_steps"][0]      # s1 + S s2
     rounds = {k: s.resample_round(k) for k in range(s.total_steps + 1) if s.resample_round(k)}
-    assert rounds == {512: 1, 1024: 2, 1536: 3, 2048: 4}
-    # r = 0.25 halved every round: 16, 8, 4 and 2 of the 64 hypotheses survive
+    assert sorted(rounds) == g["round_after_step"] and list(rounds.values()) == [1, 2, 3, 4]
+    # r halved every round: the kept counts of the fixture
     assert [s.keep_fraction(j) for j in (1, 2, 3, 4)] == [0.25, 0.125, 0.0625, 0.03125]
-    assert [s.n_keep(j) for j in (1, 2, 3, 4)] == [16, 8, 4, 2]
+    assert [s.n_keep(j) for j in (1, 2, 3, 4)] == g["kept"]
+
+
+def test_paper_learning_rates():
+    from paper_2210_10108_amd.pnerf import AdamParams
+    g = golden()
+    a = AdamParams()
+    assert a.lr_rot == pytest.approx(g["lr_rotation"][0])
+    assert a.lr_trans == pytest.approx(g["lr_translation"][0])
+    assert a.decay_base == pytest.approx(g["lr_decay_base"][0])
+    assert a.decay_steps == g["lr_decay_steps"][0]
 
 
 def test_schedule_edges():
