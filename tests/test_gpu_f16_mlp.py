@@ -192,3 +192,21 @@ def test_f16_render_colour(pn, name, K, P):
     err = np.abs(rgb.cpu().numpy() - ref).max()
     sys.stderr.write(f"[f16] {name} colour: max abs error {err:.3g}\n")
     assert err <= G.COLOR_ATOL
+
+
+@pytest.mark.parametrize("name,hyps", [("cam640_f16_occ128", [0, 255]), ("large4m_occ256", [0, 1023])])
+def test_f16_render_colour_full_batch_sampled_hypotheses(pn, name, hyps):
+    """pnerf_render with the fp16 networks over a whole workload batch (chunked as
+    the library decides): colour within 2e-3 on the sampled hypotheses."""
+    import torch
+    from tests.test_gpu_parity import workload_case
+    case = workload_case(name)
+    f = pn.Field(case.spec, mlp_precision=1)
+    rgb = f.render(G.to_dev(case.poses), G.to_dev(case.pix), case.intr)
+    torch.cuda.synchronize()
+    got = rgb.cpu().numpy()
+    f.close()
+    ref = O.OracleField(case.spec).render(case.poses[hyps], case.pix[hyps], case.intr)
+    err = np.abs(got[hyps] - ref).max()
+    sys.stderr.write(f"[f16] {name} colour: max abs error {err:.3g}\n")
+    assert err <= G.COLOR_ATOL
