@@ -424,8 +424,9 @@ def test_loss_grad_device_sized_matches_host_planned(pn):
     assert np.array_equal(l1, l2) and np.array_equal(g1, g2)
 
 
-@pytest.mark.parametrize("chunks,backward", [(2, 0), (4, 0), (7, 0), (3, 1)])
-def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks, backward):
+@pytest.mark.parametrize("chunks,backward,mlp_precision", [(2, 0, 0), (4, 0, 0), (7, 0, 0), (3, 1, 0),
+                                                           (3, 0, 1)])
+def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks, backward, mlp_precision):
     # the pipelined loss gradient (encoding of one chunk alongside the networks
     # of the previous, two streams and sample buffers) gives the same bits as
     # one chunk on the caller's stream: per-sample work does not depend on the
@@ -436,7 +437,7 @@ def test_loss_grad_overlapped_chunks_match_one_chunk(pn, chunks, backward):
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
     out = []
     for oc in (1, chunks):
-        f = pn.Field(case.spec, overlap_chunks=oc, backward=backward)
+        f = pn.Field(case.spec, overlap_chunks=oc, backward=backward, mlp_precision=mlp_precision)
         loss, dpose = f.render_loss_grad(G.to_dev(case.poses), G.to_dev(case.pix), G.to_dev(obs),
                                          case.intr)
         torch.cuda.synchronize()
