@@ -638,11 +638,11 @@ def test_loss_grad_ngp800_bump_full_batch_sampled_hypotheses(pn):
 
 
 # ------------------------------------- full-size workloads: colour, per sample
-def workload_case(name):
+def workload_case(name, seed=0):
     """The workload's full batch (fp16 storage where the workload says so) with
     the oracle's density-built occupancy grid."""
     w = synth.WORKLOADS[name]
-    case = f16_case(name) if w.param_dtype == "f16" else G.make_case(name)
+    case = f16_case(name, seed=seed) if w.param_dtype == "f16" else G.make_case(name, seed=seed)
     return with_oracle_occupancy(case, w.occ_res, w.occ_threshold)
 
 
@@ -669,15 +669,16 @@ def test_render_colour_full_batch_sampled_hypotheses(pn, name, hyps):
     assert ref.max() > 0.05
 
 
-@pytest.mark.parametrize("name,hyps,backward", [("cam640_f16_occ128", [3, 200], 0),
-                                                ("large4m_occ256", [5, 700], 0),
-                                                ("large4m_occ256", [5, 700], 2)])
-def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps, backward):
+@pytest.mark.parametrize("name,hyps,backward,seed", [("cam640_f16_occ128", [3, 200], 0, 0),
+                                                     ("large4m_occ256", [5, 700], 0, 0),
+                                                     ("large4m_occ256", [5, 700], 2, 0),
+                                                     ("large4m_occ256", [11, 512], 0, 1)])
+def test_loss_grad_sampled_hypotheses_per_sample(pn, name, hyps, backward, seed):
     """The sampled hypotheses of a full-size workload as a batch of their own
     (one chunk, so every sample can be inspected): per-hypothesis sample counts
     exactly, per-sample torque and force shares and the stage values d loss /
     d h0 and d loss / d z, loss and pose gradient (Eq. 2, Eq. 3)."""
-    full = workload_case(name)
+    full = workload_case(name, seed)
     case = dataclasses.replace(full, poses=full.poses[hyps], pix=full.pix[hyps])
     of = O.OracleField(case.spec)
     obs = G.oracle_observation(of, case.gt, case.pix, case.intr)
