@@ -134,7 +134,13 @@ def intrinsics(d) -> Intrinsics:
 
 
 class Field:
-    """A frozen field on the current device (wraps pnerf_create_field)."""
+    """A frozen field on the current device (wraps pnerf_create_field).
+
+    spec: a synth.FieldSpec (table, weights, marching, loss).  The keyword
+    arguments are the pnerf_field_params fields of the same names:
+    max_workspace_bytes (0: the library's default budget), overlap_chunks,
+    backward (0 separate kernels, 1 fused per-ray kernel, 2 fused keeping the
+    per-sample intermediates) and mlp_precision (0 split-bf16, 1 fp16 MFMA)."""
 
     def __init__(self, spec, stream=None, max_workspace_bytes: int = 0, overlap_chunks: int = 0,
                  backward: int = 0, mlp_precision: int = 0):
